@@ -1,0 +1,281 @@
+"""Pins for the CPU oracle: checks against facts fixed outside the oracle itself.
+
+Each test ties the oracle to something other than its own formulas: a library routine
+(torch's scaled-dot-product attention, softmax, logsumexp; Python's sort), a closed
+form, an invariant the paper's definitions imply, or a brute force on tiny inputs.
+They are chosen so that a plausible slip in the oracle -- a dropped 1/sqrt(d), a wrong
+sign, a transposed operand, the LSE taken over the wrong context, a tie broken the wrong
+way, an append in the wrong order -- fails at least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_23286_amd import synth
+
+
+def rand_bf16(rng, shape, scale=1.0):
+    return synth.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32) * scale)
+
+
+def f64(b):
+    return synth.bf16_bits_to_f32(b).astype(np.float64)
+
+
+def full_context(K, V, memK, memV, mem_len):
+    """Context rows per head [H, C, d] in fp64: memory rows first, then the frame."""
+    kc = [f64(memK[:, :mem_len])] if mem_len else []
+    vc = [f64(memV[:, :mem_len])] if mem_len else []
+    kc.append(f64(K).transpose(1, 0, 2))
+    vc.append(f64(V).transpose(1, 0, 2))
+    return np.concatenate(kc, axis=1), np.concatenate(vc, axis=1)
+
+
+CASES = [  # (n_tokens, n_heads, head_dim, mem_len, logit scale)
+    (1, 1, 16, 0, 1.0),
+    (7, 2, 16, 3, 1.0),
+    (37, 3, 64, 50, 1.0),
+    (64, 2, 64, 0, 0.125),
+    (20, 2, 64, 130, 3.0),    # large logits: the max-subtraction matters
+]
+
+
+@pytest.mark.parametrize("n,H,d,M,scale", CASES)
+def test_attend_matches_torch_sdpa_and_logsumexp(n, H, d, M, scale):
+    """O against torch's SDPA (fp64, CPU) and LSE against torch.logsumexp of a
+    torch.matmul logit matrix: two library routines, not the oracle's loops."""
+    rng = np.random.default_rng(n * 1000 + M)
+    Q, K, V = (rand_bf16(rng, (n, H, d), scale) for _ in range(3))
+    memK = rand_bf16(rng, (H, M + 5, d), scale)
+    memV = rand_bf16(rng, (H, M + 5, d))
+    out, lse = oracle.attend(Q, K, V, memK, memV, M)
+
+    kc, vc = full_context(K, V, memK, memV, M)
+    q = torch.from_numpy(f64(Q).transpose(1, 0, 2).copy())          # [H, n, d]
+    k = torch.from_numpy(kc)
+    v = torch.from_numpy(vc)
+    ref = torch.nn.functional.scaled_dot_product_attention(q, k, v)  # [H, n, d]
+    np.testing.assert_allclose(out.transpose(1, 0, 2), ref.numpy(), rtol=0, atol=1e-12)
+    z = torch.matmul(q, k.transpose(1, 2).contiguous()) / math.sqrt(d)
+    np.testing.assert_allclose(lse, torch.logsumexp(z, dim=-1).numpy(), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("n,H,d,M,scale", CASES)
+def test_saliency_matches_materialised_softmax(n, H, d, M, scale):
+    """LSE-saliency (Sec. 3.3) equals the column sums of the materialised softmax map
+    (torch.softmax over the full context), restricted to the sampled queries and the
+    frame's key columns -- the exactness the paper claims for the LSE route."""
+    rng = np.random.default_rng(7 + n + M)
+    Q, K, V = (rand_bf16(rng, (n, H, d), scale) for _ in range(3))
+    memK = rand_bf16(rng, (H, max(M, 1), d), scale)
+    memV = rand_bf16(rng, (H, max(M, 1), d))
+    _, lse = oracle.attend(Q, K, V, memK, memV, M)
+    qidx = np.arange(0, n, 3, dtype=np.int32)
+    sal = oracle.saliency(Q, K, lse, qidx)
+
+    kc, _ = full_context(K, V, memK, memV, M)
+    q = torch.from_numpy(f64(Q).transpose(1, 0, 2).copy())
+    A = torch.softmax(torch.matmul(q, torch.from_numpy(kc).transpose(1, 2).contiguous())
+                      / math.sqrt(d), dim=-1)                       # [H, n, C]
+    ref = A[:, qidx, M:].sum(dim=1).numpy()                         # frame columns only
+    np.testing.assert_allclose(sal, ref, rtol=1e-12, atol=1e-15)
+
+
+def test_each_attention_row_sums_to_one():
+    """I1: for every query, the attention it spreads over memory + frame is 1, so the
+    column masses over all context columns from one query add to exactly one."""
+    rng = np.random.default_rng(11)
+    n, H, d, M = 29, 2, 64, 40
+    Q, K, V = (rand_bf16(rng, (n, H, d)) for _ in range(3))
+    memK, memV = rand_bf16(rng, (H, M, d)), rand_bf16(rng, (H, M, d))
+    _, lse = oracle.attend(Q, K, V, memK, memV, M)
+    for i in (0, 13, 28):
+        qi = np.array([i], dtype=np.int32)
+        s_cur = oracle.column_mass(Q, qi, lse[:, qi], K, "frame")
+        s_mem = oracle.column_mass(Q, qi, lse[:, qi], memK, "memory")
+        np.testing.assert_allclose(s_cur.sum(1) + s_mem.sum(1), 1.0, rtol=0, atol=1e-13)
+
+
+def test_total_saliency_equals_query_count():
+    """I2: with an empty memory and every query sampled (stride 1, no specials), the
+    saliency of the frame's keys sums to the number of queries, N."""
+    rng = np.random.default_rng(5)
+    gh, gw = 6, 7
+    n, H, d = gh * gw, 3, 64
+    Q, K, V = (rand_bf16(rng, (n, H, d), 2.0) for _ in range(3))
+    _, lse = oracle.attend(Q, K, V)
+    qidx = oracle.qsub_index(gh, gw, 0, 1)
+    assert len(qidx) == n
+    sal = oracle.saliency(Q, K, lse, qidx)
+    np.testing.assert_allclose(sal.sum(axis=1), n, rtol=1e-13)
+
+
+def test_zero_queries_closed_form():
+    """C-a: Q = 0 makes every logit 0, so A = 1/C, o = mean of V over the context,
+    LSE = log C, S_j = n_q / C, and the top-k is the lowest indices (all tied)."""
+    rng = np.random.default_rng(3)
+    n, H, d, M = 33, 2, 64, 17
+    Q = np.zeros((n, H, d), dtype=np.uint16)
+    K, V = rand_bf16(rng, (n, H, d)), rand_bf16(rng, (n, H, d))
+    memK, memV = rand_bf16(rng, (H, M, d)), rand_bf16(rng, (H, M, d))
+    out, lse = oracle.attend(Q, K, V, memK, memV, M)
+    C = M + n
+    _, vc = full_context(K, V, memK, memV, M)
+    np.testing.assert_allclose(out, np.broadcast_to(vc.mean(axis=1), (n, H, d)), atol=1e-14)
+    np.testing.assert_allclose(lse, math.log(C), rtol=0, atol=1e-14)
+    qidx = np.arange(0, n, 4, dtype=np.int32)
+    sal = oracle.saliency(Q, K, lse, qidx)
+    np.testing.assert_allclose(sal, len(qidx) / C, rtol=1e-14)
+    idx = oracle.topk(sal, 5)
+    assert (idx == np.arange(5)).all()
+
+
+def test_one_dominant_key_takes_all_mass():
+    """C-c: a key along the queries' mean direction with a huge norm collects almost
+    all attention: S_j* -> n_q and o_i -> v_j*."""
+    rng = np.random.default_rng(9)
+    n, H, d = 40, 1, 64
+    Q = synth.f32_to_bf16_bits(np.abs(rng.standard_normal((n, H, d))).astype(np.float32))
+    K, V = rand_bf16(rng, (n, H, d), 0.01), rand_bf16(rng, (n, H, d))
+    jstar = 17
+    K[jstar, 0] = synth.f32_to_bf16_bits(np.full(d, 8.0, dtype=np.float32))
+    out, lse = oracle.attend(Q, K, V)
+    qidx = np.arange(0, n, 2, dtype=np.int32)
+    sal = oracle.saliency(Q, K, lse, qidx)
+    assert sal[0, jstar] == pytest.approx(len(qidx), rel=1e-6)
+    np.testing.assert_allclose(out[:, 0], np.broadcast_to(f64(V[jstar, 0]), (n, d)), atol=1e-6)
+    assert oracle.topk(sal, 1)[0, 0] == jstar
+
+
+def test_duplicate_keys_lowest_index_wins():
+    """C-b: two identical dominant key rows j1 < j2 tie exactly; top-1 must be j1, and
+    with budget 2 both are taken, in ascending order."""
+    rng = np.random.default_rng(2)
+    n, H, d = 50, 2, 64
+    Q = synth.f32_to_bf16_bits(np.abs(rng.standard_normal((n, H, d))).astype(np.float32) * 0.2)
+    K, V = rand_bf16(rng, (n, H, d), 0.05), rand_bf16(rng, (n, H, d))
+    for h, (j1, j2) in enumerate([(11, 30), (3, 49)]):
+        row = synth.f32_to_bf16_bits(np.full(d, 0.5, dtype=np.float32))
+        K[j1, h] = row
+        K[j2, h] = row
+    _, lse = oracle.attend(Q, K, V)
+    sal = oracle.saliency(Q, K, lse, np.arange(n, dtype=np.int32))
+    assert sal[0, 11] == sal[0, 30] and sal[1, 3] == sal[1, 49]
+    assert oracle.topk(sal, 1)[:, 0].tolist() == [11, 3]
+    assert oracle.topk(sal, 2).tolist() == [[11, 30], [3, 49]]
+
+
+def test_memory_row_order_does_not_matter():
+    """I6: attention is a sum over the context, so permuting memory rows leaves
+    O, LSE and S unchanged (to rounding)."""
+    rng = np.random.default_rng(4)
+    n, H, d, M = 25, 2, 64, 31
+    Q, K, V = (rand_bf16(rng, (n, H, d)) for _ in range(3))
+    memK, memV = rand_bf16(rng, (H, M, d)), rand_bf16(rng, (H, M, d))
+    perm = rng.permutation(M)
+    o1, l1 = oracle.attend(Q, K, V, memK, memV, M)
+    o2, l2 = oracle.attend(Q, K, V, memK[:, perm].copy(), memV[:, perm].copy(), M)
+    np.testing.assert_allclose(o1, o2, atol=1e-14)
+    np.testing.assert_allclose(l1, l2, atol=1e-13)
+    qidx = np.arange(0, n, 2, dtype=np.int32)
+    np.testing.assert_allclose(oracle.saliency(Q, K, l1, qidx), oracle.saliency(Q, K, l2, qidx),
+                               rtol=1e-13)
+
+
+def test_rows_subset_equals_full():
+    """Computing selected query rows only gives exactly the full computation's rows."""
+    rng = np.random.default_rng(6)
+    n, H, d, M = 45, 2, 64, 12
+    Q, K, V = (rand_bf16(rng, (n, H, d)) for _ in range(3))
+    memK, memV = rand_bf16(rng, (H, M, d)), rand_bf16(rng, (H, M, d))
+    o, l = oracle.attend(Q, K, V, memK, memV, M)
+    rows = np.array([44, 0, 17], dtype=np.int32)
+    os_, ls = oracle.attend(Q, K, V, memK, memV, M, rows=rows)
+    assert (os_ == o[rows]).all() and (ls == l[:, rows]).all()
+
+
+@pytest.mark.parametrize("n,budget", [(1, 0), (1, 1), (10, 3), (64, 1), (257, 10), (300, 300)])
+def test_topk_matches_python_sort(n, budget):
+    """Top-k against Python's sorted() on (-S, j), with many exact ties drawn from a
+    small value set so the tie-break is exercised."""
+    rng = np.random.default_rng(n + budget)
+    H = 3
+    sal = rng.integers(0, 7, size=(H, n)).astype(np.float64) / 7.0
+    idx = oracle.topk(sal, budget)
+    for h in range(H):
+        ref = sorted(range(n), key=lambda j: (-sal[h, j], j))[:budget]
+        assert idx[h].tolist() == sorted(ref)
+
+
+def test_topk_rejects_bad_budget():
+    with pytest.raises(ValueError):
+        oracle.topk(np.zeros((1, 4)), 5)
+    with pytest.raises(ValueError):
+        oracle.topk(np.zeros((1, 4)), -1)
+
+
+def test_qsub_index_small_grids():
+    """Sec. 3.3: top-left query of each 2x2 window, specials first (reading: specials
+    are not in the sampled set, partial edge windows are kept).  Expected values are
+    written out by hand for small grids."""
+    assert oracle.qsub_index(4, 4, 0, 2).tolist() == [0, 2, 8, 10]
+    assert oracle.qsub_index(3, 5, 1, 2).tolist() == [1, 3, 5, 11, 13, 15]
+    assert oracle.qsub_index(2, 3, 0, 1).tolist() == [0, 1, 2, 3, 4, 5]
+    assert oracle.qsub_index(5, 5, 0, 3).tolist() == [0, 3, 15, 18]
+    assert oracle.qsub_index(1, 1, 5, 2).tolist() == [5]
+    # workload grids: ceil(28/2)*ceil(37/2), ceil(37/2)^2, 8x8/4
+    assert len(oracle.qsub_index(28, 37, 5, 2)) == 14 * 19 == 266
+    assert len(oracle.qsub_index(37, 37, 5, 2)) == 19 * 19 == 361
+    assert len(oracle.qsub_index(8, 8, 0, 2)) == 16
+
+
+def test_append_copies_rows_in_index_order():
+    """Eq. 6: the selected rows land after the existing memory, in ascending token order,
+    as exact copies; rows already in memory are untouched."""
+    rng = np.random.default_rng(8)
+    n, H, d = 12, 2, 16
+    K, V = rand_bf16(rng, (n, H, d)), rand_bf16(rng, (n, H, d))
+    mem = oracle.Memory(H, d, 10)
+    mem.append(K, V, np.array([[1, 5], [0, 11]], dtype=np.int32))
+    before = mem.K[:, :2].copy()
+    mem.append(K, V, np.array([[2, 3], [4, 7]], dtype=np.int32))
+    assert mem.len == 4
+    assert (mem.K[:, :2] == before).all()
+    assert (mem.K[0, :4] == K[[1, 5, 2, 3], 0]).all()
+    assert (mem.V[1, :4] == V[[0, 11, 4, 7], 1]).all()
+    assert (mem.K[:, 4:] == 0).all()
+
+
+@pytest.mark.parametrize("anchor", [False, True])
+def test_memory_growth_formula(anchor):
+    """I4/I5 (Sec. 3.3 Eq. 4 and 6): |M_t| = |M_1| + (t-1) k; each non-anchor frame
+    admits exactly k <= ceil(1% N) tokens per head; the anchor frame admits all N."""
+    cfg = synth.CONFIGS["tiny"]
+    n, k, T = cfg.n_tokens, cfg.budget, cfg.n_frames
+    qidx = oracle.qsub_index(cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
+    mem = oracle.Memory(cfg.n_heads, cfg.head_dim, n + T * k)
+    for t in range(T):
+        Q, K, V = synth.frame_qkv(cfg, 0, t)
+        budget = n if (anchor and t == 0) else k
+        r = oracle.step(mem, Q, K, V, qidx, budget)
+        assert r["idx"].shape == (cfg.n_heads, budget)
+        if not (anchor and t == 0):
+            assert budget <= math.ceil(0.01 * n)
+    first = n if anchor else k
+    assert mem.len == first + (T - 1) * k
+
+
+def test_planted_keys_are_admitted():
+    """I7 (statistical sanity of the synthetic stream + oracle together): on a one-layer
+    ViT-L-shaped frame, per-head top-10 recovers the 10 planted salient keys."""
+    cfg = synth.CONFIGS["vitl_layer"]
+    Q, K, V = synth.frame_qkv(cfg, 0, 0)
+    _, lse = oracle.attend(Q, K, V)
+    qidx = oracle.qsub_index(cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
+    idx = oracle.topk(oracle.saliency(Q, K, lse, qidx), cfg.budget)
+    pos = synth.plant_positions(cfg.seed, 0, 0, cfg.n_heads, cfg.n_tokens, cfg.n_plant)
+    hits = sum(len(set(idx[h]) & set(pos[h])) for h in range(cfg.n_heads))
+    assert hits >= 0.95 * cfg.n_heads * cfg.n_plant
