@@ -1,0 +1,236 @@
+"""Throughput of RegVGGT's per-frame hot path on one MI355X.
+
+Workload: the 24-layer ViT-L-shaped stream (16 heads x 64, 1041 tokens per frame =
+28x37 patches + 5 special tokens, budget 10 tokens per head per frame, 2x2 query
+sampling), 1000 frames, memory starting empty and growing to 9,990 rows per
+(layer, head).  One step = one frame: for each of the 24 layers, attention of the
+frame over that layer's memory with per-query LSE (rv_attend_frame), then one deferred
+launch that computes every layer's LSE-saliency, selects each head's top 10 and appends
+them (rv_admit_layers).
+
+Every frame's Q/K/V (distinct per layer and frame, seeded) is generated on the GPU and
+resident in HBM before timing starts (153 MB per frame).  The timed region covers the
+steps only, between device synchronisations.  HIP events on the compute stream
+bracket each frame's attention launches and its admission launch; they give the
+attention kernel's average duration, from which the roofline fraction is computed.
+The oracle is timed on the host on a bounded sample (one layer of the frame whose
+context equals the stream's mean context) and extrapolated to frames/s.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def attention_flops(N, H, d, ctx):
+    """Algorithmic flops of one attention launch: 2*d (Q.K) + 2*d (P.V) per
+    (head, query, context key) pair."""
+    return 4.0 * d * H * N * ctx
+
+
+def admit_bytes(N, H, d, n_q, k):
+    """Algorithmic HBM bytes of the saliency + top-k + append phase for one layer."""
+    return (n_q * H * d * 2          # sampled query rows
+            + N * H * d * 2          # the frame's keys
+            + n_q * H * 4            # LSE of the sampled queries
+            + N * H * 4 * 2          # saliency written, then read by the selection
+            + 2 * k * H * d * 2 * 2  # K and V rows read and appended
+            + k * H * 8)             # provenance
+
+
+def cpu_baseline(cfg, mean_ctx, n_frames):
+    """Time the oracle on one layer of the frame whose context is the stream mean."""
+    import numpy as np
+    import oracle
+    from paper_2609_23286_amd import synth
+    N, H, k = cfg.n_tokens, cfg.n_heads, cfg.budget
+    t_mid = int(round((mean_ctx - N) / k))
+    M = t_mid * k
+    Q, K, V = synth.frame_qkv(cfg, 0, t_mid)
+    memK, memV = synth.memory_prefill(cfg, 0, M, M + k)
+    qidx = oracle.qsub_index(cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
+    omem = oracle.Memory(H, cfg.head_dim, M + k)
+    omem.K[:], omem.V[:] = memK, memV
+    omem.len = M
+    t0 = time.perf_counter()
+    oracle.step(omem, Q, K, V, qidx, k)
+    dt = time.perf_counter() - t0
+    per_frame = dt * cfg.n_layers * (mean_ctx / (M + N))
+    return {"value": 1.0 / per_frame, "unit": "frames/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": (f"one layer (16 heads, all {N} queries, saliency, top-{k}, append) of frame "
+                       f"{t_mid} (context {M + N}), {dt:.2f} s, scaled x{cfg.n_layers} layers and "
+                       f"to the {n_frames}-frame mean context {mean_ctx:.0f}")}
+
+
+def main():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=1000, help="frames timed (from an empty memory)")
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--config", default="vitl_stack_1000")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    args = p.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this path has no multi-GPU mode "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_23286_amd import rv, synth
+
+    cfg = synth.CONFIGS[args.config]
+    L, H, N, d, k = cfg.n_layers, cfg.n_heads, cfg.n_tokens, cfg.head_dim, cfg.budget
+    T, W = args.steps, args.warmup
+    qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
+    n_q = len(range(0, cfg.grid_h, cfg.stride)) * len(range(0, cfg.grid_w, cfg.stride))
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    frame_bytes = L * 3 * N * H * d * 2
+    free, total = torch.cuda.mem_get_info()
+    log(f"{cfg.name}: L={L} H={H} N={N} k={k} frames={T}; inputs {T * frame_bytes / 1e9:.1f} GB, "
+        f"device free {free / 1e9:.1f} of {total / 1e9:.1f} GB")
+    if T * frame_bytes > free - 8e9:
+        raise SystemExit("not enough device memory to keep every frame's inputs resident")
+
+    # ---- inputs: every frame resident in HBM --------------------------------------
+    t0 = time.perf_counter()
+    frames = []
+    for t in range(T):
+        buf = torch.empty((L, 3, N, H, d), dtype=torch.int16, device=dev)
+        rv.gpu_frame_qkv(cfg, t, buf)
+        frames.append(buf)
+    torch.cuda.synchronize()
+    log(f"generated {T} frames in {time.perf_counter() - t0:.1f} s")
+
+    cap = T * k + 64
+    mems = [rv.Memory(H, reserve_tokens=cap, max_tokens=cap) for _ in range(L)]
+    rv.reserve_workspace(N, H, L)
+    out = torch.empty((L, N, H, d), dtype=torch.int16, device=dev)
+    lse = torch.empty((L, H, N), dtype=torch.float32, device=dev)
+    sal = torch.empty((L, H, N), dtype=torch.float32, device=dev)
+
+    # Raw C calls with pre-marshalled arguments keep the host ahead of the GPU.
+    import ctypes
+    lib = rv.lib()
+    vp = ctypes.c_void_p
+    s_h = vp(stream.cuda_stream)
+    q = rv.rv_qsub(*qs)
+    qref = ctypes.byref(q)
+    arr = vp * L
+    out_p = [vp(out[l].data_ptr()) for l in range(L)]
+    lse_p = [vp(lse[l].data_ptr()) for l in range(L)]
+    sal_arr = arr(*[sal[l].data_ptr() for l in range(L)])
+    lse_arr = arr(*[lse[l].data_ptr() for l in range(L)])
+    mem_arr = arr(*[m.handle.value for m in mems])
+    views = [m.view() for m in mems]  # capacity is reserved: arenas never move
+    frame_ptrs = []
+    for t in range(T):
+        fb = frames[t]
+        qp = [fb[l, 0].data_ptr() for l in range(L)]
+        kp = [fb[l, 1].data_ptr() for l in range(L)]
+        vpp = [fb[l, 2].data_ptr() for l in range(L)]
+        frame_ptrs.append((qp, kp, vpp, arr(*qp), arr(*kp), arr(*vpp)))
+
+    def run_frame(t, ev=None):
+        qp, kp, vpp, qa, ka, va = frame_ptrs[t]
+        if ev is not None:
+            ev[0].record(stream)
+        for l in range(L):
+            mk, mv, hs = views[l]
+            st = lib.rv_attend_frame(vp(qp[l]), vp(kp[l]), vp(vpp[l]), N, vp(mk), vp(mv),
+                                     lib.rv_mem_len(mems[l].handle), hs, H, d, None, out_p[l], lse_p[l],
+                                     None, s_h)
+            if st:
+                raise rv.RVError(st, lib.rv_last_error().decode())
+        if ev is not None:
+            ev[1].record(stream)
+        st = lib.rv_admit_layers(L, qa, ka, va, lse_arr, N, qref, k, mem_arr, t, sal_arr, None, s_h)
+        if st:
+            raise rv.RVError(st, lib.rv_last_error().decode())
+        if ev is not None:
+            ev[2].record(stream)
+
+    # ---- warmup on frames 0..W-1, then start the stream again from empty memory -----
+    for t in range(min(W, T)):
+        run_frame(t)
+    torch.cuda.synchronize()
+    for m in mems:
+        m.reset()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(T)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for t in range(T):
+        run_frame(t, events[t])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    assert all(m.len == T * k for m in mems)
+
+    attn_ms = sum(e[0].elapsed_time(e[1]) for e in events)
+    admit_ms = sum(e[1].elapsed_time(e[2]) for e in events)
+    ctx = [t * k + N for t in range(T)]
+    flops = sum(attention_flops(N, H, d, c) for c in ctx) * L
+    n_attn = T * L
+    attn_avg_s = attn_ms / 1e3 / n_attn
+    achieved_tf = flops / n_attn / attn_avg_s / 1e12
+    bytes_admit = admit_bytes(N, H, d, n_q, k) * L * T
+    admit_gbs = bytes_admit / (admit_ms / 1e3) / 1e9
+    log(f"timed {T} frames in {elapsed:.3f} s: attention {attn_ms:.1f} ms "
+        f"({attn_avg_s * 1e6:.1f} us/launch, {achieved_tf:.1f} TFLOP/s), admission {admit_ms:.1f} ms "
+        f"({admit_ms / T * 1e3:.1f} us/frame, {admit_gbs:.0f} GB/s)")
+
+    mean_ctx = sum(ctx) / T
+    result = {
+        "metric": "frames/sec (attend+saliency+admit, 24 layers) at 1000-frame stream",
+        "value": T / elapsed,
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": T,
+        "warmup": W,
+        "ms_per_step": elapsed / T * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Philox streams of ViT-L token shape, 1% planted salient keys)",
+        "config": {"workload": f"{cfg.name}: {L} layers x {H} heads x {d}, {N} tokens/frame "
+                               f"({cfg.grid_h}x{cfg.grid_w} patches + {cfg.n_special} special), "
+                               f"budget {k}/head/frame, 2x2 query sampling, {T}-frame stream from empty memory",
+                   "layers": L, "heads": H, "head_dim": d, "tokens_per_frame": N, "budget": k,
+                   "frames": T, "sampled_queries": n_q},
+        "roofline": {"kernel": "attn_fwd_kernel", "bound": "mfma", "achieved": achieved_tf,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved_tf / PEAK_BF16_TFLOPS,
+                     "traffic": None, "avg_launch_us": attn_avg_s * 1e6,
+                     "algorithmic_flops_per_launch": flops / n_attn},
+        "phases": {"attention_ms": attn_ms, "admission_ms": admit_ms,
+                   "admission_roofline": {"kernel": "admit_kernel", "bound": "hbm", "achieved": admit_gbs,
+                                          "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                          "frac": admit_gbs / PEAK_HBM_GBS,
+                                          "algorithmic_bytes_per_launch": bytes_admit / T}},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a host sample ...")
+        result["cpu_baseline"] = cpu_baseline(cfg, mean_ctx, T)
+    for m in mems:
+        m.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,173 @@
+/*
+ * rv.h -- C ABI of librv, the MI355X (gfx950) library for RegVGGT's per-frame hot path.
+ *
+ * For each transformer layer, one incoming frame of N tokens is
+ *   1. attended over that layer's regulated KV memory plus its own tokens
+ *      (temporal-causal attention, Sec. 3.1 Eq. 2-3), keeping each query's
+ *      log-sum-exp (Sec. 3.3, LSE equation);
+ *   2. scored: each key of the frame gets the attention mass it receives from a 2x2
+ *      spatially sampled subset of the frame's queries, recovered from the LSE without
+ *      forming any score matrix (Sec. 3.3, saliency score and the A_ij equation);
+ *   3. regulated: per head, the `budget` most salient tokens are appended to the memory
+ *      (Sec. 3.3 Eq. 6; budget = floor(gamma * N), gamma = 0.01 in the paper).
+ *
+ * General conventions
+ *   - Every tensor pointer named in a compute call is a DEVICE pointer on the current
+ *     HIP device, owned by the caller, unless stated otherwise.
+ *   - bf16 means IEEE-754 binary32 truncated to its upper 16 bits (bfloat16), stored
+ *     as 2-byte little-endian words.
+ *   - Frame tensors Q, K, V, out: [n_tokens][n_heads][head_dim] bf16, contiguous (the
+ *     layout a fused QKV projection writes).  Per-head vectors (lse, saliency):
+ *     [n_heads][n_tokens] fp32.  Memory: [n_heads][head_stride][head_dim] bf16, rows
+ *     0..mem_len-1 of each head valid.
+ *   - head_dim must be 64 (the ViT-L aggregator's 1024 / 16).
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream) and is
+ *     asynchronous; nothing here synchronises the device except where stated.
+ *   - Every argument is checked before anything is enqueued.  On failure the call
+ *     returns a non-zero rv_status, enqueues nothing, changes no state, and
+ *     rv_last_error() describes the problem.  A fault in an earlier kernel surfaces as
+ *     RV_ERR_HIP from the next call that reaches the HIP runtime.
+ *   - Calls that share an rv_mem, or that run concurrently on one device, must be
+ *     ordered on one stream: the library's scratch workspace is shared per device.
+ *   - The library never aborts the process.
+ */
+#ifndef RV_H
+#define RV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rv_status {
+    RV_OK = 0,
+    RV_ERR_INVALID = 1,  /* bad argument: null pointer, size, unsupported shape */
+    RV_ERR_OOM = 2,      /* a device allocation failed; state unchanged */
+    RV_ERR_CAPACITY = 3, /* memory growth would exceed the rv_mem's max_tokens */
+    RV_ERR_HIP = 4       /* the HIP runtime reported an error */
+} rv_status;
+
+/* One layer's regulated KV memory ("context memory" M_t of Sec. 3.3 Eq. 4-6): K and V
+ * arenas [n_heads][capacity][head_dim] bf16, a provenance record per row
+ * [n_heads][capacity][2] int32 = (frame_id, token index in that frame), and the number
+ * of valid rows, which is the same for every head because every head admits exactly
+ * `budget` rows per frame (Eq. 6).  The library owns all of it. */
+typedef struct rv_mem_s *rv_mem;
+
+/* Query subset for the saliency score (Sec. 3.3, head-specific retention): the frame is
+ * n_special leading special tokens (camera, register) followed by a grid_h x grid_w
+ * patch grid in row-major order.  The grid is cut into stride x stride windows and the
+ * top-left patch of each window is a sampled query; windows cut by the right or bottom
+ * edge count too.  Special tokens are never sampled (they are still scored and may be
+ * admitted).  stride 2 is the paper's setting; stride 1 samples every patch. */
+typedef struct rv_qsub {
+    int32_t grid_h, grid_w, n_special, stride;
+} rv_qsub;
+
+/* Human-readable description of the last failure on the calling thread.  The pointer
+ * stays valid until the next rv_* call on that thread. */
+const char *rv_last_error(void);
+
+/* Library version string. */
+const char *rv_version(void);
+
+/* ---- memory (Sec. 3.3 Eq. 4-6) ---------------------------------------------------- */
+
+/* Creates an empty memory on the current device with room for reserve_tokens rows per
+ * head (0 allowed) that may grow to max_tokens rows per head.  head_dim must be 64. */
+rv_status rv_mem_create(int n_heads, int head_dim, int64_t reserve_tokens, int64_t max_tokens,
+                        rv_mem *out);
+
+/* Frees the memory (synchronises its device first).  NULL is accepted. */
+rv_status rv_mem_destroy(rv_mem m);
+
+/* Number of valid rows per head, as enqueued (a host-side mirror; no device sync). */
+int64_t rv_mem_len(rv_mem m);
+
+/* Rows per head currently allocated. */
+int64_t rv_mem_capacity(rv_mem m);
+
+/* Device pointers of the K and V arenas and the row stride between heads (in tokens),
+ * suitable for rv_attend_frame.  Growth (in rv_admit*, rv_mem_reserve) moves the
+ * arenas: take a fresh view after any call that may grow the memory. */
+rv_status rv_mem_view(rv_mem m, const void **memK, const void **memV,
+                      int64_t *head_stride_tokens);
+
+/* Ensures capacity >= tokens (<= max_tokens).  Growth allocates new arenas, copies the
+ * valid rows on `stream` and then synchronises `stream` before freeing the old ones. */
+rv_status rv_mem_reserve(rv_mem m, int64_t tokens, void *stream);
+
+/* Sets the length to 0 (arena contents are left as they are). */
+rv_status rv_mem_reset(rv_mem m);
+
+/* Overwrites rows 0..n_rows-1 of every head with K, V ([n_heads][n_rows][head_dim]
+ * bf16, host or device memory) and sets the length to n_rows; provenance of these rows
+ * becomes (frame_id, row).  Used to prefill a memory or to restore a snapshot.
+ * Synchronous with respect to the host. */
+rv_status rv_mem_write(rv_mem m, const void *K, const void *V, int64_t n_rows, int frame_id,
+                       void *stream);
+
+/* Copies rows 0..len-1 of every head into K, V ([n_heads][len][head_dim] bf16) and
+ * prov ([n_heads][len][2] int32); each destination may be NULL to skip it, and may be
+ * host or device memory.  Synchronous with respect to the host. */
+rv_status rv_mem_read(rv_mem m, void *K, void *V, int32_t *prov, void *stream);
+
+/* ---- the per-frame hot path ---------------------------------------------------------- */
+
+/* Temporal-causal attention of one frame over memory + frame (Sec. 3.1 Eq. 3): for
+ * head h and query i, the context is memory rows 0..mem_len-1 of head h followed by
+ * the frame's own n_tokens keys, with no mask inside the frame;
+ *   z_ic = q_i . k_c / sqrt(head_dim),  LSE_i = log sum_c exp(z_ic)   (natural log),
+ *   out_i = sum_c exp(z_ic - LSE_i) v_c.
+ * Q, K, V, out: [n_tokens][n_heads][64] bf16.  memK, memV: [n_heads][head_stride][64]
+ * bf16 (mem_len 0 allows NULL).  lse: [n_heads][n_tokens] fp32, required.
+ * saliency: NULL, or [n_heads][n_tokens] fp32 that receives, for every frame key j,
+ *   S_j = sum over sampled queries i (per *qs) of exp(z_ij - LSE_i)     (Sec. 3.3),
+ * in which case qs must be given and describe n_tokens.
+ * Arithmetic: bf16 inputs, fp32 logits and softmax, probabilities rounded to bf16 for
+ * the value product, fp32 accumulation, out rounded to bf16 (nearest-even).
+ * n_tokens 0 is a no-op.  May allocate its split-KV workspace on first use (see
+ * rv_reserve_workspace). */
+rv_status rv_attend_frame(const void *Q, const void *K, const void *V, int n_tokens,
+                          const void *memK, const void *memV, int64_t mem_len,
+                          int64_t head_stride_tokens, int n_heads, int head_dim,
+                          const rv_qsub *qs, void *out, float *lse, float *saliency,
+                          void *stream);
+
+/* Admission from a given saliency (Sec. 3.3 Eq. 6): per head, selects the `budget`
+ * tokens of largest saliency -- equal saliencies ordered by lower token index -- and
+ * appends their K and V rows (exact copies) to m in ascending token order; the length
+ * grows by `budget` at once on the host.  saliency: [n_heads][n_tokens] fp32, finite,
+ * >= 0.  K, V: the frame's [n_tokens][n_heads][64] bf16.  idx_out: NULL or
+ * [n_heads][budget] int32 receiving the selected indices, ascending.
+ * 0 <= budget <= n_tokens <= 16384; budget == n_tokens appends every token (the anchor
+ * frame of Eq. 4, or full retention).  Grows m if needed (RV_ERR_CAPACITY beyond
+ * max_tokens, RV_ERR_OOM on allocation failure; m unchanged in both cases). */
+rv_status rv_admit(const float *saliency, int budget, const void *K, const void *V,
+                   int n_tokens, rv_mem m, int frame_id, int32_t *idx_out, void *stream);
+
+/* Deferred admission for n_layers layers of one frame in one launch: for layer l,
+ * computes the saliency of Q[l], K[l] against lse[l] (as rv_attend_frame would),
+ * then selects and appends exactly as rv_admit does into mems[l].  Bit-identical to
+ * per-layer rv_attend_frame(..., saliency) + rv_admit.  Layer l's memory must not be
+ * read by this frame's attention after this call (Eq. 6 makes admissions visible from
+ * the next frame on).  Q, K, V, lse, mems: host arrays of n_layers device pointers /
+ * handles.  saliency_out, idx_out: NULL, or host arrays of n_layers device pointers
+ * ([n_heads][n_tokens] fp32, [n_heads][budget] int32), each of which may be NULL.
+ * All layers share n_heads, n_tokens, qs, budget.  1 <= n_layers <= 4096. */
+rv_status rv_admit_layers(int n_layers, const void *const *Q, const void *const *K,
+                          const void *const *V, const float *const *lse, int n_tokens,
+                          const rv_qsub *qs, int budget, const rv_mem *mems, int frame_id,
+                          float *const *saliency_out, int32_t *const *idx_out, void *stream);
+
+/* Pre-allocates the current device's scratch workspace (split-KV partial results,
+ * saliency staging, completion counters) for frames of up to n_tokens tokens with
+ * n_heads heads, and up to n_layers layers per rv_admit_layers call, so that later
+ * calls within those sizes do not allocate. */
+rv_status rv_reserve_workspace(int n_tokens, int n_heads, int n_layers);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

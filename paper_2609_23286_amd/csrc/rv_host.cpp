@@ -1,0 +1,599 @@
+// rv_host.cpp -- librv host side: argument checks, error state, memory arenas,
+// per-device scratch workspace and kernel launches.  See include/rv.h for the contract.
+#include "../../include/rv.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "rv_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+rv_status fail(rv_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+rv_status hip_fail(hipError_t e, const char* what) {
+  return fail(e == hipErrorOutOfMemory ? RV_ERR_OOM : RV_ERR_HIP, "%s: %s", what,
+              hipGetErrorString(e));
+}
+
+#define RV_HIP(call, what)                       \
+  do {                                           \
+    hipError_t e_ = (call);                      \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  if (!v || !*v) return dflt;
+  return std::atoi(v);
+}
+
+// ---- per-device scratch workspace ------------------------------------------------
+struct Workspace {
+  float* part = nullptr;     // split-KV partials (O, then max/sum)
+  size_t part_floats = 0;
+  int* counters = nullptr;   // completion counters, zero between launches
+  size_t n_counters = 0;
+  float* sal = nullptr;      // saliency staging when the caller passes none
+  size_t sal_floats = 0;
+  std::map<std::tuple<int, int, int, int>, std::pair<int32_t*, int>> qidx;  // per query subset
+};
+
+std::mutex g_ws_mu;
+std::map<int, Workspace> g_ws;
+
+template <class T>
+rv_status grow(T** p, size_t* have, size_t need, bool zero, const char* what) {
+  if (*have >= need) return RV_OK;
+  size_t n = std::max(need, *have * 2);
+  T* q = nullptr;
+  hipError_t e = hipMalloc(&q, n * sizeof(T));
+  if (e != hipSuccess) return hip_fail(e, what);
+  if (zero) {
+    e = hipMemset(q, 0, n * sizeof(T));
+    if (e != hipSuccess) {
+      (void)hipFree(q);
+      return hip_fail(e, what);
+    }
+  }
+  if (*p) {
+    // earlier launches may still use the old buffer
+    e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+      (void)hipFree(q);
+      return hip_fail(e, what);
+    }
+    if (zero && *have) {
+      // counters carry no state between launches, so nothing to copy
+    }
+    (void)hipFree(*p);
+  }
+  *p = q;
+  *have = n;
+  return RV_OK;
+}
+
+rv_status current_ws(Workspace** out) {
+  int dev = 0;
+  RV_HIP(hipGetDevice(&dev), "hipGetDevice");
+  *out = &g_ws[dev];
+  return RV_OK;
+}
+
+// Sampled query positions for a frame layout (Sec. 3.3, head-specific retention).
+std::vector<int32_t> qsub_positions(const rv_qsub& q) {
+  std::vector<int32_t> v;
+  for (int r = 0; r < q.grid_h; r += q.stride)
+    for (int c = 0; c < q.grid_w; c += q.stride) v.push_back(q.n_special + r * q.grid_w + c);
+  return v;
+}
+
+rv_status check_qsub(const rv_qsub* qs, int n_tokens) {
+  if (!qs) return fail(RV_ERR_INVALID, "query subset descriptor is NULL");
+  if (qs->grid_h < 0 || qs->grid_w < 0 || qs->n_special < 0 || qs->stride < 1)
+    return fail(RV_ERR_INVALID, "query subset has negative sizes or stride < 1");
+  if ((int64_t)qs->grid_h * qs->grid_w + qs->n_special != n_tokens)
+    return fail(RV_ERR_INVALID, "query subset %dx%d+%d does not describe %d tokens", qs->grid_h,
+                qs->grid_w, qs->n_special, n_tokens);
+  return RV_OK;
+}
+
+rv_status device_qidx(Workspace* ws, const rv_qsub& q, hipStream_t s, const int32_t** ptr, int* n) {
+  auto key = std::make_tuple(q.grid_h, q.grid_w, q.n_special, q.stride);
+  auto it = ws->qidx.find(key);
+  if (it == ws->qidx.end()) {
+    std::vector<int32_t> v = qsub_positions(q);
+    int32_t* d = nullptr;
+    RV_HIP(hipMalloc(&d, std::max<size_t>(1, v.size()) * sizeof(int32_t)), "qidx alloc");
+    if (!v.empty()) {
+      hipError_t e = hipMemcpy(d, v.data(), v.size() * sizeof(int32_t), hipMemcpyHostToDevice);
+      if (e != hipSuccess) {
+        (void)hipFree(d);
+        return hip_fail(e, "qidx upload");
+      }
+    }
+    it = ws->qidx.emplace(key, std::make_pair(d, (int)v.size())).first;
+  }
+  (void)s;
+  *ptr = it->second.first;
+  *n = it->second.second;
+  return RV_OK;
+}
+
+// Split-KV plan for one attention launch.
+struct AttnPlan {
+  int q_tiles, nt_mem, nt_total, n_splits;
+};
+
+AttnPlan plan_attention(int n_tokens, int64_t mem_len, int n_heads) {
+  AttnPlan p;
+  p.q_tiles = (int)ceil_div(n_tokens, rv::kAttnBQ);
+  p.nt_mem = (int)ceil_div(mem_len, rv::kAttnBK);
+  p.nt_total = p.nt_mem + (int)ceil_div(n_tokens, rv::kAttnBK);
+  const int base = p.q_tiles * n_heads;
+  const int target = env_int("RV_ATTN_TARGET_WGS", 1024);
+  const int min_tiles = std::max(1, env_int("RV_ATTN_MIN_TILES_PER_SPLIT", 2));
+  int s = (int)ceil_div(target, base);
+  s = std::min(s, rv::kMaxSplits);
+  s = std::min(s, std::max(1, p.nt_total / min_tiles));
+  p.n_splits = std::max(1, s);
+  return p;
+}
+
+rv_status reserve_attention(Workspace* ws, int n_tokens, int n_heads) {
+  const size_t tiles = (size_t)ceil_div(n_tokens, rv::kAttnBQ) * n_heads;
+  const size_t slots = tiles * rv::kMaxSplits;
+  rv_status st = grow(&ws->part, &ws->part_floats, slots * rv::kAttnBQ * (rv::kHeadDim + 2), false,
+                      "attention workspace");
+  if (st != RV_OK) return st;
+  return RV_OK;
+}
+
+rv_status reserve_counters(Workspace* ws, size_t n) {
+  return grow(&ws->counters, &ws->n_counters, n, true, "counter workspace");
+}
+
+}  // namespace
+
+// ---- memory arena ----------------------------------------------------------------
+struct rv_mem_s {
+  int device = 0;
+  int n_heads = 0;
+  int64_t cap = 0, max_tokens = 0, len = 0;
+  uint16_t* K = nullptr;
+  uint16_t* V = nullptr;
+  int32_t* prov = nullptr;
+};
+
+namespace {
+
+rv_status arena_alloc(int n_heads, int64_t cap, uint16_t** K, uint16_t** V, int32_t** prov) {
+  *K = *V = nullptr;
+  *prov = nullptr;
+  if (cap == 0) return RV_OK;
+  const size_t rows = (size_t)n_heads * (size_t)cap;
+  hipError_t e = hipMalloc(K, rows * rv::kHeadDim * 2);
+  if (e == hipSuccess) e = hipMalloc(V, rows * rv::kHeadDim * 2);
+  if (e == hipSuccess) e = hipMalloc(prov, rows * 2 * sizeof(int32_t));
+  if (e != hipSuccess) {
+    if (*K) (void)hipFree(*K);
+    if (*V) (void)hipFree(*V);
+    if (*prov) (void)hipFree(*prov);
+    *K = *V = nullptr;
+    *prov = nullptr;
+    return hip_fail(e, "memory arena allocation");
+  }
+  return RV_OK;
+}
+
+// Grows m to hold at least `tokens` rows per head; strong guarantee on failure.
+rv_status arena_reserve(rv_mem m, int64_t tokens, hipStream_t s) {
+  if (tokens <= m->cap) return RV_OK;
+  if (tokens > m->max_tokens)
+    return fail(RV_ERR_CAPACITY, "memory needs %lld rows per head, max_tokens is %lld",
+                (long long)tokens, (long long)m->max_tokens);
+  int64_t cap = std::max<int64_t>(tokens, std::min<int64_t>(m->max_tokens, std::max<int64_t>(256, m->cap * 2)));
+  uint16_t *K, *V;
+  int32_t* prov;
+  rv_status st = arena_alloc(m->n_heads, cap, &K, &V, &prov);
+  if (st != RV_OK) return st;
+  hipError_t e = hipSuccess;
+  if (m->len > 0) {
+    const size_t row = rv::kHeadDim * 2;
+    e = hipMemcpy2DAsync(K, cap * row, m->K, m->cap * row, m->len * row, m->n_heads,
+                         hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpy2DAsync(V, cap * row, m->V, m->cap * row, m->len * row, m->n_heads,
+                           hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpy2DAsync(prov, cap * 8, m->prov, m->cap * 8, m->len * 8, m->n_heads,
+                           hipMemcpyDeviceToDevice, s);
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    (void)hipFree(K);
+    (void)hipFree(V);
+    (void)hipFree(prov);
+    return hip_fail(e, "memory growth copy");
+  }
+  if (m->K) (void)hipFree(m->K);
+  if (m->V) (void)hipFree(m->V);
+  if (m->prov) (void)hipFree(m->prov);
+  m->K = K;
+  m->V = V;
+  m->prov = prov;
+  m->cap = cap;
+  return RV_OK;
+}
+
+rv_status check_device(rv_mem m) {
+  int dev = 0;
+  RV_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev != m->device)
+    return fail(RV_ERR_INVALID, "memory lives on device %d but device %d is current", m->device, dev);
+  return RV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* rv_last_error(void) { return g_err.c_str(); }
+
+const char* rv_version(void) { return "librv 0.1 (gfx950)"; }
+
+rv_status rv_mem_create(int n_heads, int head_dim, int64_t reserve_tokens, int64_t max_tokens,
+                        rv_mem* out) {
+  if (!out) return fail(RV_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (n_heads < 1) return fail(RV_ERR_INVALID, "n_heads must be >= 1 (got %d)", n_heads);
+  if (head_dim != rv::kHeadDim) return fail(RV_ERR_INVALID, "head_dim must be 64 (got %d)", head_dim);
+  if (reserve_tokens < 0 || max_tokens < 0 || reserve_tokens > max_tokens)
+    return fail(RV_ERR_INVALID, "need 0 <= reserve_tokens <= max_tokens");
+  rv_mem m = new (std::nothrow) rv_mem_s;
+  if (!m) return fail(RV_ERR_OOM, "host allocation failed");
+  hipError_t e = hipGetDevice(&m->device);
+  if (e != hipSuccess) {
+    delete m;
+    return hip_fail(e, "hipGetDevice");
+  }
+  m->n_heads = n_heads;
+  m->max_tokens = max_tokens;
+  rv_status st = arena_alloc(n_heads, reserve_tokens, &m->K, &m->V, &m->prov);
+  if (st != RV_OK) {
+    delete m;
+    return st;
+  }
+  m->cap = reserve_tokens;
+  *out = m;
+  return RV_OK;
+}
+
+rv_status rv_mem_destroy(rv_mem m) {
+  if (!m) return RV_OK;
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(m->device);
+  (void)hipDeviceSynchronize();
+  if (m->K) (void)hipFree(m->K);
+  if (m->V) (void)hipFree(m->V);
+  if (m->prov) (void)hipFree(m->prov);
+  (void)hipSetDevice(prev);
+  delete m;
+  return RV_OK;
+}
+
+int64_t rv_mem_len(rv_mem m) { return m ? m->len : -1; }
+
+int64_t rv_mem_capacity(rv_mem m) { return m ? m->cap : -1; }
+
+rv_status rv_mem_view(rv_mem m, const void** memK, const void** memV, int64_t* head_stride_tokens) {
+  if (!m || !memK || !memV || !head_stride_tokens) return fail(RV_ERR_INVALID, "NULL argument");
+  *memK = m->K;
+  *memV = m->V;
+  *head_stride_tokens = m->cap;
+  return RV_OK;
+}
+
+rv_status rv_mem_reserve(rv_mem m, int64_t tokens, void* stream) {
+  if (!m) return fail(RV_ERR_INVALID, "memory is NULL");
+  if (tokens < 0) return fail(RV_ERR_INVALID, "tokens must be >= 0");
+  rv_status st = check_device(m);
+  if (st != RV_OK) return st;
+  return arena_reserve(m, tokens, (hipStream_t)stream);
+}
+
+rv_status rv_mem_reset(rv_mem m) {
+  if (!m) return fail(RV_ERR_INVALID, "memory is NULL");
+  m->len = 0;
+  return RV_OK;
+}
+
+rv_status rv_mem_write(rv_mem m, const void* K, const void* V, int64_t n_rows, int frame_id,
+                       void* stream) {
+  if (!m || (n_rows > 0 && (!K || !V))) return fail(RV_ERR_INVALID, "NULL argument");
+  if (n_rows < 0) return fail(RV_ERR_INVALID, "n_rows must be >= 0");
+  rv_status st = check_device(m);
+  if (st != RV_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const int64_t keep = m->len;
+  m->len = 0;  // nothing to preserve: rows are overwritten
+  st = arena_reserve(m, n_rows, s);
+  if (st != RV_OK) {
+    m->len = keep;
+    return st;
+  }
+  if (n_rows > 0) {
+    const size_t row = rv::kHeadDim * 2;
+    std::vector<int32_t> prov((size_t)n_rows * 2);
+    for (int64_t r = 0; r < n_rows; ++r) {
+      prov[2 * r] = frame_id;
+      prov[2 * r + 1] = (int32_t)r;
+    }
+    hipError_t e = hipMemcpy2DAsync(m->K, m->cap * row, K, n_rows * row, n_rows * row, m->n_heads,
+                                    hipMemcpyDefault, s);
+    if (e == hipSuccess)
+      e = hipMemcpy2DAsync(m->V, m->cap * row, V, n_rows * row, n_rows * row, m->n_heads,
+                           hipMemcpyDefault, s);
+    for (int h = 0; e == hipSuccess && h < m->n_heads; ++h)
+      e = hipMemcpyAsync(m->prov + (size_t)h * m->cap * 2, prov.data(), prov.size() * 4,
+                         hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "rv_mem_write copy");
+  }
+  m->len = n_rows;
+  return RV_OK;
+}
+
+rv_status rv_mem_read(rv_mem m, void* K, void* V, int32_t* prov, void* stream) {
+  if (!m) return fail(RV_ERR_INVALID, "memory is NULL");
+  rv_status st = check_device(m);
+  if (st != RV_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (m->len == 0) return RV_OK;
+  const size_t row = rv::kHeadDim * 2;
+  hipError_t e = hipSuccess;
+  if (K) e = hipMemcpy2DAsync(K, m->len * row, m->K, m->cap * row, m->len * row, m->n_heads, hipMemcpyDefault, s);
+  if (e == hipSuccess && V)
+    e = hipMemcpy2DAsync(V, m->len * row, m->V, m->cap * row, m->len * row, m->n_heads, hipMemcpyDefault, s);
+  if (e == hipSuccess && prov)
+    e = hipMemcpy2DAsync(prov, m->len * 8, m->prov, m->cap * 8, m->len * 8, m->n_heads, hipMemcpyDefault, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "rv_mem_read copy");
+  return RV_OK;
+}
+
+rv_status rv_reserve_workspace(int n_tokens, int n_heads, int n_layers) {
+  if (n_tokens < 1 || n_tokens > rv::kMaxTokens || n_heads < 1 || n_layers < 1)
+    return fail(RV_ERR_INVALID, "bad workspace sizes");
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace* ws;
+  rv_status st = current_ws(&ws);
+  if (st != RV_OK) return st;
+  st = reserve_attention(ws, n_tokens, n_heads);
+  if (st != RV_OK) return st;
+  const size_t tiles = (size_t)ceil_div(n_tokens, rv::kAttnBQ) * n_heads;
+  const size_t per_launch = std::min<size_t>(n_layers, rv::kMaxLayersPerLaunch) * n_heads;
+  st = reserve_counters(ws, std::max(tiles, per_launch));
+  if (st != RV_OK) return st;
+  return grow(&ws->sal, &ws->sal_floats, (size_t)std::min(n_layers, rv::kMaxLayersPerLaunch) * n_heads * n_tokens,
+              false, "saliency workspace");
+}
+
+rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
+                          const void* memV, int64_t mem_len, int64_t head_stride_tokens, int n_heads,
+                          int head_dim, const rv_qsub* qs, void* out, float* lse, float* saliency,
+                          void* stream) {
+  if (n_tokens < 0 || n_tokens > rv::kMaxTokens)
+    return fail(RV_ERR_INVALID, "n_tokens must be in [0, %d] (got %d)", rv::kMaxTokens, n_tokens);
+  if (n_heads < 1) return fail(RV_ERR_INVALID, "n_heads must be >= 1");
+  if (head_dim != rv::kHeadDim) return fail(RV_ERR_INVALID, "head_dim must be 64 (got %d)", head_dim);
+  if (mem_len < 0) return fail(RV_ERR_INVALID, "mem_len must be >= 0");
+  if (mem_len > 0 && (!memK || !memV)) return fail(RV_ERR_INVALID, "memK/memV NULL with mem_len > 0");
+  if (mem_len > 0 && head_stride_tokens < mem_len)
+    return fail(RV_ERR_INVALID, "head_stride_tokens (%lld) < mem_len (%lld)", (long long)head_stride_tokens,
+                (long long)mem_len);
+  if (n_tokens == 0) return RV_OK;
+  if (!Q || !K || !V || !out || !lse) return fail(RV_ERR_INVALID, "Q, K, V, out and lse are required");
+  if (saliency) {
+    rv_status st = check_qsub(qs, n_tokens);
+    if (st != RV_OK) return st;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace* ws;
+  rv_status st = current_ws(&ws);
+  if (st != RV_OK) return st;
+
+  const AttnPlan p = plan_attention(n_tokens, mem_len, n_heads);
+  st = reserve_attention(ws, n_tokens, n_heads);
+  if (st != RV_OK) return st;
+  st = reserve_counters(ws, (size_t)p.q_tiles * n_heads);
+  if (st != RV_OK) return st;
+  const int32_t* qidx = nullptr;
+  int n_q = 0;
+  if (saliency) {
+    st = device_qidx(ws, *qs, s, &qidx, &n_q);
+    if (st != RV_OK) return st;
+  }
+
+  rv::AttnArgs a{};
+  a.Q = (const uint16_t*)Q;
+  a.K = (const uint16_t*)K;
+  a.V = (const uint16_t*)V;
+  a.memK = (const uint16_t*)memK;
+  a.memV = (const uint16_t*)memV;
+  a.mem_len = mem_len;
+  a.head_stride = head_stride_tokens;
+  a.out = (uint16_t*)out;
+  a.lse = lse;
+  a.part_o = ws->part;
+  a.part_ml = ws->part + (size_t)p.q_tiles * n_heads * rv::kMaxSplits * rv::kAttnBQ * rv::kHeadDim;
+  a.counters = ws->counters;
+  a.n_tokens = n_tokens;
+  a.n_heads = n_heads;
+  a.q_tiles = p.q_tiles;
+  a.n_splits = p.n_splits;
+  a.nt_mem = p.nt_mem;
+  a.nt_total = p.nt_total;
+  a.n_work = p.q_tiles * n_heads * p.n_splits;
+  a.per_xcd = (int)ceil_div(a.n_work, 8);
+  RV_HIP(rv::launch_attention(a, s), "attention launch");
+
+  if (saliency) {
+    rv::AdmitArgs b{};
+    b.layer[0].Q = (const uint16_t*)Q;
+    b.layer[0].K = (const uint16_t*)K;
+    b.layer[0].lse = lse;
+    b.layer[0].sal = saliency;
+    b.qidx = qidx;
+    b.n_q = n_q;
+    b.n_tokens = n_tokens;
+    b.n_heads = n_heads;
+    b.n_layers = 1;
+    b.key_chunks = (int)ceil_div(n_tokens, rv::kSalBK);
+    b.mode = rv::kModeSaliency;
+    RV_HIP(rv::launch_admit(b, s), "saliency launch");
+  }
+  return RV_OK;
+}
+
+rv_status rv_admit(const float* saliency, int budget, const void* K, const void* V, int n_tokens, rv_mem m,
+                   int frame_id, int32_t* idx_out, void* stream) {
+  if (!m) return fail(RV_ERR_INVALID, "memory is NULL");
+  if (n_tokens < 1 || n_tokens > rv::kMaxTokens)
+    return fail(RV_ERR_INVALID, "n_tokens must be in [1, %d] (got %d)", rv::kMaxTokens, n_tokens);
+  if (budget < 0 || budget > n_tokens)
+    return fail(RV_ERR_INVALID, "budget must be in [0, n_tokens] (got %d)", budget);
+  if (budget > 0 && (!saliency || !K || !V)) return fail(RV_ERR_INVALID, "saliency, K and V are required");
+  rv_status st = check_device(m);
+  if (st != RV_OK) return st;
+  if (budget == 0) return RV_OK;
+  hipStream_t s = (hipStream_t)stream;
+  st = arena_reserve(m, m->len + budget, s);
+  if (st != RV_OK) return st;
+
+  rv::AdmitArgs b{};
+  b.layer[0].K = (const uint16_t*)K;
+  b.layer[0].V = (const uint16_t*)V;
+  b.layer[0].sal = const_cast<float*>(saliency);
+  b.layer[0].idx = idx_out;
+  b.layer[0].memK = m->K;
+  b.layer[0].memV = m->V;
+  b.layer[0].prov = m->prov;
+  b.layer[0].mem_len = m->len;
+  b.layer[0].head_stride = m->cap;
+  b.n_tokens = n_tokens;
+  b.n_heads = m->n_heads;
+  b.n_layers = 1;
+  b.budget = budget;
+  b.frame_id = frame_id;
+  b.mode = rv::kModeSelect;
+  RV_HIP(rv::launch_admit(b, s), "admit launch");
+  m->len += budget;
+  return RV_OK;
+}
+
+rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const* K, const void* const* V,
+                          const float* const* lse, int n_tokens, const rv_qsub* qs, int budget,
+                          const rv_mem* mems, int frame_id, float* const* saliency_out,
+                          int32_t* const* idx_out, void* stream) {
+  if (n_layers < 1 || n_layers > 4096) return fail(RV_ERR_INVALID, "n_layers must be in [1, 4096]");
+  if (!Q || !K || !V || !lse || !mems) return fail(RV_ERR_INVALID, "NULL pointer array");
+  if (n_tokens < 1 || n_tokens > rv::kMaxTokens)
+    return fail(RV_ERR_INVALID, "n_tokens must be in [1, %d] (got %d)", rv::kMaxTokens, n_tokens);
+  if (budget < 0 || budget > n_tokens)
+    return fail(RV_ERR_INVALID, "budget must be in [0, n_tokens] (got %d)", budget);
+  rv_status st = check_qsub(qs, n_tokens);
+  if (st != RV_OK) return st;
+  const int H = mems[0] ? mems[0]->n_heads : 0;
+  for (int l = 0; l < n_layers; ++l) {
+    if (!Q[l] || !K[l] || !V[l] || !lse[l] || !mems[l])
+      return fail(RV_ERR_INVALID, "layer %d: NULL tensor or memory", l);
+    if (mems[l]->n_heads != H) return fail(RV_ERR_INVALID, "layer %d: head count differs", l);
+    st = check_device(mems[l]);
+    if (st != RV_OK) return st;
+    if (mems[l]->len + budget > mems[l]->max_tokens)
+      return fail(RV_ERR_CAPACITY, "layer %d: memory would exceed max_tokens", l);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace* ws;
+  st = current_ws(&ws);
+  if (st != RV_OK) return st;
+  // growth first, for every layer, before anything is enqueued
+  for (int l = 0; l < n_layers; ++l) {
+    st = arena_reserve(mems[l], mems[l]->len + budget, s);
+    if (st != RV_OK) return st;
+  }
+  const int chunk_layers = std::min(n_layers, rv::kMaxLayersPerLaunch);
+  st = reserve_counters(ws, (size_t)chunk_layers * H);
+  if (st != RV_OK) return st;
+  bool need_ws_sal = !saliency_out;
+  for (int l = 0; saliency_out && l < n_layers; ++l) need_ws_sal |= !saliency_out[l];
+  if (need_ws_sal) {
+    st = grow(&ws->sal, &ws->sal_floats, (size_t)chunk_layers * H * n_tokens, false, "saliency workspace");
+    if (st != RV_OK) return st;
+  }
+  const int32_t* qidx = nullptr;
+  int n_q = 0;
+  st = device_qidx(ws, *qs, s, &qidx, &n_q);
+  if (st != RV_OK) return st;
+
+  for (int l0 = 0; l0 < n_layers; l0 += rv::kMaxLayersPerLaunch) {
+    const int nl = std::min(rv::kMaxLayersPerLaunch, n_layers - l0);
+    rv::AdmitArgs b{};
+    for (int i = 0; i < nl; ++i) {
+      const int l = l0 + i;
+      rv::AdmitLayer& L = b.layer[i];
+      L.Q = (const uint16_t*)Q[l];
+      L.K = (const uint16_t*)K[l];
+      L.V = (const uint16_t*)V[l];
+      L.lse = lse[l];
+      L.sal = (saliency_out && saliency_out[l]) ? saliency_out[l] : ws->sal + (size_t)i * H * n_tokens;
+      L.idx = idx_out ? idx_out[l] : nullptr;
+      L.memK = mems[l]->K;
+      L.memV = mems[l]->V;
+      L.prov = mems[l]->prov;
+      L.mem_len = mems[l]->len;
+      L.head_stride = mems[l]->cap;
+    }
+    b.qidx = qidx;
+    b.counters = ws->counters;
+    b.n_q = n_q;
+    b.n_tokens = n_tokens;
+    b.n_heads = H;
+    b.n_layers = nl;
+    b.budget = budget;
+    b.frame_id = frame_id;
+    b.key_chunks = (int)ceil_div(n_tokens, rv::kSalBK);
+    b.mode = rv::kModeBoth;
+    RV_HIP(rv::launch_admit(b, s), "admit_layers launch");
+  }
+  for (int l = 0; l < n_layers; ++l) mems[l]->len += budget;
+  return RV_OK;
+}
+
+}  // extern "C"

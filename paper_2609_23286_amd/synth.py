@@ -32,6 +32,7 @@ Recipe (stated once; the GPU generator follows it step for step):
 """
 from dataclasses import dataclass, field
 import math
+import os
 
 import numpy as np
 
@@ -48,20 +49,22 @@ IH_SD = math.sqrt(8.0 * (65536.0 ** 2 - 1.0) / 12.0)
 
 def philox4x32_10(c0, c1, c2, c3, k0, k1):
     """Philox4x32 with 10 rounds on uint32 arrays (broadcast); returns 4 uint32 arrays."""
-    c = [np.asarray(x, dtype=np.uint64) & MASK32 for x in (c0, c1, c2, c3)]
-    c = list(np.broadcast_arrays(*c))
-    k0 = np.uint64(k0 & MASK32)
-    k1 = np.uint64(k1 & MASK32)
+    u64 = np.uint64
+    c0, c1, c2, c3 = (np.asarray(x, dtype=np.uint64) & u64(MASK32) for x in (c0, c1, c2, c3))
+    k0, k1 = int(k0) & MASK32, int(k1) & MASK32
+    m32, sh = u64(MASK32), u64(32)
     for r in range(10):
         if r:
-            k0 = np.uint64((int(k0) + W0) & MASK32)
-            k1 = np.uint64((int(k1) + W1) & MASK32)
-        p0 = c[0] * np.uint64(M0)
-        p1 = c[2] * np.uint64(M1)
-        hi0, lo0 = p0 >> np.uint64(32), p0 & np.uint64(MASK32)
-        hi1, lo1 = p1 >> np.uint64(32), p1 & np.uint64(MASK32)
-        c = [hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0]
-    return [x.astype(np.uint32) for x in c]
+            k0 = (k0 + W0) & MASK32
+            k1 = (k1 + W1) & MASK32
+        p0 = c0 * u64(M0)
+        p1 = c2 * u64(M1)
+        c0 = (p1 >> sh) ^ c1 ^ u64(k0)
+        c1 = p1 & m32
+        c2 = (p0 >> sh) ^ c3 ^ u64(k1)
+        c3 = p0 & m32
+    c0, c1, c2, c3 = np.broadcast_arrays(c0, c1, c2, c3)
+    return [x.astype(np.uint32) for x in (c0, c1, c2, c3)]
 
 
 def f32_to_bf16_bits(x):
@@ -73,6 +76,28 @@ def f32_to_bf16_bits(x):
 
 def bf16_bits_to_f32(b):
     return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+_CHUNK = 1 << 18
+
+
+def _normal_chunk(e0, e1, frame, stream_id, k0, k1, scale, out):
+    """Elements e0..e1-1 of one counter stream -> bf16 bits into out[e0:e1]."""
+    e = np.arange(e0, e1, dtype=np.uint64)
+    w = philox4x32_10(e & np.uint64(MASK32), e >> np.uint64(32), np.uint64(frame),
+                      np.uint64(stream_id), k0, k1)
+    s = np.zeros(e.shape, dtype=np.int64)
+    for x in w:
+        x = x.astype(np.int64)
+        s += (x & 0xFFFF) + (x >> 16)
+    s -= IH_MEAN
+    out[e0:e1] = f32_to_bf16_bits(s.astype(np.float32) * scale)
+
+
+def _irwin_hall_stream(seed, frame, layer, tag, n):
+    """Centred order-8 Irwin-Hall integers of one counter stream (length n)."""
+    w = _stream_words(seed, frame, layer, tag, n)
+    return irwin_hall8(w)
 
 
 def _stream_words(seed, frame, layer, tag, n):
@@ -90,12 +115,22 @@ def irwin_hall8(words):
 
 
 def normal_bf16(seed, frame, layer, tag, shape, sigma):
-    """Near-Gaussian N(0, sigma^2) tensor as bf16 bit patterns (see module recipe)."""
+    """Near-Gaussian N(0, sigma^2) tensor as bf16 bit patterns (see module recipe).
+    Large tensors are drawn in independent chunks on a thread pool (numpy releases
+    the GIL); the bits do not depend on the chunking."""
     n = int(np.prod(shape))
-    centred = irwin_hall8(_stream_words(seed, frame, layer, tag, n))
     scale = np.float32(sigma / IH_SD)
-    x = centred.astype(np.float32) * scale
-    return f32_to_bf16_bits(x).reshape(shape)
+    out = np.empty(n, dtype=np.uint16)
+    args = (frame & MASK32, ((layer << 8) | tag) & MASK32, seed & MASK32, seed >> 32, scale, out)
+    bounds = [(a, min(n, a + _CHUNK)) for a in range(0, n, _CHUNK)]
+    if len(bounds) <= 1:
+        for a, b in bounds:
+            _normal_chunk(a, b, *args)
+    else:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(lambda ab: _normal_chunk(ab[0], ab[1], *args), bounds))
+    return out.reshape(shape)
 
 
 def plant_positions(seed, frame, layer, n_heads, n_tokens, n_plant):
@@ -190,8 +225,7 @@ def frame_qkv(cfg: StreamConfig, layer: int, frame: int):
     K = normal_bf16(cfg.seed, frame, layer, TAG_K, shape, cfg.sigma)
     V = normal_bf16(cfg.seed, frame, layer, TAG_V, shape, cfg.sigma)
     if cfg.lognormal_sigma > 0.0:
-        xi = irwin_hall8(_stream_words(cfg.seed, frame, layer, TAG_LOGN,
-                                       cfg.n_tokens * cfg.n_heads)) / IH_SD
+        xi = _irwin_hall_stream(cfg.seed, frame, layer, TAG_LOGN, cfg.n_tokens * cfg.n_heads) / IH_SD
         s = np.exp(cfg.lognormal_sigma * xi).astype(np.float32).reshape(cfg.n_tokens, cfg.n_heads, 1)
         K = f32_to_bf16_bits(bf16_bits_to_f32(K) * s)
     if cfg.n_plant > 0:

@@ -1,0 +1,229 @@
+"""GPU parity, kernel by kernel: librv through its C ABI against the fp64 oracle on the
+same seeded inputs.  Shapes span several tiles with ragged tails, empty and one-row
+memories, one-token frames, and the ViT-L frame (1041 tokens x 16 heads)."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_23286_amd import synth
+from util import (BAND, LSE_ATOL, OUT_ATOL, SAL_RTOL, bf16_to_f64, check_index_sets, to_dev,
+                  to_host_u16)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def rv():
+    from paper_2609_23286_amd import rv as _rv
+    return _rv
+
+
+def frame(seed, N, H, sigma=0.125):
+    return tuple(synth.normal_bf16(seed, 0, 0, tag, (N, H, 64), sigma) for tag in range(3))
+
+
+def memory_rows(seed, H, M, sigma=0.125):
+    K = synth.normal_bf16(seed, 1, 0, synth.TAG_MEMK, (H, M, 64), sigma)
+    V = synth.normal_bf16(seed, 1, 0, synth.TAG_MEMV, (H, M, 64), sigma)
+    return K, V
+
+
+def qsub_for(N):
+    if N == 1041:
+        return (28, 37, 5, 2)
+    return (1, N, 0, 2)   # a 1 x N strip: every other token
+
+
+def run_attend(rv, Q, K, V, memK, memV, qs, with_saliency=True):
+    import torch
+    N, H, _ = Q.shape
+    M = memK.shape[1]
+    mem = rv.Memory(H, reserve_tokens=M + 7, max_tokens=M + 64)
+    if M:
+        mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+    Qd, Kd, Vd = to_dev(Q), to_dev(K), to_dev(V)
+    out = torch.empty((N, H, 64), dtype=torch.int16, device="cuda")
+    lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
+    sal = torch.empty((H, N), dtype=torch.float32, device="cuda") if with_saliency else None
+    rv.attend_frame(Qd, Kd, Vd, mem, out, lse, sal, qs)
+    torch.cuda.synchronize()
+    res = (bf16_to_f64(to_host_u16(out)), lse.cpu().numpy().astype(np.float64),
+           None if sal is None else sal.cpu().numpy().astype(np.float64))
+    mem.close()
+    return res
+
+
+ATTEND_CASES = [  # (N, H, M, sigma)
+    (1, 1, 0, 0.125),
+    (1, 1, 1, 0.125),
+    (17, 2, 0, 0.125),
+    (64, 2, 0, 0.125),
+    (64, 2, 1, 0.125),
+    (65, 2, 63, 0.5),
+    (130, 2, 65, 0.125),
+    (200, 3, 1000, 0.125),
+    (300, 2, 700, 2.0),       # logits of a few units: running-max raises and rescales
+    (1041, 16, 0, 0.125),
+    (1041, 16, 257, 0.125),
+]
+
+
+@pytest.mark.parametrize("N,H,M,sigma", ATTEND_CASES)
+def test_attend_and_saliency_match_oracle(rv, N, H, M, sigma):
+    print(f"attend N={N} H={H} M={M} sigma={sigma}", flush=True)
+    Q, K, V = frame(100 + N + M, N, H, sigma)
+    memK, memV = memory_rows(200 + N + M, H, M, sigma)
+    qs = qsub_for(N)
+    out, lse, sal = run_attend(rv, Q, K, V, memK, memV, qs)
+    out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M)
+    qidx = oracle.qsub_index(*qs)
+    sal_o = oracle.saliency(Q, K, lse_o, qidx)
+    assert np.isfinite(out).all() and np.isfinite(lse).all() and np.isfinite(sal).all()
+    assert np.abs(out - out_o).max() <= OUT_ATOL
+    assert np.abs(lse - lse_o).max() <= LSE_ATOL
+    assert (np.abs(sal - sal_o) <= SAL_RTOL * sal_o).all()
+
+
+@pytest.mark.parametrize("target", ["1", "64", "100000"])
+def test_split_kv_partitions_agree_with_oracle(rv, target, monkeypatch):
+    """The split-KV plan (one split, a few, the maximum) changes only rounding order."""
+    monkeypatch.setenv("RV_ATTN_TARGET_WGS", target)
+    monkeypatch.setenv("RV_ATTN_MIN_TILES_PER_SPLIT", "1")
+    N, H, M = 333, 4, 1500
+    Q, K, V = frame(7, N, H)
+    memK, memV = memory_rows(8, H, M)
+    out, lse, _ = run_attend(rv, Q, K, V, memK, memV, qsub_for(N), with_saliency=False)
+    out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M)
+    assert np.abs(out - out_o).max() <= OUT_ATOL
+    assert np.abs(lse - lse_o).max() <= LSE_ATOL
+
+
+def test_saliency_is_bit_reproducible(rv):
+    N, H, M = 1041, 16, 500
+    Q, K, V = frame(3, N, H)
+    memK, memV = memory_rows(4, H, M)
+    a = run_attend(rv, Q, K, V, memK, memV, qsub_for(N))
+    b = run_attend(rv, Q, K, V, memK, memV, qsub_for(N))
+    for x, y in zip(a, b):
+        assert (x == y).all()
+
+
+SELECT_CASES = [  # (N, H, budget)
+    (1, 1, 0), (1, 1, 1), (64, 2, 1), (100, 3, 7), (1041, 16, 10), (1041, 4, 1040),
+    (1041, 2, 1041), (5000, 2, 50), (16384, 1, 163),
+]
+
+
+@pytest.mark.parametrize("N,H,budget", SELECT_CASES)
+def test_admit_matches_oracle_topk_on_given_saliency(rv, N, H, budget):
+    """rv_admit on a given saliency full of exact ties: the index set, its order, the
+    appended rows and their provenance must equal the oracle's exactly."""
+    import torch
+    print(f"admit N={N} H={H} budget={budget}", flush=True)
+    rng = np.random.default_rng(N + budget)
+    sal = (rng.integers(0, 9, size=(H, N)).astype(np.float32) / 9.0)
+    K, V, _ = frame(11, N, H)
+    mem = rv.Memory(H, reserve_tokens=3, max_tokens=budget + 10)
+    pre = memory_rows(12, H, 3)
+    mem.write(torch.from_numpy(pre[0].view(np.int16)), torch.from_numpy(pre[1].view(np.int16)), frame_id=-1)
+    idx = torch.full((H, budget), -7, dtype=torch.int32, device="cuda")
+    rv.admit(to_dev(sal), budget, to_dev(K), to_dev(V), mem, 42, idx)
+    torch.cuda.synchronize()
+    ref = oracle.topk(sal.astype(np.float64), budget)
+    got = idx.cpu().numpy()
+    assert (got == ref).all()
+    assert mem.len == 3 + budget
+    mk, mv, prov = mem.read()
+    mk, mv, prov = mk.numpy().view(np.uint16), mv.numpy().view(np.uint16), prov.numpy()
+    assert (mk[:, :3] == pre[0]).all() and (mv[:, :3] == pre[1]).all()
+    for h in range(H):
+        assert (mk[h, 3:] == K[ref[h], h]).all()
+        assert (mv[h, 3:] == V[ref[h], h]).all()
+        assert (prov[h, 3:, 0] == 42).all() and (prov[h, 3:, 1] == ref[h]).all()
+    mem.close()
+
+
+def test_admit_capacity_error_leaves_memory_unchanged(rv):
+    import torch
+    N, H = 64, 2
+    K, V, _ = frame(5, N, H)
+    sal = to_dev(np.linspace(1, 2, N * H, dtype=np.float32).reshape(H, N))
+    mem = rv.Memory(H, reserve_tokens=0, max_tokens=15)
+    rv.admit(sal, 10, to_dev(K), to_dev(V), mem, 0)
+    before = [t.clone() for t in mem.read()]
+    with pytest.raises(rv.RVError) as e:
+        rv.admit(sal, 10, to_dev(K), to_dev(V), mem, 1)
+    assert e.value.status == rv.RV_ERR_CAPACITY
+    assert mem.len == 10
+    after = mem.read()
+    assert all((x == y).all() for x, y in zip(before, after))
+    mem.close()
+
+
+def test_bad_shapes_are_rejected(rv):
+    import torch
+    Q = torch.zeros((10, 2, 64), dtype=torch.int16, device="cuda")
+    out = torch.zeros_like(Q)
+    lse = torch.zeros((2, 10), dtype=torch.float32, device="cuda")
+    with pytest.raises(ValueError):
+        rv.attend_frame(Q, Q, Q[:9], None, out, lse)
+    with pytest.raises(rv.RVError) as e:
+        rv.attend_frame(Q, Q, Q, None, out, lse, lse, qs=(3, 3, 0, 2))
+    assert e.value.status == rv.RV_ERR_INVALID
+
+
+def test_admit_layers_is_bit_identical_to_per_layer_calls(rv):
+    """Deferred, layer-batched admission == per-layer saliency + admit, bit for bit."""
+    import torch
+    L, N, H, M, budget = 3, 300, 4, 200, 5
+    qs = (10, 30, 0, 2)
+    results = []
+    for batched in (False, True):
+        mems, sals, idxs = [], [], []
+        for l in range(L):
+            Q, K, V = frame(50 + l, N, H)
+            memK, memV = memory_rows(60 + l, H, M)
+            mem = rv.Memory(H, reserve_tokens=M, max_tokens=M + budget)
+            mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+            Qd, Kd, Vd = to_dev(Q), to_dev(K), to_dev(V)
+            out = torch.empty_like(Qd)
+            lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
+            sal = torch.empty((H, N), dtype=torch.float32, device="cuda")
+            idx = torch.empty((H, budget), dtype=torch.int32, device="cuda")
+            if batched:
+                rv.attend_frame(Qd, Kd, Vd, mem, out, lse)
+            else:
+                rv.attend_frame(Qd, Kd, Vd, mem, out, lse, sal, qs)
+                rv.admit(sal, budget, Kd, Vd, mem, 9, idx)
+            mems.append((mem, Qd, Kd, Vd, lse))
+            sals.append(sal)
+            idxs.append(idx)
+        if batched:
+            rv.admit_layers([m[1] for m in mems], [m[2] for m in mems], [m[3] for m in mems],
+                            [m[4] for m in mems], qs, budget, [m[0] for m in mems], 9, sals, idxs)
+        torch.cuda.synchronize()
+        results.append(([s.cpu() for s in sals], [i.cpu() for i in idxs],
+                        [m[0].read() for m in mems]))
+        for m in mems:
+            m[0].close()
+    (sa, ia, ma), (sb, ib, mb) = results
+    for l in range(L):
+        assert (sa[l] == sb[l]).all()
+        assert (ia[l] == ib[l]).all()
+        assert all((x == y).all() for x, y in zip(ma[l], mb[l]))
+
+
+def test_gpu_generator_matches_cpu_generator(rv):
+    """The benchmark's GPU-side generator reproduces the CPU generator's bits."""
+    import torch
+    for name, frame_id in (("tiny", 3), ("vitl_layer", 17)):
+        cfg = synth.CONFIGS[name]
+        out = torch.empty((cfg.n_layers, 3, cfg.n_tokens, cfg.n_heads, 64), dtype=torch.int16, device="cuda")
+        rv.gpu_frame_qkv(cfg, frame_id, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().view(np.uint16)
+        Q, K, V = synth.frame_qkv(cfg, 0, frame_id)
+        assert (got[0, 0] == Q).all() and (got[0, 2] == V).all()
+        assert (got[0, 1] == K).all()
