@@ -9,6 +9,13 @@ SAL_RTOL = 1e-3      # saliency, relative, every key
 BAND = 1e-4          # relative band around the k-th largest oracle saliency
 
 
+def out_error_bound(out_oracle, v_absmax):
+    """Worst-case error of a bf16 attention output: the probabilities are rounded to
+    bf16 (relative error <= 2^-8 each, so <= 2^-8 max|v| after normalisation) and the
+    output is rounded to bf16 (<= 2^-8 |o|); fp32 accumulation adds ~1e-6."""
+    return 2.0 ** -8 * (float(np.abs(out_oracle).max()) + float(v_absmax)) + 1e-5
+
+
 def to_dev(a):
     import torch
     a = np.ascontiguousarray(a)
