@@ -180,6 +180,7 @@ def main():
         run_frame(t, events[t])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
+    rv.device_status()
     assert all(m.len == T * k for m in mems)
 
     attn_ms = sum(e[0].elapsed_time(e[1]) for e in events)

@@ -161,6 +161,12 @@ rv_status rv_admit_layers(int n_layers, const void *const *Q, const void *const 
                           const rv_qsub *qs, int budget, const rv_mem *mems, int frame_id,
                           float *const *saliency_out, int32_t *const *idx_out, void *stream);
 
+/* Synchronises the current device and reports, then clears, the status bits the
+ * library's kernels raise: RV_OK, or RV_ERR_HIP with rv_last_error() naming the
+ * condition (a workgroup ran on an XCD the library's placement probe never saw, or an
+ * attention launch ended with work undone).  Test harnesses call it after each step. */
+rv_status rv_device_status(void);
+
 /* Pre-allocates the current device's scratch workspace (split-KV partial results,
  * saliency staging, completion counters) for frames of up to n_tokens tokens with
  * n_heads heads, and up to n_layers layers per rv_admit_layers call, so that later

@@ -6,293 +6,391 @@
 //   LSE_i = log sum_c exp(z_ic),  o_i = sum_c exp(z_ic - LSE_i) v_c.
 //
 // Design (CDNA4):
-// * A workgroup is 4 wave64s and owns 128 queries of one head (32 per wave).  K/V tiles
-//   of 64 keys are staged in LDS: K row-major, V transposed, both with padded rows.
-// * Scores are formed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16, so that
-//   each lane holds one query's column: the softmax max / sum are in-lane reductions
-//   plus one exchange between the two 32-lane halves that share a query.
-// * The output is accumulated transposed too, O^T += V^T P^T, with P^T taken straight
-//   from the score registers: the 16 accumulator rows a lane holds are exactly the 8+8
-//   keys the B operand wants, once V^T's columns are stored in the matching order.
-// * Online softmax in base 2 with the 1/sqrt(d) scale folded into one FMA; the running
-//   maximum is only raised when a tile's maximum exceeds it by more than 2^8, so the
-//   rescale of the accumulators is rare (exact in any case: the LSE uses the maximum the
-//   sums were taken against).
-// * Split-KV: (head, query tile) pairs alone cannot fill 256 CUs (1041 tokens x 16 heads
-//   is 144 workgroups), so the key tiles are cut into n_splits ranges.  Every split
-//   writes an unnormalised partial (O, max, sum); the last workgroup of a query tile to
-//   finish (atomic counter) merges all partials in split order, so the result does not
-//   depend on scheduling.
-// * Workgroup ids are remapped so that consecutive work items (same head) run on the
-//   same XCD and share that head's K/V in the XCD's L2.
+// * Work unit = (head, 128-query tile); 4 wave64s, 32 queries each.  Key/value tiles of
+//   64 rows are staged in LDS, row-major with 144-byte rows, double-buffered: the next
+//   tile's global loads are in flight while the current one is computed.
+// * Scores are formed transposed, S^T = K Q^T (v_mfma_f32_32x32x16_bf16), so each lane
+//   owns one query column: softmax max/sum are in-lane plus one exchange between the
+//   two 32-lane halves sharing a query.  The output is accumulated transposed too,
+//   O^T += V^T P^T: P^T is the score accumulator itself (its 16 rows per lane are the
+//   8+8 keys the B operand wants), and V^T comes straight from the row-major V tile
+//   through ds_read_b64_tr_b16 transposing reads.
+// * Online softmax in base 2 with 1/sqrt(64) folded into one FMA; the running maximum
+//   is raised only when a tile exceeds it by more than 2^8, so accumulator rescales are
+//   rare (exact either way: the LSE uses the maximum the sums were taken against).
+// * Scheduling: 1041 queries x 16 heads is only 144 units, too few for 256 CUs, so each
+//   unit's key range is split (stream-K).  Units are dealt to one queue per XCD; a
+//   workgroup reads the XCC id it runs on and takes fixed-size chunks of (unit, key
+//   tile) iterations from that XCD's queue only.  All partial results of a unit are
+//   thus written and merged under one L2: a contributor waits for its stores to reach
+//   L2 and bumps the unit's counter; the last contributor merges the partials in chunk
+//   order (deterministic).  No device-wide cache flush is needed.
 #include "rv_internal.h"
 
 namespace rv {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int BQ = kAttnBQ;
 constexpr int BK = kAttnBK;
 constexpr int D = kHeadDim;
-constexpr int LDS_STRIDE = D + 8;  // 144-byte rows: 16-byte lane reads hit distinct banks
+constexpr int LDS_STRIDE = D + 8;               // 144-byte rows
+constexpr int TILE = BK * LDS_STRIDE;           // one K or V tile, in bf16 elements
+constexpr int STAGE = 2 * TILE;                 // K tile then V tile
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kScaleLog2 = 1.44269504088896341f * 0.125f;  // log2(e) / sqrt(64)
-constexpr float kRescaleSlack = 8.0f;   // allow p <= 2^8 before raising the running max
+constexpr float kRescaleSlack = 8.0f;
 constexpr float kNegBig = -1.0e30f;
+
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) {
-  return (uint32_t)lo | ((uint32_t)hi << 16);
-}
-
-// Four fp32 -> bf16 (round to nearest even), packed into two dwords.
 __device__ __forceinline__ uint2 to_bf16x4(float a, float b, float c, float d) {
   typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
   bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
-  return *reinterpret_cast<uint2*>(&v);
+  return __builtin_bit_cast(uint2, v);
 }
 
-__global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sK[BK * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) uint16_t sVt[D * LDS_STRIDE];
-  __shared__ int s_last;
+__device__ __forceinline__ int hw_xcc_id() { return __builtin_amdgcn_s_getreg((3 << 11) | 20) & 15; }
 
-  // XCD-aware remap: hardware deals workgroup ids round-robin over the 8 XCDs.
-  const int bid = blockIdx.x;
-  const int w = (bid & 7) * a.per_xcd + (bid >> 3);
-  if (w >= a.n_work) return;
-  const int split = w % a.n_splits;
-  const int tile_id = w / a.n_splits;  // h * q_tiles + qt
-  const int qt = tile_id % a.q_tiles;
-  const int h = tile_id / a.q_tiles;
+// Where key tile t of head h lives: the memory segment first, then the frame.
+struct TileSrc {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t rs;  // row stride in elements
+  int valid;   // rows present (<= 64)
+};
 
+__device__ __forceinline__ TileSrc tile_src(const AttnArgs& a, int h, int t) {
+  TileSrc s;
+  if (t < a.nt_mem) {
+    const int64_t r0 = (int64_t)t * BK;
+    s.k = a.memK + ((int64_t)h * a.head_stride + r0) * D;
+    s.v = a.memV + ((int64_t)h * a.head_stride + r0) * D;
+    s.rs = D;
+    s.valid = (int)min((int64_t)BK, a.mem_len - r0);
+  } else {
+    const int r0 = (t - a.nt_mem) * BK;
+    s.k = a.K + ((int64_t)r0 * a.n_heads + h) * D;
+    s.v = a.V + ((int64_t)r0 * a.n_heads + h) * D;
+    s.rs = (int64_t)a.n_heads * D;
+    s.valid = min(BK, a.n_tokens - r0);
+  }
+  return s;
+}
+
+// One thread's share of a tile: rows tid/8 and tid/8 + 32, 16-byte chunk tid % 8.
+struct Staged {
+  uint4 k0, k1, v0, v1;
+};
+
+__device__ __forceinline__ void load_tile(const TileSrc& s, int tid, Staged& st) {
+  const int r = tid >> 3, c = tid & 7;
+  const uint4 z = {0u, 0u, 0u, 0u};
+  st.k0 = r < s.valid ? *reinterpret_cast<const uint4*>(s.k + r * s.rs + c * 8) : z;
+  st.v0 = r < s.valid ? *reinterpret_cast<const uint4*>(s.v + r * s.rs + c * 8) : z;
+  st.k1 = r + 32 < s.valid ? *reinterpret_cast<const uint4*>(s.k + (r + 32) * s.rs + c * 8) : z;
+  st.v1 = r + 32 < s.valid ? *reinterpret_cast<const uint4*>(s.v + (r + 32) * s.rs + c * 8) : z;
+}
+
+__device__ __forceinline__ void store_tile(uint16_t* stage, int tid, const Staged& st) {
+  const int r = tid >> 3, c = tid & 7;
+  *reinterpret_cast<uint4*>(&stage[r * LDS_STRIDE + c * 8]) = st.k0;
+  *reinterpret_cast<uint4*>(&stage[(r + 32) * LDS_STRIDE + c * 8]) = st.k1;
+  *reinterpret_cast<uint4*>(&stage[TILE + r * LDS_STRIDE + c * 8]) = st.v0;
+  *reinterpret_cast<uint4*>(&stage[TILE + (r + 32) * LDS_STRIDE + c * 8]) = st.v1;
+}
+
+struct SoftmaxState {
+  float m;      // running max of z * log2(e) / 8
+  float l;      // this lane's share of the row sum
+  f32x16 o0;    // O^T rows d = 0..31 for this lane's query (accumulator layout)
+  f32x16 o1;    // d = 32..63
+};
+
+// One 64-key tile for this wave's 32 queries.
+__device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8 (&qf)[4], int lane, int valid,
+                                             SoftmaxState& sm) {
+  const int l32 = lane & 31, half = lane >> 5;
+  f32x16 s0 = {}, s1 = {};
+#pragma unroll
+  for (int ds = 0; ds < 4; ++ds) {
+    const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&stage[l32 * LDS_STRIDE + ds * 16 + half * 8]);
+    const bf16x8 kb = *reinterpret_cast<const bf16x8*>(&stage[(32 + l32) * LDS_STRIDE + ds * 16 + half * 8]);
+    s0 = mfma32(ka, qf[ds], s0);
+    s1 = mfma32(kb, qf[ds], s1);
+  }
+  // accumulator entry r of this lane: key 8*(r/4) + 4*half + r%4 (+32 in s1)
+  if (valid < BK) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = 8 * (r >> 2) + 4 * half + (r & 3);
+      if (key >= valid) s0[r] = kNegBig;
+      if (key + 32 >= valid) s1[r] = kNegBig;
+    }
+  }
+  float mx = fmaxf(s0[0], s1[0]);
+#pragma unroll
+  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_cand = mx * kScaleLog2;
+  if (__any(m_cand > sm.m + kRescaleSlack)) {
+    const float m_new = fmaxf(sm.m, m_cand);
+    const float alpha = __builtin_amdgcn_exp2f(sm.m - m_new);
+    sm.l *= alpha;
+    sm.o0 *= alpha;
+    sm.o1 *= alpha;
+    sm.m = m_new;
+  }
+  bf16x8 p[4];
+  float rsum = 0.f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], kScaleLog2, -sm.m));
+    const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], kScaleLog2, -sm.m));
+    rsum += e0 + e1;
+    p[r >> 3][r & 7] = (__bf16)e0;
+    p[2 + (r >> 3)][r & 7] = (__bf16)e1;
+  }
+  sm.l += rsum;
+
+  // V^T operand through transposing LDS reads.  Within each 16-lane group, lane i
+  // receives element i%4 of the 8-byte chunk addressed by lane 4r + i/4 (r = 0..3), so
+  // lane 4r + j points at row (key) r, columns d0 + 4j .. +3: lane i then holds
+  // V[key r][d0 + i] for the 4 keys.  Keys follow the P^T slot order: for k-step ks and
+  // lane half hh, slots 0..3 are keys ks*16 + 4hh + r, slots 4..7 keys ks*16 + 8 + 4hh + r.
+  const uint16_t* vt = stage + TILE;
+  const int g = lane >> 4, i16 = lane & 15, rr = i16 >> 2, jj = i16 & 3, hh = g >> 1;
+  const int col = 16 * (g & 1) + 4 * jj;
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int row = ks * 16 + 4 * hh + rr;
+#pragma unroll
+    for (int db = 0; db < 2; ++db) {
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_i16x4*)(vt + row * LDS_STRIDE + db * 32 + col));
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_i16x4*)(vt + (row + 8) * LDS_STRIDE + db * 32 + col));
+      const i16x8 w = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      const bf16x8 va = __builtin_bit_cast(bf16x8, w);
+      if (db == 0)
+        sm.o0 = mfma32(va, p[ks], sm.o0);
+      else
+        sm.o1 = mfma32(va, p[ks], sm.o1);
+    }
+  }
+}
+
+__device__ __forceinline__ void write_final_lane(const AttnArgs& a, int h, int qi, int half, const SoftmaxState& sm,
+                                                 float l_tot) {
+  const float inv = 1.f / l_tot;
+  uint16_t* op = a.out + ((int64_t)qi * a.n_heads + h) * D + 4 * half;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    *reinterpret_cast<uint2*>(op + 8 * j) =
+        to_bf16x4(sm.o0[4 * j] * inv, sm.o0[4 * j + 1] * inv, sm.o0[4 * j + 2] * inv, sm.o0[4 * j + 3] * inv);
+    *reinterpret_cast<uint2*>(op + 32 + 8 * j) =
+        to_bf16x4(sm.o1[4 * j] * inv, sm.o1[4 * j + 1] * inv, sm.o1[4 * j + 2] * inv, sm.o1[4 * j + 3] * inv);
+  }
+  if (half == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (sm.m + __log2f(l_tot)) * kLn2;
+}
+
+// Merge every partial of `unit` (contributor chunks c_first..c_last of queue q, in
+// chunk order) and write the final output rows and LSE.
+__device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_first, int c_last) {
+  const int tid = threadIdx.x;
+  const int h = unit / a.q_tiles, qt = unit % a.q_tiles;
+  const int row = tid >> 1, dh = (tid & 1) * 32;
+  const int qi = qt * BQ + row;
+  if (qi >= a.n_tokens) return;
+  float mmax = kNegBig;
+  for (int c = c_first; c <= c_last; ++c) {
+    const int slot = 2 * (a.chunk_base[q] + c) + ((int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1);
+    mmax = fmaxf(mmax, a.part[(int64_t)slot * kAttnSlotFloats + BQ * D + row]);
+  }
+  float acc[32];
+#pragma unroll
+  for (int e = 0; e < 32; ++e) acc[e] = 0.f;
+  float L = 0.f;
+  for (int c = c_first; c <= c_last; ++c) {
+    const int slot = 2 * (a.chunk_base[q] + c) + ((int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1);
+    const float* ps = a.part + (int64_t)slot * kAttnSlotFloats;
+    const float w = __builtin_amdgcn_exp2f(ps[BQ * D + row] - mmax);
+    L += w * ps[BQ * D + BQ + row];
+    const float4* po = reinterpret_cast<const float4*>(ps + row * D + dh);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float4 v = po[e];
+      acc[4 * e] += w * v.x;
+      acc[4 * e + 1] += w * v.y;
+      acc[4 * e + 2] += w * v.z;
+      acc[4 * e + 3] += w * v.w;
+    }
+  }
+  const float inv = 1.f / L;
+  uint16_t* op = a.out + ((int64_t)qi * a.n_heads + h) * D + dh;
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    *reinterpret_cast<uint2*>(op + 4 * e) =
+        to_bf16x4(acc[4 * e] * inv, acc[4 * e + 1] * inv, acc[4 * e + 2] * inv, acc[4 * e + 3] * inv);
+  if (dh == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (mmax + __log2f(L)) * kLn2;
+}
+
+__global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+  __shared__ int s_val;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
-  const int N = a.n_tokens, H = a.n_heads;
-  const int q0 = qt * BQ + wave * 32;
-  const int qi = q0 + l32;
-  const bool wave_active = q0 < N;
 
-  // B operand of S^T = K Q^T: this lane's query, head dims ds*16 + half*8 .. +7.
-  bf16x8 qf[4];
-  if (qi < N) {
-    const uint16_t* qp = a.Q + ((int64_t)qi * H + h) * D + half * 8;
-#pragma unroll
-    for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
+  // Counters of the launch two ahead (same ring row as the launch two back) restart.
+  if (blockIdx.x == 0 && tid < kMaxQueues) a.queue_ctr[((a.seq + 2) & 3) * kMaxQueues + tid] = 0;
+  if (blockIdx.x == 0 && tid == kMaxQueues) a.exit_ctr[(a.seq + 2) & 3] = 0ull;
+
+  const int q = a.xcc_queue[hw_xcc_id()];
+  int units_done = 0;
+  if (q < 0) {
+    if (tid == 0) atomicOr(a.err, 1);  // an XCD the host did not map: its share goes to others
   } else {
-#pragma unroll
-    for (int ds = 0; ds < 4; ++ds) qf[ds] = bf16x8{};
-  }
+    int* qctr = a.queue_ctr + (a.seq & 3) * kMaxQueues + q;
+    const int ub = a.unit_base[q];
+    const int total = (a.unit_base[q + 1] - ub) * a.T;
+    for (;;) {
+      if (tid == 0) s_val = atomicAdd(qctr, 1);
+      __syncthreads();
+      const int c = s_val;
+      __syncthreads();
+      if (c >= a.n_chunks[q]) break;
+      const int it0 = c * a.E, it1 = min(total, it0 + a.E);
 
-  const int t_begin = (int)((int64_t)a.nt_total * split / a.n_splits);
-  const int t_end = (int)((int64_t)a.nt_total * (split + 1) / a.n_splits);
+      // segment state
+      int ui = it0 / a.T;
+      int t0 = it0 % a.T;
+      int unit = ub + ui;
+      int h = unit / a.q_tiles, qt = unit % a.q_tiles;
+      int qi = qt * BQ + wave * 32 + l32;
+      bool wave_active = qt * BQ + wave * 32 < a.n_tokens;
+      bf16x8 qf[4];
+      SoftmaxState sm;
 
-  float m_run = kNegBig;  // running max of z * log2(e) / 8
-  float l_run = 0.f;      // this lane's share of the row sum (its 32 of each 64 keys)
-  f32x16 o0 = {}, o1 = {};  // O^T rows d = 0..31 and 32..63 for this lane's query
+      auto begin_segment = [&]() {
+        if (qi < a.n_tokens) {
+          const uint16_t* qp = a.Q + ((int64_t)qi * a.n_heads + h) * D + half * 8;
+#pragma unroll
+          for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
+        } else {
+#pragma unroll
+          for (int ds = 0; ds < 4; ++ds) qf[ds] = bf16x8{};
+        }
+        sm.m = kNegBig;
+        sm.l = 0.f;
+        sm.o0 = f32x16{};
+        sm.o1 = f32x16{};
+      };
+      begin_segment();
 
-  for (int t = t_begin; t < t_end; ++t) {
-    const uint16_t *kbase, *vbase;
-    int64_t rs;
-    int valid;
-    if (t < a.nt_mem) {
-      const int64_t r0 = (int64_t)t * BK;
-      kbase = a.memK + ((int64_t)h * a.head_stride + r0) * D;
-      vbase = a.memV + ((int64_t)h * a.head_stride + r0) * D;
-      rs = D;
-      valid = (int)min((int64_t)BK, a.mem_len - r0);
-    } else {
-      const int r0 = (t - a.nt_mem) * BK;
-      kbase = a.K + ((int64_t)r0 * H + h) * D;
-      vbase = a.V + ((int64_t)r0 * H + h) * D;
-      rs = (int64_t)H * D;
-      valid = min(BK, N - r0);
-    }
+      Staged st;
+      load_tile(tile_src(a, h, t0), tid, st);
+      store_tile(lds, tid, st);
+      __syncthreads();
 
-    __syncthreads();  // previous tile fully consumed
-    {
-      // K tile, row-major: rows tid/8 and tid/8 + 32, 16-byte chunk tid % 8.
-      const int r = tid >> 3, c = tid & 7;
-      uint4 k0 = {0u, 0u, 0u, 0u}, k1 = {0u, 0u, 0u, 0u};
-      if (r < valid) k0 = *reinterpret_cast<const uint4*>(kbase + r * rs + c * 8);
-      if (r + 32 < valid) k1 = *reinterpret_cast<const uint4*>(kbase + (r + 32) * rs + c * 8);
-      *reinterpret_cast<uint4*>(&sK[r * LDS_STRIDE + c * 8]) = k0;
-      *reinterpret_cast<uint4*>(&sK[(r + 32) * LDS_STRIDE + c * 8]) = k1;
-    }
-    {
-      // V tile transposed: wave g takes keys 16g..16g+15, lane = head dim.  Within each
-      // 16-key group, columns 0..7 hold keys {0-3, 8-11} and 8..15 hold {4-7, 12-15}:
-      // the keys the two lane halves carry in the score accumulator.
-      const int d = lane, g = wave;
-      uint16_t v[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = g * 16 + i;
-        v[i] = key < valid ? vbase[key * rs + d] : (uint16_t)0;
-      }
-      uint4 lo, hi;
-      lo.x = pack2(v[0], v[1]);
-      lo.y = pack2(v[2], v[3]);
-      lo.z = pack2(v[8], v[9]);
-      lo.w = pack2(v[10], v[11]);
-      hi.x = pack2(v[4], v[5]);
-      hi.y = pack2(v[6], v[7]);
-      hi.z = pack2(v[12], v[13]);
-      hi.w = pack2(v[14], v[15]);
-      *reinterpret_cast<uint4*>(&sVt[d * LDS_STRIDE + g * 16]) = lo;
-      *reinterpret_cast<uint4*>(&sVt[d * LDS_STRIDE + g * 16 + 8]) = hi;
-    }
-    __syncthreads();
-    if (!wave_active) continue;
+      for (int it = it0; it < it1; ++it) {
+        const int buf = (it - it0) & 1;
+        const int t = it % a.T;
+        const bool has_next = it + 1 < it1;
+        if (has_next) {
+          const int un = ub + (it + 1) / a.T;
+          load_tile(tile_src(a, un / a.q_tiles, (it + 1) % a.T), tid, st);
+        }
+        const TileSrc cur = tile_src(a, h, t);  // only .valid is used
+        if (wave_active) tile_compute(lds + buf * STAGE, qf, lane, cur.valid, sm);
 
-    // S^T (64 keys x 32 queries): s0 keys 0..31, s1 keys 32..63.  Accumulator entry r of
-    // a lane is key 8*(r/4) + 4*half + r%4 (+32 for s1) against query qi.
-    f32x16 s0 = {}, s1 = {};
+        if (t == a.T - 1 || it == it1 - 1) {
+          // end of this chunk's segment of `unit`
+          const float l_tot = sm.l + __shfl_xor(sm.l, 32);
+          if (t0 == 0 && t == a.T - 1) {
+            if (wave_active && qi < a.n_tokens) write_final_lane(a, h, qi, half, sm, l_tot);
+            ++units_done;
+          } else {
+            const int seg = (int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1;
+            float* ps = a.part + (int64_t)(2 * (a.chunk_base[q] + c) + seg) * kAttnSlotFloats;
+            if (wave_active) {
+              const int row = wave * 32 + l32;
+              float* po = ps + row * D + 4 * half;
 #pragma unroll
-    for (int ds = 0; ds < 4; ++ds) {
-      const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&sK[l32 * LDS_STRIDE + ds * 16 + half * 8]);
-      const bf16x8 kb =
-          *reinterpret_cast<const bf16x8*>(&sK[(32 + l32) * LDS_STRIDE + ds * 16 + half * 8]);
-      s0 = mfma32(ka, qf[ds], s0);
-      s1 = mfma32(kb, qf[ds], s1);
-    }
-    if (valid < BK) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = 8 * (r >> 2) + 4 * half + (r & 3);
-        if (key >= valid) s0[r] = kNegBig;
-        if (key + 32 >= valid) s1[r] = kNegBig;
-      }
-    }
-
-    float mx = s0[0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s0[r]);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s1[r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_cand = mx * kScaleLog2;
-    if (__any(m_cand > m_run + kRescaleSlack)) {
-      const float m_new = fmaxf(m_run, m_cand);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-      o0 *= alpha;
-      o1 *= alpha;
-      m_run = m_new;
-    }
-
-    // P = 2^(z*log2e/8 - m), fp32 for the row sum, bf16 for the value product.
-    bf16x8 p[4];
-    float rsum = 0.f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], kScaleLog2, -m_run));
-      const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], kScaleLog2, -m_run));
-      rsum += e0 + e1;
-      p[r >> 3][r & 7] = (__bf16)e0;
-      p[2 + (r >> 3)][r & 7] = (__bf16)e1;
-    }
-    l_run += rsum;
-
-    // O^T (64 dims x 32 queries) += V^T P^T over four 16-key steps.
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const bf16x8 va = *reinterpret_cast<const bf16x8*>(&sVt[l32 * LDS_STRIDE + ks * 16 + half * 8]);
-      const bf16x8 vb =
-          *reinterpret_cast<const bf16x8*>(&sVt[(32 + l32) * LDS_STRIDE + ks * 16 + half * 8]);
-      o0 = mfma32(va, p[ks], o0);
-      o1 = mfma32(vb, p[ks], o1);
-    }
-  }
-
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-
-  if (a.n_splits == 1) {
-    if (wave_active && qi < N) {
-      const float inv = 1.f / l_tot;
-      uint16_t* op = a.out + ((int64_t)qi * H + h) * D + 4 * half;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        *reinterpret_cast<uint2*>(op + 8 * j) =
-            to_bf16x4(o0[4 * j] * inv, o0[4 * j + 1] * inv, o0[4 * j + 2] * inv, o0[4 * j + 3] * inv);
-        *reinterpret_cast<uint2*>(op + 32 + 8 * j) =
-            to_bf16x4(o1[4 * j] * inv, o1[4 * j + 1] * inv, o1[4 * j + 2] * inv, o1[4 * j + 3] * inv);
-      }
-      if (half == 0) a.lse[(int64_t)h * N + qi] = (m_run + __log2f(l_tot)) * kLn2;
-    }
-    return;
-  }
-
-  // ---- split-KV: publish this split's partial, the last split merges ----
-  const int64_t slot = (int64_t)tile_id * a.n_splits + split;
-  if (wave_active) {
-    const int row = wave * 32 + l32;
-    float* po = a.part_o + (slot * BQ + row) * D + 4 * half;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      *reinterpret_cast<float4*>(po + 8 * j) = make_float4(o0[4 * j], o0[4 * j + 1], o0[4 * j + 2], o0[4 * j + 3]);
-      *reinterpret_cast<float4*>(po + 32 + 8 * j) =
-          make_float4(o1[4 * j], o1[4 * j + 1], o1[4 * j + 2], o1[4 * j + 3]);
-    }
-    if (half == 0) {
-      a.part_ml[slot * 2 * BQ + row] = m_run;
-      a.part_ml[slot * 2 * BQ + BQ + row] = l_tot;
-    }
-  }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = atomicAdd(&a.counters[tile_id], 1) == a.n_splits - 1;
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-
-  // Merge, in split order: thread -> (row = tid/2, 32 head dims).
-  const int row = tid >> 1, dh = (tid & 1) * 32;
-  const int q = qt * BQ + row;
-  if (q < N) {
-    const int64_t slot0 = (int64_t)tile_id * a.n_splits;
-    float mmax = kNegBig;
-    for (int s = 0; s < a.n_splits; ++s) mmax = fmaxf(mmax, a.part_ml[(slot0 + s) * 2 * BQ + row]);
-    float acc[32];
-#pragma unroll
-    for (int e = 0; e < 32; ++e) acc[e] = 0.f;
-    float L = 0.f;
-    for (int s = 0; s < a.n_splits; ++s) {
-      const float ms = a.part_ml[(slot0 + s) * 2 * BQ + row];
-      const float ls = a.part_ml[(slot0 + s) * 2 * BQ + BQ + row];
-      const float wgt = __builtin_amdgcn_exp2f(ms - mmax);
-      L += wgt * ls;
-      const float4* po = reinterpret_cast<const float4*>(a.part_o + ((slot0 + s) * BQ + row) * D + dh);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float4 v = po[e];
-        acc[4 * e] += wgt * v.x;
-        acc[4 * e + 1] += wgt * v.y;
-        acc[4 * e + 2] += wgt * v.z;
-        acc[4 * e + 3] += wgt * v.w;
+              for (int j = 0; j < 4; ++j) {
+                *reinterpret_cast<float4*>(po + 8 * j) =
+                    make_float4(sm.o0[4 * j], sm.o0[4 * j + 1], sm.o0[4 * j + 2], sm.o0[4 * j + 3]);
+                *reinterpret_cast<float4*>(po + 32 + 8 * j) =
+                    make_float4(sm.o1[4 * j], sm.o1[4 * j + 1], sm.o1[4 * j + 2], sm.o1[4 * j + 3]);
+              }
+              if (half == 0) {
+                ps[BQ * D + row] = sm.m;
+                ps[BQ * D + BQ + row] = l_tot;
+              }
+            }
+            // release to the XCD's L2 (the vector L1 is write-through)
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            const int c_first = (int)(((int64_t)ui * a.T) / a.E);
+            const int c_last = (int)(((int64_t)(ui + 1) * a.T - 1) / a.E);
+            if (tid == 0) s_val = atomicAdd(&a.unit_ctr[unit], 1) == c_last - c_first;
+            __syncthreads();
+            const bool last = s_val != 0;
+            __syncthreads();
+            if (last) {
+              asm volatile("buffer_inv sc0" ::: "memory");  // no stale vector-L1 lines
+              merge_unit(a, q, unit, ui, c_first, c_last);
+              if (tid == 0) a.unit_ctr[unit] = 0;
+              ++units_done;
+            }
+          }
+          if (has_next) {
+            // next unit of this chunk
+            ++ui;
+            t0 = 0;
+            unit = ub + ui;
+            h = unit / a.q_tiles;
+            qt = unit % a.q_tiles;
+            qi = qt * BQ + wave * 32 + l32;
+            wave_active = qt * BQ + wave * 32 < a.n_tokens;
+            begin_segment();
+          }
+        }
+        if (has_next) store_tile(lds + (buf ^ 1) * STAGE, tid, st);
+        __syncthreads();
       }
     }
-    const float inv = 1.f / L;
-    uint16_t* op = a.out + ((int64_t)q * H + h) * D + dh;
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      *reinterpret_cast<uint2*>(op + 4 * e) =
-          to_bf16x4(acc[4 * e] * inv, acc[4 * e + 1] * inv, acc[4 * e + 2] * inv, acc[4 * e + 3] * inv);
-    if (dh == 0) a.lse[(int64_t)h * N + q] = (mmax + __log2f(L)) * kLn2;
   }
-  if (tid == 0) a.counters[tile_id] = 0;  // ready for the next launch
+  // Completion record: (workgroups exited << 32) + units finished, one atomic per WG.
+  if (tid == 0) {
+    const unsigned long long add = (1ull << 32) + (unsigned long long)units_done;
+    const unsigned long long prev = atomicAdd(&a.exit_ctr[a.seq & 3], add);
+    if ((prev >> 32) == gridDim.x - 1u && (unsigned)((prev + add) & 0xffffffffu) != (unsigned)a.n_units)
+      atomicOr(a.err, 2);  // some unit was never finished
+  }
+}
+
+__global__ void xcc_probe_kernel(int* ids) {
+  if (threadIdx.x == 0) ids[blockIdx.x] = hw_xcc_id();
 }
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(attn_fwd_kernel, dim3(8 * a.per_xcd), dim3(kAttnThreads), 0, s, a);
+hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t s) {
+  hipLaunchKernelGGL(attn_fwd_kernel, dim3(grid), dim3(kAttnThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_xcc_probe(int* ids, int n_blocks, hipStream_t s) {
+  hipLaunchKernelGGL(xcc_probe_kernel, dim3(n_blocks), dim3(64), 0, s, ids);
   return hipGetLastError();
 }
 

@@ -50,16 +50,27 @@ int env_int(const char* name, int dflt) {
   return std::atoi(v);
 }
 
-// ---- per-device scratch workspace ------------------------------------------------
+// ---- per-device context: placement calibration, limits, scratch workspace --------
 struct Workspace {
-  float* part = nullptr;     // split-KV partials (O, then max/sum)
+  bool ready = false;
+  int n_cus = 0;
+  int max_lds = 0;
+  int n_queues = 1;
+  int xcc_queue[16];
+  float* part = nullptr;     // attention partial slots
   size_t part_floats = 0;
-  int* counters = nullptr;   // completion counters, zero between launches
-  size_t n_counters = 0;
+  int* unit_ctr = nullptr;   // attention unit counters (zero between launches)
+  size_t n_unit_ctr = 0;
+  int* ctrl = nullptr;       // queue counters [4][kMaxQueues], exit counters, status bits
+  int seq = 0;               // attention launch sequence number
   float* sal = nullptr;      // saliency staging when the caller passes none
   size_t sal_floats = 0;
   std::map<std::tuple<int, int, int, int>, std::pair<int32_t*, int>> qidx;  // per query subset
 };
+constexpr size_t kCtrlQueueInts = 4 * rv::kMaxQueues;
+constexpr size_t kCtrlExitOffsetBytes = kCtrlQueueInts * 4;        // 4 x uint64
+constexpr size_t kCtrlErrOffsetBytes = kCtrlExitOffsetBytes + 4 * 8;
+constexpr size_t kCtrlBytes = kCtrlErrOffsetBytes + 64;
 
 std::mutex g_ws_mu;
 std::map<int, Workspace> g_ws;
@@ -85,9 +96,6 @@ rv_status grow(T** p, size_t* have, size_t need, bool zero, const char* what) {
       (void)hipFree(q);
       return hip_fail(e, what);
     }
-    if (zero && *have) {
-      // counters carry no state between launches, so nothing to copy
-    }
     (void)hipFree(*p);
   }
   *p = q;
@@ -95,10 +103,45 @@ rv_status grow(T** p, size_t* have, size_t need, bool zero, const char* what) {
   return RV_OK;
 }
 
+// Learns which XCC ids the device's workgroups run on (one work queue per XCC), the
+// CU count and the LDS limit, and allocates the control block.
+rv_status init_device(Workspace* ws, int dev) {
+  if (ws->ready) return RV_OK;
+  RV_HIP(hipDeviceGetAttribute(&ws->n_cus, hipDeviceAttributeMultiprocessorCount, dev), "CU count");
+  RV_HIP(hipDeviceGetAttribute(&ws->max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev), "LDS limit");
+  const int n_probe = 2048;
+  int* d_ids = nullptr;
+  RV_HIP(hipMalloc(&d_ids, n_probe * sizeof(int)), "placement probe");
+  std::vector<int> ids(n_probe, -1);
+  hipError_t e = rv::launch_xcc_probe(d_ids, n_probe, nullptr);
+  if (e == hipSuccess) e = hipMemcpy(ids.data(), d_ids, n_probe * sizeof(int), hipMemcpyDeviceToHost);
+  (void)hipFree(d_ids);
+  if (e != hipSuccess) return hip_fail(e, "placement probe");
+  for (int i = 0; i < 16; ++i) ws->xcc_queue[i] = -1;
+  int nq = 0;
+  for (int i = 0; i < 16; ++i)
+    if (std::find(ids.begin(), ids.end(), i) != ids.end()) ws->xcc_queue[i] = nq++;
+  if (nq == 0) return fail(RV_ERR_HIP, "placement probe saw no XCC id");
+  ws->n_queues = nq;
+  char* ctrl = nullptr;
+  RV_HIP(hipMalloc(&ctrl, kCtrlBytes), "control block");
+  e = hipMemset(ctrl, 0, kCtrlBytes);
+  if (e != hipSuccess) {
+    (void)hipFree(ctrl);
+    return hip_fail(e, "control block");
+  }
+  ws->ctrl = reinterpret_cast<int*>(ctrl);
+  ws->ready = true;
+  return RV_OK;
+}
+
 rv_status current_ws(Workspace** out) {
   int dev = 0;
   RV_HIP(hipGetDevice(&dev), "hipGetDevice");
-  *out = &g_ws[dev];
+  Workspace* ws = &g_ws[dev];
+  rv_status st = init_device(ws, dev);
+  if (st != RV_OK) return st;
+  *out = ws;
   return RV_OK;
 }
 
@@ -120,7 +163,7 @@ rv_status check_qsub(const rv_qsub* qs, int n_tokens) {
   return RV_OK;
 }
 
-rv_status device_qidx(Workspace* ws, const rv_qsub& q, hipStream_t s, const int32_t** ptr, int* n) {
+rv_status device_qidx(Workspace* ws, const rv_qsub& q, const int32_t** ptr, int* n) {
   auto key = std::make_tuple(q.grid_h, q.grid_w, q.n_special, q.stride);
   auto it = ws->qidx.find(key);
   if (it == ws->qidx.end()) {
@@ -136,43 +179,51 @@ rv_status device_qidx(Workspace* ws, const rv_qsub& q, hipStream_t s, const int3
     }
     it = ws->qidx.emplace(key, std::make_pair(d, (int)v.size())).first;
   }
-  (void)s;
   *ptr = it->second.first;
   *n = it->second.second;
   return RV_OK;
 }
 
-// Split-KV plan for one attention launch.
+// Stream-K plan of one attention launch: units (head, 128-query tile) dealt in
+// contiguous ranges to the per-XCD queues; each queue's (unit, key tile) iterations cut
+// into chunks of E tiles, about kAttnWgPerCu chunks per CU.
 struct AttnPlan {
-  int q_tiles, nt_mem, nt_total, n_splits;
+  int q_tiles, nt_mem, T, n_units, E, grid, total_chunks;
+  int unit_base[rv::kMaxQueues + 1];
+  int n_chunks[rv::kMaxQueues];
+  int chunk_base[rv::kMaxQueues];
 };
 
-AttnPlan plan_attention(int n_tokens, int64_t mem_len, int n_heads) {
-  AttnPlan p;
+AttnPlan plan_attention(const Workspace& ws, int n_tokens, int64_t mem_len, int n_heads) {
+  AttnPlan p{};
   p.q_tiles = (int)ceil_div(n_tokens, rv::kAttnBQ);
   p.nt_mem = (int)ceil_div(mem_len, rv::kAttnBK);
-  p.nt_total = p.nt_mem + (int)ceil_div(n_tokens, rv::kAttnBK);
-  const int base = p.q_tiles * n_heads;
-  const int target = env_int("RV_ATTN_TARGET_WGS", 1024);
-  const int min_tiles = std::max(1, env_int("RV_ATTN_MIN_TILES_PER_SPLIT", 2));
-  int s = (int)ceil_div(target, base);
-  s = std::min(s, rv::kMaxSplits);
-  s = std::min(s, std::max(1, p.nt_total / min_tiles));
-  p.n_splits = std::max(1, s);
+  p.T = p.nt_mem + (int)ceil_div(n_tokens, rv::kAttnBK);
+  p.n_units = p.q_tiles * n_heads;
+  const int nq = ws.n_queues;
+  const int wg_per_queue =
+      std::max(1, env_int("RV_ATTN_WG_PER_CU", rv::kAttnWgPerCu) * ws.n_cus / nq);
+  int64_t max_total = 0;
+  for (int q = 0; q <= nq; ++q) p.unit_base[q] = (int)((int64_t)q * p.n_units / nq);
+  for (int q = 0; q < nq; ++q)
+    max_total = std::max<int64_t>(max_total, (int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.T);
+  const int e_min = std::max(1, env_int("RV_ATTN_MIN_CHUNK", 2));
+  p.E = (int)std::max<int64_t>(e_min, ceil_div(max_total, wg_per_queue));
+  p.total_chunks = 0;
+  for (int q = 0; q < nq; ++q) {
+    p.n_chunks[q] = (int)ceil_div((int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.T, p.E);
+    p.chunk_base[q] = p.total_chunks;
+    p.total_chunks += p.n_chunks[q];
+  }
+  p.grid = nq * wg_per_queue;
   return p;
 }
 
-rv_status reserve_attention(Workspace* ws, int n_tokens, int n_heads) {
-  const size_t tiles = (size_t)ceil_div(n_tokens, rv::kAttnBQ) * n_heads;
-  const size_t slots = tiles * rv::kMaxSplits;
-  rv_status st = grow(&ws->part, &ws->part_floats, slots * rv::kAttnBQ * (rv::kHeadDim + 2), false,
+rv_status reserve_attention(Workspace* ws, const AttnPlan& p) {
+  rv_status st = grow(&ws->part, &ws->part_floats, (size_t)2 * p.total_chunks * rv::kAttnSlotFloats, false,
                       "attention workspace");
   if (st != RV_OK) return st;
-  return RV_OK;
-}
-
-rv_status reserve_counters(Workspace* ws, size_t n) {
-  return grow(&ws->counters, &ws->n_counters, n, true, "counter workspace");
+  return grow(&ws->unit_ctr, &ws->n_unit_ctr, (size_t)p.n_units, true, "attention counters");
 }
 
 }  // namespace
@@ -392,14 +443,28 @@ rv_status rv_reserve_workspace(int n_tokens, int n_heads, int n_layers) {
   Workspace* ws;
   rv_status st = current_ws(&ws);
   if (st != RV_OK) return st;
-  st = reserve_attention(ws, n_tokens, n_heads);
+  // the chunk count of a plan does not grow with the context: plan a long one
+  const AttnPlan p = plan_attention(*ws, n_tokens, (int64_t)1 << 20, n_heads);
+  st = reserve_attention(ws, p);
   if (st != RV_OK) return st;
-  const size_t tiles = (size_t)ceil_div(n_tokens, rv::kAttnBQ) * n_heads;
-  const size_t per_launch = std::min<size_t>(n_layers, rv::kMaxLayersPerLaunch) * n_heads;
-  st = reserve_counters(ws, std::max(tiles, per_launch));
+  return grow(&ws->sal, &ws->sal_floats,
+              (size_t)std::min(n_layers, rv::kMaxLayersPerLaunch) * n_heads * n_tokens, false, "saliency workspace");
+}
+
+rv_status rv_device_status(void) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace* ws;
+  rv_status st = current_ws(&ws);
   if (st != RV_OK) return st;
-  return grow(&ws->sal, &ws->sal_floats, (size_t)std::min(n_layers, rv::kMaxLayersPerLaunch) * n_heads * n_tokens,
-              false, "saliency workspace");
+  RV_HIP(hipDeviceSynchronize(), "device synchronisation");
+  int bits = 0;
+  char* err = reinterpret_cast<char*>(ws->ctrl) + kCtrlErrOffsetBytes;
+  RV_HIP(hipMemcpy(&bits, err, sizeof bits, hipMemcpyDeviceToHost), "status read");
+  if (bits == 0) return RV_OK;
+  RV_HIP(hipMemset(err, 0, sizeof bits), "status reset");
+  return fail(RV_ERR_HIP, "device status 0x%x:%s%s", bits,
+              (bits & 1) ? " a workgroup ran on an XCC the placement probe had not seen;" : "",
+              (bits & 2) ? " an attention launch finished with units left undone" : "");
 }
 
 rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
@@ -427,15 +492,13 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   rv_status st = current_ws(&ws);
   if (st != RV_OK) return st;
 
-  const AttnPlan p = plan_attention(n_tokens, mem_len, n_heads);
-  st = reserve_attention(ws, n_tokens, n_heads);
-  if (st != RV_OK) return st;
-  st = reserve_counters(ws, (size_t)p.q_tiles * n_heads);
+  const AttnPlan p = plan_attention(*ws, n_tokens, mem_len, n_heads);
+  st = reserve_attention(ws, p);
   if (st != RV_OK) return st;
   const int32_t* qidx = nullptr;
   int n_q = 0;
   if (saliency) {
-    st = device_qidx(ws, *qs, s, &qidx, &n_q);
+    st = device_qidx(ws, *qs, &qidx, &n_q);
     if (st != RV_OK) return st;
   }
 
@@ -449,18 +512,28 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   a.head_stride = head_stride_tokens;
   a.out = (uint16_t*)out;
   a.lse = lse;
-  a.part_o = ws->part;
-  a.part_ml = ws->part + (size_t)p.q_tiles * n_heads * rv::kMaxSplits * rv::kAttnBQ * rv::kHeadDim;
-  a.counters = ws->counters;
+  a.part = ws->part;
+  a.unit_ctr = ws->unit_ctr;
+  a.queue_ctr = ws->ctrl;
+  a.exit_ctr = reinterpret_cast<unsigned long long*>(reinterpret_cast<char*>(ws->ctrl) + kCtrlExitOffsetBytes);
+  a.err = reinterpret_cast<int*>(reinterpret_cast<char*>(ws->ctrl) + kCtrlErrOffsetBytes);
   a.n_tokens = n_tokens;
   a.n_heads = n_heads;
   a.q_tiles = p.q_tiles;
-  a.n_splits = p.n_splits;
   a.nt_mem = p.nt_mem;
-  a.nt_total = p.nt_total;
-  a.n_work = p.q_tiles * n_heads * p.n_splits;
-  a.per_xcd = (int)ceil_div(a.n_work, 8);
-  RV_HIP(rv::launch_attention(a, s), "attention launch");
+  a.T = p.T;
+  a.n_units = p.n_units;
+  a.n_queues = ws->n_queues;
+  a.E = p.E;
+  a.seq = ws->seq;
+  for (int q = 0; q <= ws->n_queues; ++q) a.unit_base[q] = p.unit_base[q];
+  for (int q = 0; q < ws->n_queues; ++q) {
+    a.n_chunks[q] = p.n_chunks[q];
+    a.chunk_base[q] = p.chunk_base[q];
+  }
+  for (int i = 0; i < 16; ++i) a.xcc_queue[i] = ws->xcc_queue[i];
+  RV_HIP(rv::launch_attention(a, p.grid, s), "attention launch");
+  ws->seq = (ws->seq + 1) & 0x3fffffff;
 
   if (saliency) {
     rv::AdmitArgs b{};
@@ -473,9 +546,10 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
     b.n_tokens = n_tokens;
     b.n_heads = n_heads;
     b.n_layers = 1;
-    b.key_chunks = (int)ceil_div(n_tokens, rv::kSalBK);
     b.mode = rv::kModeSaliency;
-    RV_HIP(rv::launch_admit(b, s), "saliency launch");
+    b.stage_queries = 1;
+    if (rv::admit_lds_bytes(b) > (size_t)rv::admit_max_dynamic_lds(ws->max_lds)) b.stage_queries = 0;
+    RV_HIP(rv::launch_admit(b, ws->max_lds, s), "saliency launch");
   }
   return RV_OK;
 }
@@ -492,6 +566,10 @@ rv_status rv_admit(const float* saliency, int budget, const void* K, const void*
   if (st != RV_OK) return st;
   if (budget == 0) return RV_OK;
   hipStream_t s = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace* ws;
+  st = current_ws(&ws);
+  if (st != RV_OK) return st;
   st = arena_reserve(m, m->len + budget, s);
   if (st != RV_OK) return st;
 
@@ -511,7 +589,9 @@ rv_status rv_admit(const float* saliency, int budget, const void* K, const void*
   b.budget = budget;
   b.frame_id = frame_id;
   b.mode = rv::kModeSelect;
-  RV_HIP(rv::launch_admit(b, s), "admit launch");
+  if (rv::admit_lds_bytes(b) > (size_t)rv::admit_max_dynamic_lds(ws->max_lds))
+    return fail(RV_ERR_INVALID, "frame too large for the selection workgroup's LDS");
+  RV_HIP(rv::launch_admit(b, ws->max_lds, s), "admit launch");
   m->len += budget;
   return RV_OK;
 }
@@ -543,28 +623,36 @@ rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const*
   Workspace* ws;
   st = current_ws(&ws);
   if (st != RV_OK) return st;
-  // growth first, for every layer, before anything is enqueued
-  for (int l = 0; l < n_layers; ++l) {
-    st = arena_reserve(mems[l], mems[l]->len + budget, s);
-    if (st != RV_OK) return st;
-  }
-  const int chunk_layers = std::min(n_layers, rv::kMaxLayersPerLaunch);
-  st = reserve_counters(ws, (size_t)chunk_layers * H);
+  const int32_t* qidx = nullptr;
+  int n_q = 0;
+  st = device_qidx(ws, *qs, &qidx, &n_q);
   if (st != RV_OK) return st;
+  rv::AdmitArgs probe{};
+  probe.n_tokens = n_tokens;
+  probe.n_q = n_q;
+  probe.budget = budget;
+  probe.mode = rv::kModeBoth;
+  probe.stage_queries = 1;
+  const size_t lds_cap = (size_t)rv::admit_max_dynamic_lds(ws->max_lds);
+  if (rv::admit_lds_bytes(probe) > lds_cap) probe.stage_queries = 0;
+  if (rv::admit_lds_bytes(probe) > lds_cap)
+    return fail(RV_ERR_INVALID, "frame too large for the admission workgroup's LDS");
+  const int chunk_layers = std::min(n_layers, rv::kMaxLayersPerLaunch);
   bool need_ws_sal = !saliency_out;
   for (int l = 0; saliency_out && l < n_layers; ++l) need_ws_sal |= !saliency_out[l];
   if (need_ws_sal) {
     st = grow(&ws->sal, &ws->sal_floats, (size_t)chunk_layers * H * n_tokens, false, "saliency workspace");
     if (st != RV_OK) return st;
   }
-  const int32_t* qidx = nullptr;
-  int n_q = 0;
-  st = device_qidx(ws, *qs, s, &qidx, &n_q);
-  if (st != RV_OK) return st;
+  // growth for every layer before anything is enqueued
+  for (int l = 0; l < n_layers; ++l) {
+    st = arena_reserve(mems[l], mems[l]->len + budget, s);
+    if (st != RV_OK) return st;
+  }
 
   for (int l0 = 0; l0 < n_layers; l0 += rv::kMaxLayersPerLaunch) {
     const int nl = std::min(rv::kMaxLayersPerLaunch, n_layers - l0);
-    rv::AdmitArgs b{};
+    rv::AdmitArgs b = probe;
     for (int i = 0; i < nl; ++i) {
       const int l = l0 + i;
       rv::AdmitLayer& L = b.layer[i];
@@ -581,16 +669,10 @@ rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const*
       L.head_stride = mems[l]->cap;
     }
     b.qidx = qidx;
-    b.counters = ws->counters;
-    b.n_q = n_q;
-    b.n_tokens = n_tokens;
     b.n_heads = H;
     b.n_layers = nl;
-    b.budget = budget;
     b.frame_id = frame_id;
-    b.key_chunks = (int)ceil_div(n_tokens, rv::kSalBK);
-    b.mode = rv::kModeBoth;
-    RV_HIP(rv::launch_admit(b, s), "admit_layers launch");
+    RV_HIP(rv::launch_admit(b, ws->max_lds, s), "admit_layers launch");
   }
   for (int l = 0; l < n_layers; ++l) mems[l]->len += budget;
   return RV_OK;

@@ -12,11 +12,20 @@ constexpr int kAttnBK = 64;      // keys per staged K/V tile
 constexpr int kAttnThreads = 256;
 constexpr int kMaxSplits = 16;   // split-KV partitions per (head, query tile)
 constexpr int kSalBK = 128;      // keys per saliency workgroup (4 waves x 32)
-constexpr int kAdmitThreads = 256;
+constexpr int kAdmitThreads = 512;   // one workgroup per (layer, head)
 constexpr int kMaxTokens = 16384;  // frame size limit (LDS-resident sampled queries and selected indices)
 constexpr int kMaxLayersPerLaunch = 24;
 
-// Attention forward with per-query LSE over [memory ; frame].
+constexpr int kMaxQueues = 16;     // work queues (one per XCD) in the attention kernel
+constexpr int kAttnWgPerCu = 2;    // attention workgroups resident per CU
+
+// Attention forward with per-query LSE over [memory ; frame], XCD-local stream-K.
+//
+// A unit is (head, 128-query tile); its context is T key tiles of 64 keys.  Units are
+// dealt to per-XCD queues (contiguous unit ranges); each queue's (unit, key tile)
+// iteration space is cut into chunks of E tiles.  A workgroup reads the id of the XCD it
+// runs on and takes chunks from that XCD's queue only, so every partial result of a
+// unit is produced and merged under one L2.
 struct AttnArgs {
   const uint16_t* Q;       // [N][H][64]
   const uint16_t* K;
@@ -27,18 +36,26 @@ struct AttnArgs {
   int64_t head_stride;
   uint16_t* out;           // [N][H][64]
   float* lse;              // [H][N]
-  float* part_o;           // [H*q_tiles][n_splits][BQ][64] fp32, unnormalised
-  float* part_ml;          // [H*q_tiles][n_splits][2][BQ]: running max (log2 units), row sum
-  int* counters;           // [H*q_tiles] split completion counters, self-resetting
+  float* part;             // partial slots, kAttnSlotFloats each
+  int* unit_ctr;           // [n_units] contributor counters, zero between launches
+  int* queue_ctr;          // [4][kMaxQueues] chunk counters; launch `seq` uses row seq%4
+  unsigned long long* exit_ctr;  // [4]: (workgroups exited << 32) + units finished
+  int* err;                // device status bits (see rv_device_status)
   int n_tokens;
   int n_heads;
   int q_tiles;
-  int n_splits;
-  int nt_mem;              // key tiles in the memory segment
-  int nt_total;            // nt_mem + key tiles in the frame segment
-  int n_work;              // H * q_tiles * n_splits
-  int per_xcd;             // workgroups mapped to each XCD (grid = 8 * per_xcd)
+  int nt_mem;              // key tiles of the memory segment
+  int T;                   // key tiles per unit (memory + frame)
+  int n_units;             // n_heads * q_tiles
+  int n_queues;
+  int E;                   // key tiles per chunk
+  int seq;                 // launch sequence number
+  int unit_base[kMaxQueues + 1];
+  int n_chunks[kMaxQueues];
+  int chunk_base[kMaxQueues];
+  int xcc_queue[16];       // hardware XCC id -> queue, -1 if unmapped
 };
+constexpr int kAttnSlotFloats = kAttnBQ * kHeadDim + 2 * kAttnBQ;
 
 // One layer's share of the saliency / selection / append kernel.
 struct AdmitLayer {
@@ -58,24 +75,32 @@ struct AdmitLayer {
 enum AdmitMode : int {
   kModeSaliency = 1,       // saliency only
   kModeSelect = 2,         // selection + append from a given saliency
-  kModeBoth = 3,           // saliency, then the last workgroup of a head selects + appends
+  kModeBoth = 3,           // saliency, then selection + append, in one workgroup per (layer, head)
 };
 
 struct AdmitArgs {
   AdmitLayer layer[kMaxLayersPerLaunch];
   const int32_t* qidx;     // [n_q] sampled query positions
-  int* counters;           // [n_layers*H], self-resetting
   int n_q;
   int n_tokens;
   int n_heads;
   int n_layers;
   int budget;
   int frame_id;
-  int key_chunks;          // ceil(N / kSalBK)
   int mode;
+  int stage_queries;       // stage the sampled query rows in LDS
 };
 
-hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
-hipError_t launch_admit(const AdmitArgs& a, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t s);
+// Records the hardware XCC id of each of n_blocks workgroups into ids (device memory).
+hipError_t launch_xcc_probe(int* ids, int n_blocks, hipStream_t s);
+// Dynamic LDS bytes the admission kernel needs for these arguments, and the most it may
+// use on a device whose per-workgroup LDS limit is max_lds (room is left for the
+// kernel's static LDS).
+constexpr int kAdmitStaticLdsMargin = 4096;
+size_t admit_lds_bytes(const AdmitArgs& a);
+int admit_max_dynamic_lds(int max_lds);
+// max_lds: the device's LDS limit per workgroup (bytes), for the kernel attribute.
+hipError_t launch_admit(const AdmitArgs& a, int max_lds, hipStream_t s);
 
 }  // namespace rv

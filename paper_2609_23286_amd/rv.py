@@ -54,6 +54,7 @@ def _load():
         "rv_admit": ([vp, i32, vp, vp, i32, vp, i32, vp, vp], i32),
         "rv_admit_layers": ([i32, P(vp), P(vp), P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp), vp], i32),
         "rv_reserve_workspace": ([i32, i32, i32], i32),
+        "rv_device_status": ([], i32),
     }
     for name, (args, res) in sigs.items():
         f = getattr(lib, name)
@@ -110,6 +111,11 @@ def qsub(grid_h, grid_w, n_special, stride):
 
 def reserve_workspace(n_tokens, n_heads, n_layers=1):
     _check(_lib.rv_reserve_workspace(n_tokens, n_heads, n_layers))
+
+
+def device_status():
+    """Synchronise the device; raise RVError if a kernel raised a status bit."""
+    _check(_lib.rv_device_status())
 
 
 class Memory:

@@ -48,7 +48,7 @@ def run_attend(rv, Q, K, V, memK, memV, qs, with_saliency=True):
     lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
     sal = torch.empty((H, N), dtype=torch.float32, device="cuda") if with_saliency else None
     rv.attend_frame(Qd, Kd, Vd, mem, out, lse, sal, qs)
-    torch.cuda.synchronize()
+    rv.device_status()
     res = (bf16_to_f64(to_host_u16(out)), lse.cpu().numpy().astype(np.float64),
            None if sal is None else sal.cpu().numpy().astype(np.float64))
     mem.close()
@@ -90,11 +90,12 @@ def test_attend_and_saliency_match_oracle(rv, N, H, M, sigma):
     assert (np.abs(sal - sal_o) <= SAL_RTOL * sal_o).all()
 
 
-@pytest.mark.parametrize("target", ["1", "64", "100000"])
-def test_split_kv_partitions_agree_with_oracle(rv, target, monkeypatch):
-    """The split-KV plan (one split, a few, the maximum) changes only rounding order."""
-    monkeypatch.setenv("RV_ATTN_TARGET_WGS", target)
-    monkeypatch.setenv("RV_ATTN_MIN_TILES_PER_SPLIT", "1")
+@pytest.mark.parametrize("wg_per_cu,min_chunk", [("1", "1"), ("2", "2"), ("4", "1"), ("1", "100000")])
+def test_stream_k_plans_agree_with_oracle(rv, wg_per_cu, min_chunk, monkeypatch):
+    """Stream-K plans (chunks of one key tile, of a few, whole units) change only the
+    rounding order of the partial merges."""
+    monkeypatch.setenv("RV_ATTN_WG_PER_CU", wg_per_cu)
+    monkeypatch.setenv("RV_ATTN_MIN_CHUNK", min_chunk)
     N, H, M = 333, 4, 1500
     Q, K, V = frame(7, N, H)
     memK, memV = memory_rows(8, H, M)
@@ -134,7 +135,7 @@ def test_admit_matches_oracle_topk_on_given_saliency(rv, N, H, budget):
     mem.write(torch.from_numpy(pre[0].view(np.int16)), torch.from_numpy(pre[1].view(np.int16)), frame_id=-1)
     idx = torch.full((H, budget), -7, dtype=torch.int32, device="cuda")
     rv.admit(to_dev(sal), budget, to_dev(K), to_dev(V), mem, 42, idx)
-    torch.cuda.synchronize()
+    rv.device_status()
     ref = oracle.topk(sal.astype(np.float64), budget)
     got = idx.cpu().numpy()
     assert (got == ref).all()

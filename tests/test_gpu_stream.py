@@ -37,7 +37,7 @@ def gpu_frame_step(rv, mem, Q, K, V, qs, budget, frame_id):
     idx = torch.empty((H, budget), dtype=torch.int32, device="cuda")
     rv.attend_frame(Qd, Kd, Vd, mem, out, lse, sal, qs)
     rv.admit(sal, budget, Kd, Vd, mem, frame_id, idx)
-    torch.cuda.synchronize()
+    rv.device_status()
     return (bf16_to_f64(to_host_u16(out)), lse.cpu().numpy().astype(np.float64),
             sal.cpu().numpy().astype(np.float64), idx.cpu().numpy())
 
