@@ -15,10 +15,12 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-result",
 ]
+# The kernels take finite inputs: no NaN-quieting canonicalisation around min/max.
+KERNEL_FLAGS = ["-fno-honor-nans", "-Xarch_device", "-mno-amdgpu-ieee"]
 
 
-def _hipcc(out, sources, verbose):
-    cmd = ["hipcc", *HIPCC_FLAGS, "-o", out + ".tmp", *sources]
+def _hipcc(out, sources, verbose, extra=()):
+    cmd = ["hipcc", *HIPCC_FLAGS, *extra, "-o", out + ".tmp", *sources]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
@@ -26,7 +28,8 @@ def _hipcc(out, sources, verbose):
 
 
 def build(verbose: bool = False):
-    _hipcc(LIB, [os.path.join(CSRC, f) for f in ("rv_host.cpp", "attend.hip", "admit.hip")], verbose)
+    _hipcc(LIB, [os.path.join(CSRC, f) for f in ("rv_host.cpp", "attend.hip", "admit.hip")], verbose,
+           KERNEL_FLAGS)
     _hipcc(SYNTH_LIB, [os.path.join(CSRC, "synth_gpu.hip")], verbose)
     return LIB, SYNTH_LIB
 

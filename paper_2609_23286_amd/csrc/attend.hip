@@ -60,44 +60,61 @@ __device__ __forceinline__ uint2 to_bf16x4(float a, float b, float c, float d) {
 
 __device__ __forceinline__ int hw_xcc_id() { return __builtin_amdgcn_s_getreg((3 << 11) | 20) & 15; }
 
-// Where key tile t of head h lives: the memory segment first, then the frame.
-struct TileSrc {
-  const uint16_t* k;
-  const uint16_t* v;
-  int64_t rs;  // row stride in elements
-  int valid;   // rows present (<= 64)
-};
-
-__device__ __forceinline__ TileSrc tile_src(const AttnArgs& a, int h, int t) {
-  TileSrc s;
-  if (t < a.nt_mem) {
-    const int64_t r0 = (int64_t)t * BK;
-    s.k = a.memK + ((int64_t)h * a.head_stride + r0) * D;
-    s.v = a.memV + ((int64_t)h * a.head_stride + r0) * D;
-    s.rs = D;
-    s.valid = (int)min((int64_t)BK, a.mem_len - r0);
-  } else {
-    const int r0 = (t - a.nt_mem) * BK;
-    s.k = a.K + ((int64_t)r0 * a.n_heads + h) * D;
-    s.v = a.V + ((int64_t)r0 * a.n_heads + h) * D;
-    s.rs = (int64_t)a.n_heads * D;
-    s.valid = min(BK, a.n_tokens - r0);
-  }
-  return s;
+// Partner value of the other 32-lane half (lane l <-> l ^ 32): v_permlane32_swap returns
+// the two halves exchanged between its operands, so the pair holds {own, partner} in
+// some order on every lane; sums and maxima over the pair need no lane test.
+__device__ __forceinline__ float half_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// One thread's share of a tile: rows tid/8 and tid/8 + 32, 16-byte chunk tid % 8.
+// Key/value rows of one head: the memory segment (row stride 64) followed by the frame
+// (row stride H*64).
+struct HeadSrc {
+  const uint16_t* km;
+  const uint16_t* vm;
+  const uint16_t* kc;
+  const uint16_t* vc;
+  int64_t cur_rs;
+};
+
+// One thread's share of a tile: rows tid/8 and tid/8 + 32, 16-byte chunk tid % 8.  Rows
+// past the end of the segment re-read its last row (always in bounds); their scores are
+// masked, so their contents never matter.
 struct Staged {
   uint4 k0, k1, v0, v1;
 };
 
-__device__ __forceinline__ void load_tile(const TileSrc& s, int tid, Staged& st) {
+__device__ __forceinline__ int tile_valid(const AttnArgs& a, int t) {
+  return t < a.nt_mem ? (int)min((int64_t)BK, a.mem_len - (int64_t)t * BK)
+                      : min(BK, a.n_tokens - (t - a.nt_mem) * BK);
+}
+
+__device__ __forceinline__ Staged load_tile(const AttnArgs& a, const HeadSrc& hs, int t, int tid) {
   const int r = tid >> 3, c = tid & 7;
-  const uint4 z = {0u, 0u, 0u, 0u};
-  st.k0 = r < s.valid ? *reinterpret_cast<const uint4*>(s.k + r * s.rs + c * 8) : z;
-  st.v0 = r < s.valid ? *reinterpret_cast<const uint4*>(s.v + r * s.rs + c * 8) : z;
-  st.k1 = r + 32 < s.valid ? *reinterpret_cast<const uint4*>(s.k + (r + 32) * s.rs + c * 8) : z;
-  st.v1 = r + 32 < s.valid ? *reinterpret_cast<const uint4*>(s.v + (r + 32) * s.rs + c * 8) : z;
+  const int valid = tile_valid(a, t);
+  const int r0 = min(r, valid - 1), r1 = min(r + 32, valid - 1);
+  const uint16_t *kb, *vb;
+  int64_t rs;
+  if (t < a.nt_mem) {
+    kb = hs.km + (int64_t)t * BK * D;
+    vb = hs.vm + (int64_t)t * BK * D;
+    rs = D;
+  } else {
+    kb = hs.kc + (int64_t)(t - a.nt_mem) * BK * hs.cur_rs;
+    vb = hs.vc + (int64_t)(t - a.nt_mem) * BK * hs.cur_rs;
+    rs = hs.cur_rs;
+  }
+  Staged st;
+  st.k0 = *reinterpret_cast<const uint4*>(kb + r0 * rs + c * 8);
+  st.k1 = *reinterpret_cast<const uint4*>(kb + r1 * rs + c * 8);
+  st.v0 = *reinterpret_cast<const uint4*>(vb + r0 * rs + c * 8);
+  st.v1 = *reinterpret_cast<const uint4*>(vb + r1 * rs + c * 8);
+  return st;
 }
 
 __device__ __forceinline__ void store_tile(uint16_t* stage, int tid, const Staged& st) {
@@ -129,18 +146,20 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
   }
   // accumulator entry r of this lane: key 8*(r/4) + 4*half + r%4 (+32 in s1)
   if (valid < BK) {
+    // keys >= valid get -1e30: sat(key + 1 - valid) is 1 exactly for them, 0 otherwise
+    // (arithmetic masking keeps the 32 lane masks out of scalar registers)
+    const float fv = (float)(valid - 4 * half - 1);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int key = 8 * (r >> 2) + 4 * half + (r & 3);
-      if (key >= valid) s0[r] = kNegBig;
-      if (key + 32 >= valid) s1[r] = kNegBig;
+      const float key = (float)(8 * (r >> 2) + (r & 3));
+      s0[r] = fmaf(__saturatef(key - fv), kNegBig, s0[r]);
+      s1[r] = fmaf(__saturatef(key + 32.0f - fv), kNegBig, s1[r]);
     }
   }
   float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
   for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_cand = mx * kScaleLog2;
+  const float m_cand = half_max(mx) * kScaleLog2;
   if (__any(m_cand > sm.m + kRescaleSlack)) {
     const float m_new = fmaxf(sm.m, m_cand);
     const float alpha = __builtin_amdgcn_exp2f(sm.m - m_new);
@@ -188,20 +207,6 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
   }
 }
 
-__device__ __forceinline__ void write_final_lane(const AttnArgs& a, int h, int qi, int half, const SoftmaxState& sm,
-                                                 float l_tot) {
-  const float inv = 1.f / l_tot;
-  uint16_t* op = a.out + ((int64_t)qi * a.n_heads + h) * D + 4 * half;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    *reinterpret_cast<uint2*>(op + 8 * j) =
-        to_bf16x4(sm.o0[4 * j] * inv, sm.o0[4 * j + 1] * inv, sm.o0[4 * j + 2] * inv, sm.o0[4 * j + 3] * inv);
-    *reinterpret_cast<uint2*>(op + 32 + 8 * j) =
-        to_bf16x4(sm.o1[4 * j] * inv, sm.o1[4 * j + 1] * inv, sm.o1[4 * j + 2] * inv, sm.o1[4 * j + 3] * inv);
-  }
-  if (half == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (sm.m + __log2f(l_tot)) * kLn2;
-}
-
 // Merge every partial of `unit` (contributor chunks c_first..c_last of queue q, in
 // chunk order) and write the final output rows and LSE.
 __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_first, int c_last) {
@@ -243,12 +248,108 @@ __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_fir
   if (dh == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (mmax + __log2f(L)) * kLn2;
 }
 
+// Key tiles t0..t1-1 of `unit` (queue-local index ui) as part of chunk c of queue q.
+// Returns 1 if this call finished the unit (wrote its output), else 0.
+__device__ int process_segment(const AttnArgs& a, int q, int c, int unit, int ui, int t0, int t1, uint16_t* lds,
+                               int* s_flag) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int h = unit / a.q_tiles, qt = unit % a.q_tiles;
+  const int q0 = qt * BQ + wave * 32;
+  const int qi = q0 + l32;
+  const bool wave_active = q0 < a.n_tokens;
+
+  HeadSrc hs;
+  hs.km = a.memK + (int64_t)h * a.head_stride * D;
+  hs.vm = a.memV + (int64_t)h * a.head_stride * D;
+  hs.kc = a.K + (int64_t)h * D;
+  hs.vc = a.V + (int64_t)h * D;
+  hs.cur_rs = (int64_t)a.n_heads * D;
+
+  // B operand of S^T = K Q^T: this lane's query, head dims ds*16 + half*8 .. +7.
+  bf16x8 qf[4];
+  {
+    const uint16_t* qp = a.Q + ((int64_t)min(qi, a.n_tokens - 1) * a.n_heads + h) * D + half * 8;
+#pragma unroll
+    for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
+  }
+  SoftmaxState sm;
+  sm.m = kNegBig;
+  sm.l = 0.f;
+  sm.o0 = f32x16{};
+  sm.o1 = f32x16{};
+
+  {
+    const Staged st = load_tile(a, hs, t0, tid);
+    store_tile(lds, tid, st);
+  }
+  __syncthreads();
+  for (int t = t0; t < t1; ++t) {
+    const int buf = (t - t0) & 1;
+    // prefetch the next tile (the last iteration re-reads its own tile into the idle
+    // buffer: branch-free, so the staged values stay in registers)
+    const Staged st = load_tile(a, hs, min(t + 1, t1 - 1), tid);
+    if (wave_active) tile_compute(lds + buf * STAGE, qf, lane, tile_valid(a, t), sm);
+    store_tile(lds + (buf ^ 1) * STAGE, tid, st);
+    __syncthreads();
+  }
+
+  const float l_tot = half_sum(sm.l);
+  if (t0 == 0 && t1 == a.T) {
+    if (wave_active && qi < a.n_tokens) {
+      const float inv = 1.f / l_tot;
+      uint16_t* op = a.out + ((int64_t)qi * a.n_heads + h) * D + 4 * half;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        *reinterpret_cast<uint2*>(op + 8 * j) =
+            to_bf16x4(sm.o0[4 * j] * inv, sm.o0[4 * j + 1] * inv, sm.o0[4 * j + 2] * inv, sm.o0[4 * j + 3] * inv);
+        *reinterpret_cast<uint2*>(op + 32 + 8 * j) =
+            to_bf16x4(sm.o1[4 * j] * inv, sm.o1[4 * j + 1] * inv, sm.o1[4 * j + 2] * inv, sm.o1[4 * j + 3] * inv);
+      }
+      if (half == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (sm.m + __log2f(l_tot)) * kLn2;
+    }
+    return 1;
+  }
+
+  // Partial result: publish, then the last contributor of the unit merges.
+  const int seg = (int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1;
+  float* ps = a.part + (int64_t)(2 * (a.chunk_base[q] + c) + seg) * kAttnSlotFloats;
+  if (wave_active) {
+    const int row = wave * 32 + l32;
+    float* po = ps + row * D + 4 * half;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      *reinterpret_cast<float4*>(po + 8 * j) =
+          make_float4(sm.o0[4 * j], sm.o0[4 * j + 1], sm.o0[4 * j + 2], sm.o0[4 * j + 3]);
+      *reinterpret_cast<float4*>(po + 32 + 8 * j) =
+          make_float4(sm.o1[4 * j], sm.o1[4 * j + 1], sm.o1[4 * j + 2], sm.o1[4 * j + 3]);
+    }
+    if (half == 0) {
+      ps[BQ * D + row] = sm.m;
+      ps[BQ * D + BQ + row] = l_tot;
+    }
+  }
+  // release to the XCD's L2 (the vector L1 is write-through)
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  const int c_first = (int)(((int64_t)ui * a.T) / a.E);
+  const int c_last = (int)(((int64_t)(ui + 1) * a.T - 1) / a.E);
+  if (tid == 0) *s_flag = atomicAdd(&a.unit_ctr[unit], 1) == c_last - c_first;
+  __syncthreads();
+  const bool last = *s_flag != 0;
+  __syncthreads();
+  if (!last) return 0;
+  asm volatile("buffer_inv sc0" ::: "memory");  // no stale vector-L1 lines
+  merge_unit(a, q, unit, ui, c_first, c_last);
+  if (tid == 0) a.unit_ctr[unit] = 0;  // ready for the next launch
+  return 1;
+}
+
 __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
   __shared__ int s_val;
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, half = lane >> 5;
 
   // Counters of the launch two ahead (same ring row as the launch two back) restart.
   if (blockIdx.x == 0 && tid < kMaxQueues) a.queue_ctr[((a.seq + 2) & 3) * kMaxQueues + tid] = 0;
@@ -257,124 +358,36 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
   const int q = a.xcc_queue[hw_xcc_id()];
   int units_done = 0;
   if (q < 0) {
-    if (tid == 0) atomicOr(a.err, 1);  // an XCD the host did not map: its share goes to others
+    if (tid == 0) __hip_atomic_fetch_or(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   } else {
     int* qctr = a.queue_ctr + (a.seq & 3) * kMaxQueues + q;
     const int ub = a.unit_base[q];
     const int total = (a.unit_base[q + 1] - ub) * a.T;
+    const int n_chunks = a.n_chunks[q];
     for (;;) {
       if (tid == 0) s_val = atomicAdd(qctr, 1);
       __syncthreads();
       const int c = s_val;
       __syncthreads();
-      if (c >= a.n_chunks[q]) break;
-      const int it0 = c * a.E, it1 = min(total, it0 + a.E);
-
-      // segment state
-      int ui = it0 / a.T;
-      int t0 = it0 % a.T;
-      int unit = ub + ui;
-      int h = unit / a.q_tiles, qt = unit % a.q_tiles;
-      int qi = qt * BQ + wave * 32 + l32;
-      bool wave_active = qt * BQ + wave * 32 < a.n_tokens;
-      bf16x8 qf[4];
-      SoftmaxState sm;
-
-      auto begin_segment = [&]() {
-        if (qi < a.n_tokens) {
-          const uint16_t* qp = a.Q + ((int64_t)qi * a.n_heads + h) * D + half * 8;
-#pragma unroll
-          for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
-        } else {
-#pragma unroll
-          for (int ds = 0; ds < 4; ++ds) qf[ds] = bf16x8{};
-        }
-        sm.m = kNegBig;
-        sm.l = 0.f;
-        sm.o0 = f32x16{};
-        sm.o1 = f32x16{};
-      };
-      begin_segment();
-
-      Staged st;
-      load_tile(tile_src(a, h, t0), tid, st);
-      store_tile(lds, tid, st);
-      __syncthreads();
-
-      for (int it = it0; it < it1; ++it) {
-        const int buf = (it - it0) & 1;
-        const int t = it % a.T;
-        const bool has_next = it + 1 < it1;
-        if (has_next) {
-          const int un = ub + (it + 1) / a.T;
-          load_tile(tile_src(a, un / a.q_tiles, (it + 1) % a.T), tid, st);
-        }
-        const TileSrc cur = tile_src(a, h, t);  // only .valid is used
-        if (wave_active) tile_compute(lds + buf * STAGE, qf, lane, cur.valid, sm);
-
-        if (t == a.T - 1 || it == it1 - 1) {
-          // end of this chunk's segment of `unit`
-          const float l_tot = sm.l + __shfl_xor(sm.l, 32);
-          if (t0 == 0 && t == a.T - 1) {
-            if (wave_active && qi < a.n_tokens) write_final_lane(a, h, qi, half, sm, l_tot);
-            ++units_done;
-          } else {
-            const int seg = (int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1;
-            float* ps = a.part + (int64_t)(2 * (a.chunk_base[q] + c) + seg) * kAttnSlotFloats;
-            if (wave_active) {
-              const int row = wave * 32 + l32;
-              float* po = ps + row * D + 4 * half;
-#pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                *reinterpret_cast<float4*>(po + 8 * j) =
-                    make_float4(sm.o0[4 * j], sm.o0[4 * j + 1], sm.o0[4 * j + 2], sm.o0[4 * j + 3]);
-                *reinterpret_cast<float4*>(po + 32 + 8 * j) =
-                    make_float4(sm.o1[4 * j], sm.o1[4 * j + 1], sm.o1[4 * j + 2], sm.o1[4 * j + 3]);
-              }
-              if (half == 0) {
-                ps[BQ * D + row] = sm.m;
-                ps[BQ * D + BQ + row] = l_tot;
-              }
-            }
-            // release to the XCD's L2 (the vector L1 is write-through)
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
-            const int c_first = (int)(((int64_t)ui * a.T) / a.E);
-            const int c_last = (int)(((int64_t)(ui + 1) * a.T - 1) / a.E);
-            if (tid == 0) s_val = atomicAdd(&a.unit_ctr[unit], 1) == c_last - c_first;
-            __syncthreads();
-            const bool last = s_val != 0;
-            __syncthreads();
-            if (last) {
-              asm volatile("buffer_inv sc0" ::: "memory");  // no stale vector-L1 lines
-              merge_unit(a, q, unit, ui, c_first, c_last);
-              if (tid == 0) a.unit_ctr[unit] = 0;
-              ++units_done;
-            }
-          }
-          if (has_next) {
-            // next unit of this chunk
-            ++ui;
-            t0 = 0;
-            unit = ub + ui;
-            h = unit / a.q_tiles;
-            qt = unit % a.q_tiles;
-            qi = qt * BQ + wave * 32 + l32;
-            wave_active = qt * BQ + wave * 32 < a.n_tokens;
-            begin_segment();
-          }
-        }
-        if (has_next) store_tile(lds + (buf ^ 1) * STAGE, tid, st);
-        __syncthreads();
+      if (c >= n_chunks) break;
+      int it = c * a.E;
+      const int it_end = min(total, it + a.E);
+      while (it < it_end) {
+        const int ui = it / a.T;
+        const int t0 = it - ui * a.T;
+        const int seg_end = min(it_end, (ui + 1) * a.T);
+        units_done += process_segment(a, q, c, ub + ui, ui, t0, t0 + (seg_end - it), lds, &s_val);
+        it = seg_end;
       }
     }
   }
   // Completion record: (workgroups exited << 32) + units finished, one atomic per WG.
   if (tid == 0) {
     const unsigned long long add = (1ull << 32) + (unsigned long long)units_done;
-    const unsigned long long prev = atomicAdd(&a.exit_ctr[a.seq & 3], add);
+    const unsigned long long prev =
+        __hip_atomic_fetch_add(&a.exit_ctr[a.seq & 3], add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     if ((prev >> 32) == gridDim.x - 1u && (unsigned)((prev + add) & 0xffffffffu) != (unsigned)a.n_units)
-      atomicOr(a.err, 2);  // some unit was never finished
+      __hip_atomic_fetch_or(a.err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
 }
 
