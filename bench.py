@@ -183,6 +183,9 @@ def main():
     rv.device_status()
     assert all(m.len == T * k for m in mems)
 
+    for f in sorted({0, T // 2, T - 1}):
+        log(f"frame {f}: attention {events[f][0].elapsed_time(events[f][1]) * 1e3 / L:.1f} us/launch "
+            f"(context {f * k + N}), admission {events[f][1].elapsed_time(events[f][2]) * 1e3:.1f} us")
     attn_ms = sum(e[0].elapsed_time(e[1]) for e in events)
     admit_ms = sum(e[1].elapsed_time(e[2]) for e in events)
     ctx = [t * k + N for t in range(T)]

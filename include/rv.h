@@ -163,8 +163,9 @@ rv_status rv_admit_layers(int n_layers, const void *const *Q, const void *const 
 
 /* Synchronises the current device and reports, then clears, the status bits the
  * library's kernels raise: RV_OK, or RV_ERR_HIP with rv_last_error() naming the
- * condition (a workgroup ran on an XCD the library's placement probe never saw, or an
- * attention launch ended with work undone).  Test harnesses call it after each step. */
+ * condition (an attention workgroup found itself on another XCD than the round-robin
+ * placement of workgroup ids the library verified at start-up, in which case that
+ * launch's merged outputs may be wrong).  Test harnesses call it after each step. */
 rv_status rv_device_status(void);
 
 /* Pre-allocates the current device's scratch workspace (split-KV partial results,

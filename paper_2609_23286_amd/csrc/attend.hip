@@ -19,12 +19,14 @@
 //   is raised only when a tile exceeds it by more than 2^8, so accumulator rescales are
 //   rare (exact either way: the LSE uses the maximum the sums were taken against).
 // * Scheduling: 1041 queries x 16 heads is only 144 units, too few for 256 CUs, so each
-//   unit's key range is split (stream-K).  Units are dealt to one queue per XCD; a
-//   workgroup reads the XCC id it runs on and takes fixed-size chunks of (unit, key
-//   tile) iterations from that XCD's queue only.  All partial results of a unit are
-//   thus written and merged under one L2: a contributor waits for its stores to reach
-//   L2 and bumps the unit's counter; the last contributor merges the partials in chunk
-//   order (deterministic).  No device-wide cache flush is needed.
+//   unit's key range is split (stream-K).  Units are dealt to one queue per XCD; each
+//   queue's (unit, key tile) iterations are cut into equal chunks, one per workgroup,
+//   and the workgroup ids of a queue are the ones the hardware places on that XCD
+//   (ids are dealt round-robin over the XCDs; verified at start-up and by every
+//   workgroup).  All partial results of a unit are thus written and merged under one
+//   L2: a contributor waits for its stores to reach L2 and bumps the unit's counter;
+//   the last contributor merges the partials in chunk order (deterministic).  No
+//   device-wide cache flush is needed, and no workgroup waits on another.
 #include "rv_internal.h"
 
 namespace rv {
@@ -72,19 +74,23 @@ __device__ __forceinline__ float half_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
 // Key/value rows of one head: the memory segment (row stride 64) followed by the frame
-// (row stride H*64).
-struct HeadSrc {
+// (row stride H*64).  Per thread: the element offsets of its two rows (tid/8 and
+// tid/8 + 32, 16-byte chunk tid % 8) in either segment, fixed for the whole segment.
+struct TileCursor {
   const uint16_t* km;
   const uint16_t* vm;
   const uint16_t* kc;
   const uint16_t* vc;
-  int64_t cur_rs;
+  int64_t cur_tile;        // elements between consecutive frame tiles: 64 * H * 64
+  int off_m0, off_m1;      // thread offsets inside a memory tile
+  int off_c0, off_c1;      // thread offsets inside a frame tile
 };
 
-// One thread's share of a tile: rows tid/8 and tid/8 + 32, 16-byte chunk tid % 8.  Rows
-// past the end of the segment re-read its last row (always in bounds); their scores are
-// masked, so their contents never matter.
+// One thread's share of a tile.  Rows past the end of a segment re-read its last row
+// (always in bounds); their scores are masked, so their contents never matter.
 struct Staged {
   uint4 k0, k1, v0, v1;
 };
@@ -94,26 +100,39 @@ __device__ __forceinline__ int tile_valid(const AttnArgs& a, int t) {
                       : min(BK, a.n_tokens - (t - a.nt_mem) * BK);
 }
 
-__device__ __forceinline__ Staged load_tile(const AttnArgs& a, const HeadSrc& hs, int t, int tid) {
-  const int r = tid >> 3, c = tid & 7;
-  const int valid = tile_valid(a, t);
-  const int r0 = min(r, valid - 1), r1 = min(r + 32, valid - 1);
+__device__ __forceinline__ Staged load_tile(const AttnArgs& a, const TileCursor& tc, int t, int tid) {
   const uint16_t *kb, *vb;
-  int64_t rs;
-  if (t < a.nt_mem) {
-    kb = hs.km + (int64_t)t * BK * D;
-    vb = hs.vm + (int64_t)t * BK * D;
-    rs = D;
+  int o0, o1;
+  if (t < a.nt_mem) {  // uniform branch
+    kb = tc.km + (int64_t)t * (BK * D);
+    vb = tc.vm + (int64_t)t * (BK * D);
+    o0 = tc.off_m0;
+    o1 = tc.off_m1;
+    const int64_t rows = a.mem_len - (int64_t)t * BK;
+    if (rows < BK) {  // ragged last memory tile
+      const int r = tid >> 3, c = tid & 7, last = (int)rows - 1;
+      o0 = min(r, last) * D + c * 8;
+      o1 = min(r + 32, last) * D + c * 8;
+    }
   } else {
-    kb = hs.kc + (int64_t)(t - a.nt_mem) * BK * hs.cur_rs;
-    vb = hs.vc + (int64_t)(t - a.nt_mem) * BK * hs.cur_rs;
-    rs = hs.cur_rs;
+    const int tc_i = t - a.nt_mem;
+    kb = tc.kc + (int64_t)tc_i * tc.cur_tile;
+    vb = tc.vc + (int64_t)tc_i * tc.cur_tile;
+    o0 = tc.off_c0;
+    o1 = tc.off_c1;
+    const int rows = a.n_tokens - tc_i * BK;
+    if (rows < BK) {  // ragged last frame tile
+      const int r = tid >> 3, c = tid & 7, last = rows - 1;
+      const int rs = a.n_heads * D;
+      o0 = min(r, last) * rs + c * 8;
+      o1 = min(r + 32, last) * rs + c * 8;
+    }
   }
   Staged st;
-  st.k0 = *reinterpret_cast<const uint4*>(kb + r0 * rs + c * 8);
-  st.k1 = *reinterpret_cast<const uint4*>(kb + r1 * rs + c * 8);
-  st.v0 = *reinterpret_cast<const uint4*>(vb + r0 * rs + c * 8);
-  st.v1 = *reinterpret_cast<const uint4*>(vb + r1 * rs + c * 8);
+  st.k0 = *reinterpret_cast<const uint4*>(kb + o0);
+  st.k1 = *reinterpret_cast<const uint4*>(kb + o1);
+  st.v0 = *reinterpret_cast<const uint4*>(vb + o0);
+  st.v1 = *reinterpret_cast<const uint4*>(vb + o1);
   return st;
 }
 
@@ -208,35 +227,62 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
 }
 
 // Merge every partial of `unit` (contributor chunks c_first..c_last of queue q, in
-// chunk order) and write the final output rows and LSE.
+// chunk order) and write the final output rows and LSE.  Thread -> (row, 32 dims); all
+// partial loads are issued before any is consumed.
+constexpr int kMergeMax = 8;
+
+__device__ __forceinline__ const float* slot_ptr(const AttnArgs& a, int q, int c, int ui) {
+  const int slot = 2 * (a.chunk_base[q] + c) + ((int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1);
+  return a.part + (int64_t)slot * kAttnSlotFloats;
+}
+
 __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_first, int c_last) {
   const int tid = threadIdx.x;
   const int h = unit / a.q_tiles, qt = unit % a.q_tiles;
   const int row = tid >> 1, dh = (tid & 1) * 32;
   const int qi = qt * BQ + row;
   if (qi >= a.n_tokens) return;
-  float mmax = kNegBig;
-  for (int c = c_first; c <= c_last; ++c) {
-    const int slot = 2 * (a.chunk_base[q] + c) + ((int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1);
-    mmax = fmaxf(mmax, a.part[(int64_t)slot * kAttnSlotFloats + BQ * D + row]);
-  }
+  float mmax = kNegBig, L = 0.f;
   float acc[32];
 #pragma unroll
   for (int e = 0; e < 32; ++e) acc[e] = 0.f;
-  float L = 0.f;
-  for (int c = c_first; c <= c_last; ++c) {
-    const int slot = 2 * (a.chunk_base[q] + c) + ((int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1);
-    const float* ps = a.part + (int64_t)slot * kAttnSlotFloats;
-    const float w = __builtin_amdgcn_exp2f(ps[BQ * D + row] - mmax);
-    L += w * ps[BQ * D + BQ + row];
-    const float4* po = reinterpret_cast<const float4*>(ps + row * D + dh);
+  for (int c0 = c_first; c0 <= c_last; c0 += kMergeMax) {
+    const int n = min(kMergeMax, c_last - c0 + 1);
+    float mv[kMergeMax], lv[kMergeMax];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float4 v = po[e];
-      acc[4 * e] += w * v.x;
-      acc[4 * e + 1] += w * v.y;
-      acc[4 * e + 2] += w * v.z;
-      acc[4 * e + 3] += w * v.w;
+    for (int j = 0; j < kMergeMax; ++j) {
+      if (j < n) {
+        const float* ps = slot_ptr(a, q, c0 + j, ui);
+        mv[j] = ps[BQ * D + row];
+        lv[j] = ps[BQ * D + BQ + row];
+      } else {
+        mv[j] = kNegBig;
+        lv[j] = 0.f;
+      }
+    }
+    float m_new = mmax;
+#pragma unroll
+    for (int j = 0; j < kMergeMax; ++j) m_new = fmaxf(m_new, mv[j]);
+    const float scale = __builtin_amdgcn_exp2f(mmax - m_new);
+    L *= scale;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) acc[e] *= scale;
+    mmax = m_new;
+#pragma unroll
+    for (int j = 0; j < kMergeMax; ++j) {
+      if (j < n) {
+        const float w = __builtin_amdgcn_exp2f(mv[j] - mmax);
+        L += w * lv[j];
+        const float4* po = reinterpret_cast<const float4*>(slot_ptr(a, q, c0 + j, ui) + row * D + dh);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float4 v = po[e];
+          acc[4 * e] += w * v.x;
+          acc[4 * e + 1] += w * v.y;
+          acc[4 * e + 2] += w * v.z;
+          acc[4 * e + 3] += w * v.w;
+        }
+      }
     }
   }
   const float inv = 1.f / L;
@@ -249,23 +295,32 @@ __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_fir
 }
 
 // Key tiles t0..t1-1 of `unit` (queue-local index ui) as part of chunk c of queue q.
-// Returns 1 if this call finished the unit (wrote its output), else 0.
-__device__ int process_segment(const AttnArgs& a, int q, int c, int unit, int ui, int t0, int t1, uint16_t* lds,
+__device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int ui, int t0, int t1, uint16_t* lds,
                                int* s_flag) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
-  const int h = unit / a.q_tiles, qt = unit % a.q_tiles;
+  unit = uniform(unit);
+  t0 = uniform(t0);
+  t1 = uniform(t1);
+  const int h = uniform(unit / a.q_tiles), qt = uniform(unit % a.q_tiles);
   const int q0 = qt * BQ + wave * 32;
   const int qi = q0 + l32;
   const bool wave_active = q0 < a.n_tokens;
 
-  HeadSrc hs;
-  hs.km = a.memK + (int64_t)h * a.head_stride * D;
-  hs.vm = a.memV + (int64_t)h * a.head_stride * D;
-  hs.kc = a.K + (int64_t)h * D;
-  hs.vc = a.V + (int64_t)h * D;
-  hs.cur_rs = (int64_t)a.n_heads * D;
+  TileCursor tc;
+  {
+    const int r = tid >> 3, c8 = (tid & 7) * 8, rs = a.n_heads * D;
+    tc.km = a.memK + (int64_t)h * a.head_stride * D;
+    tc.vm = a.memV + (int64_t)h * a.head_stride * D;
+    tc.kc = a.K + (int64_t)h * D;
+    tc.vc = a.V + (int64_t)h * D;
+    tc.cur_tile = (int64_t)BK * rs;
+    tc.off_m0 = r * D + c8;
+    tc.off_m1 = (r + 32) * D + c8;
+    tc.off_c0 = r * rs + c8;
+    tc.off_c1 = (r + 32) * rs + c8;
+  }
 
   // B operand of S^T = K Q^T: this lane's query, head dims ds*16 + half*8 .. +7.
   bf16x8 qf[4];
@@ -281,15 +336,15 @@ __device__ int process_segment(const AttnArgs& a, int q, int c, int unit, int ui
   sm.o1 = f32x16{};
 
   {
-    const Staged st = load_tile(a, hs, t0, tid);
+    const Staged st = load_tile(a, tc, t0, tid);
     store_tile(lds, tid, st);
   }
   __syncthreads();
-  for (int t = t0; t < t1; ++t) {
+  for (int t = t0; t < t1; t = uniform(t + 1)) {
     const int buf = (t - t0) & 1;
     // prefetch the next tile (the last iteration re-reads its own tile into the idle
     // buffer: branch-free, so the staged values stay in registers)
-    const Staged st = load_tile(a, hs, min(t + 1, t1 - 1), tid);
+    const Staged st = load_tile(a, tc, min(t + 1, t1 - 1), tid);
     if (wave_active) tile_compute(lds + buf * STAGE, qf, lane, tile_valid(a, t), sm);
     store_tile(lds + (buf ^ 1) * STAGE, tid, st);
     __syncthreads();
@@ -309,7 +364,7 @@ __device__ int process_segment(const AttnArgs& a, int q, int c, int unit, int ui
       }
       if (half == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (sm.m + __log2f(l_tot)) * kLn2;
     }
-    return 1;
+    return;
   }
 
   // Partial result: publish, then the last contributor of the unit merges.
@@ -330,8 +385,12 @@ __device__ int process_segment(const AttnArgs& a, int q, int c, int unit, int ui
       ps[BQ * D + BQ + row] = l_tot;
     }
   }
-  // release to the XCD's L2 (the vector L1 is write-through)
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (a.safe) {
+    __threadfence();  // placement not verified: device-scope release
+  } else {
+    // release to the XCD's L2 (the vector L1 is write-through)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
   __syncthreads();
   const int c_first = (int)(((int64_t)ui * a.T) / a.E);
   const int c_last = (int)(((int64_t)(ui + 1) * a.T - 1) / a.E);
@@ -339,11 +398,13 @@ __device__ int process_segment(const AttnArgs& a, int q, int c, int unit, int ui
   __syncthreads();
   const bool last = *s_flag != 0;
   __syncthreads();
-  if (!last) return 0;
-  asm volatile("buffer_inv sc0" ::: "memory");  // no stale vector-L1 lines
+  if (!last) return;
+  if (a.safe)
+    __threadfence();  // device-scope acquire
+  else
+    asm volatile("buffer_inv sc0" ::: "memory");  // no stale vector-L1 lines
   merge_unit(a, q, unit, ui, c_first, c_last);
   if (tid == 0) a.unit_ctr[unit] = 0;  // ready for the next launch
-  return 1;
 }
 
 __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(AttnArgs a) {
@@ -351,43 +412,25 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
   __shared__ int s_val;
   const int tid = threadIdx.x;
 
-  // Counters of the launch two ahead (same ring row as the launch two back) restart.
-  if (blockIdx.x == 0 && tid < kMaxQueues) a.queue_ctr[((a.seq + 2) & 3) * kMaxQueues + tid] = 0;
-  if (blockIdx.x == 0 && tid == kMaxQueues) a.exit_ctr[(a.seq + 2) & 3] = 0ull;
-
-  const int q = a.xcc_queue[hw_xcc_id()];
-  int units_done = 0;
-  if (q < 0) {
-    if (tid == 0) __hip_atomic_fetch_or(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-  } else {
-    int* qctr = a.queue_ctr + (a.seq & 3) * kMaxQueues + q;
-    const int ub = a.unit_base[q];
-    const int total = (a.unit_base[q + 1] - ub) * a.T;
-    const int n_chunks = a.n_chunks[q];
-    for (;;) {
-      if (tid == 0) s_val = atomicAdd(qctr, 1);
-      __syncthreads();
-      const int c = s_val;
-      __syncthreads();
-      if (c >= n_chunks) break;
-      int it = c * a.E;
-      const int it_end = min(total, it + a.E);
-      while (it < it_end) {
-        const int ui = it / a.T;
-        const int t0 = it - ui * a.T;
-        const int seg_end = min(it_end, (ui + 1) * a.T);
-        units_done += process_segment(a, q, c, ub + ui, ui, t0, t0 + (seg_end - it), lds, &s_val);
-        it = seg_end;
-      }
-    }
-  }
-  // Completion record: (workgroups exited << 32) + units finished, one atomic per WG.
-  if (tid == 0) {
-    const unsigned long long add = (1ull << 32) + (unsigned long long)units_done;
-    const unsigned long long prev =
-        __hip_atomic_fetch_add(&a.exit_ctr[a.seq & 3], add, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    if ((prev >> 32) == gridDim.x - 1u && (unsigned)((prev + add) & 0xffffffffu) != (unsigned)a.n_units)
-      __hip_atomic_fetch_or(a.err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  // Workgroup b serves queue b % n_queues, chunk b / n_queues.  The hardware deals
+  // workgroup ids round-robin over the XCDs (checked when the library starts), so all
+  // chunks of a queue share one L2; each workgroup verifies it against the XCC id it
+  // runs on and raises a status bit if not.
+  const int q = (int)(blockIdx.x % (unsigned)a.n_queues);
+  const int c = (int)(blockIdx.x / (unsigned)a.n_queues);
+  if (!a.safe && tid == 0 && a.xcc_queue[hw_xcc_id()] != q)
+    __hip_atomic_fetch_or(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  if (c >= a.n_chunks[q]) return;
+  const int ub = a.unit_base[q];
+  const int total = (a.unit_base[q + 1] - ub) * a.T;
+  int it = c * a.E;
+  const int it_end = min(total, it + a.E);
+  while (it < it_end) {
+    const int ui = it / a.T;
+    const int t0 = it - ui * a.T;
+    const int seg_end = min(it_end, (ui + 1) * a.T);
+    process_segment(a, q, c, ub + ui, ui, t0, t0 + (seg_end - it), lds, &s_val);
+    it = seg_end;
   }
 }
 

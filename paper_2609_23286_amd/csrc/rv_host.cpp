@@ -61,16 +61,14 @@ struct Workspace {
   size_t part_floats = 0;
   int* unit_ctr = nullptr;   // attention unit counters (zero between launches)
   size_t n_unit_ctr = 0;
-  int* ctrl = nullptr;       // queue counters [4][kMaxQueues], exit counters, status bits
-  int seq = 0;               // attention launch sequence number
+  int* ctrl = nullptr;       // device status bits
+  bool safe = false;         // workgroup placement not round-robin: device-scope fences
   float* sal = nullptr;      // saliency staging when the caller passes none
   size_t sal_floats = 0;
   std::map<std::tuple<int, int, int, int>, std::pair<int32_t*, int>> qidx;  // per query subset
 };
-constexpr size_t kCtrlQueueInts = 4 * rv::kMaxQueues;
-constexpr size_t kCtrlExitOffsetBytes = kCtrlQueueInts * 4;        // 4 x uint64
-constexpr size_t kCtrlErrOffsetBytes = kCtrlExitOffsetBytes + 4 * 8;
-constexpr size_t kCtrlBytes = kCtrlErrOffsetBytes + 64;
+constexpr size_t kCtrlErrOffsetBytes = 0;
+constexpr size_t kCtrlBytes = 256;
 
 std::mutex g_ws_mu;
 std::map<int, Workspace> g_ws;
@@ -103,13 +101,16 @@ rv_status grow(T** p, size_t* have, size_t need, bool zero, const char* what) {
   return RV_OK;
 }
 
-// Learns which XCC ids the device's workgroups run on (one work queue per XCC), the
-// CU count and the LDS limit, and allocates the control block.
+// Learns where the hardware places workgroups: workgroup ids are expected to be dealt
+// round-robin over the XCDs (id b on the XCD of id b % n), which the attention kernel's
+// XCD-local merges rely on.  Also reads the CU count and the LDS limit, and allocates
+// the status block.  If placement is not round-robin the library uses device-scope
+// fences instead (correct, slower).
 rv_status init_device(Workspace* ws, int dev) {
   if (ws->ready) return RV_OK;
   RV_HIP(hipDeviceGetAttribute(&ws->n_cus, hipDeviceAttributeMultiprocessorCount, dev), "CU count");
   RV_HIP(hipDeviceGetAttribute(&ws->max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev), "LDS limit");
-  const int n_probe = 2048;
+  const int n_probe = 4096;
   int* d_ids = nullptr;
   RV_HIP(hipMalloc(&d_ids, n_probe * sizeof(int)), "placement probe");
   std::vector<int> ids(n_probe, -1);
@@ -117,18 +118,30 @@ rv_status init_device(Workspace* ws, int dev) {
   if (e == hipSuccess) e = hipMemcpy(ids.data(), d_ids, n_probe * sizeof(int), hipMemcpyDeviceToHost);
   (void)hipFree(d_ids);
   if (e != hipSuccess) return hip_fail(e, "placement probe");
+  // n = number of distinct XCC ids; round-robin iff ids[b] == ids[b % n] for all b
+  std::vector<int> distinct;
+  for (int id : ids)
+    if (std::find(distinct.begin(), distinct.end(), id) == distinct.end()) distinct.push_back(id);
+  const int n = (int)distinct.size();
+  bool rr = n >= 1 && n <= rv::kMaxQueues;
+  for (int b = 0; rr && b < n; ++b)
+    for (int b2 = 0; b2 < b; ++b2) rr = rr && ids[b] != ids[b2];
+  for (int b = 0; rr && b < n_probe; ++b) rr = ids[b] == ids[b % n];
   for (int i = 0; i < 16; ++i) ws->xcc_queue[i] = -1;
-  int nq = 0;
-  for (int i = 0; i < 16; ++i)
-    if (std::find(ids.begin(), ids.end(), i) != ids.end()) ws->xcc_queue[i] = nq++;
-  if (nq == 0) return fail(RV_ERR_HIP, "placement probe saw no XCC id");
-  ws->n_queues = nq;
+  if (rr) {
+    ws->n_queues = n;
+    for (int qi = 0; qi < n; ++qi) ws->xcc_queue[ids[qi] & 15] = qi;
+    ws->safe = false;
+  } else {
+    ws->n_queues = 8;
+    ws->safe = true;
+  }
   char* ctrl = nullptr;
-  RV_HIP(hipMalloc(&ctrl, kCtrlBytes), "control block");
+  RV_HIP(hipMalloc(&ctrl, kCtrlBytes), "status block");
   e = hipMemset(ctrl, 0, kCtrlBytes);
   if (e != hipSuccess) {
     (void)hipFree(ctrl);
-    return hip_fail(e, "control block");
+    return hip_fail(e, "status block");
   }
   ws->ctrl = reinterpret_cast<int*>(ctrl);
   ws->ready = true;
@@ -462,9 +475,9 @@ rv_status rv_device_status(void) {
   RV_HIP(hipMemcpy(&bits, err, sizeof bits, hipMemcpyDeviceToHost), "status read");
   if (bits == 0) return RV_OK;
   RV_HIP(hipMemset(err, 0, sizeof bits), "status reset");
-  return fail(RV_ERR_HIP, "device status 0x%x:%s%s", bits,
-              (bits & 1) ? " a workgroup ran on an XCC the placement probe had not seen;" : "",
-              (bits & 2) ? " an attention launch finished with units left undone" : "");
+  return fail(RV_ERR_HIP, "device status 0x%x:%s", bits,
+              (bits & 1) ? " an attention workgroup ran on another XCD than its id's round-robin "
+                           "placement (merged results may be wrong)" : "");
 }
 
 rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
@@ -514,8 +527,6 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   a.lse = lse;
   a.part = ws->part;
   a.unit_ctr = ws->unit_ctr;
-  a.queue_ctr = ws->ctrl;
-  a.exit_ctr = reinterpret_cast<unsigned long long*>(reinterpret_cast<char*>(ws->ctrl) + kCtrlExitOffsetBytes);
   a.err = reinterpret_cast<int*>(reinterpret_cast<char*>(ws->ctrl) + kCtrlErrOffsetBytes);
   a.n_tokens = n_tokens;
   a.n_heads = n_heads;
@@ -525,7 +536,7 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   a.n_units = p.n_units;
   a.n_queues = ws->n_queues;
   a.E = p.E;
-  a.seq = ws->seq;
+  a.safe = ws->safe ? 1 : 0;
   for (int q = 0; q <= ws->n_queues; ++q) a.unit_base[q] = p.unit_base[q];
   for (int q = 0; q < ws->n_queues; ++q) {
     a.n_chunks[q] = p.n_chunks[q];
@@ -533,7 +544,6 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   }
   for (int i = 0; i < 16; ++i) a.xcc_queue[i] = ws->xcc_queue[i];
   RV_HIP(rv::launch_attention(a, p.grid, s), "attention launch");
-  ws->seq = (ws->seq + 1) & 0x3fffffff;
 
   if (saliency) {
     rv::AdmitArgs b{};

@@ -23,9 +23,8 @@ constexpr int kAttnWgPerCu = 2;    // attention workgroups resident per CU
 //
 // A unit is (head, 128-query tile); its context is T key tiles of 64 keys.  Units are
 // dealt to per-XCD queues (contiguous unit ranges); each queue's (unit, key tile)
-// iteration space is cut into chunks of E tiles.  A workgroup reads the id of the XCD it
-// runs on and takes chunks from that XCD's queue only, so every partial result of a
-// unit is produced and merged under one L2.
+// iteration space is cut into chunks of E tiles, chunk c of queue q going to workgroup
+// c * n_queues + q, which the hardware places on queue q's XCD.
 struct AttnArgs {
   const uint16_t* Q;       // [N][H][64]
   const uint16_t* K;
@@ -38,8 +37,6 @@ struct AttnArgs {
   float* lse;              // [H][N]
   float* part;             // partial slots, kAttnSlotFloats each
   int* unit_ctr;           // [n_units] contributor counters, zero between launches
-  int* queue_ctr;          // [4][kMaxQueues] chunk counters; launch `seq` uses row seq%4
-  unsigned long long* exit_ctr;  // [4]: (workgroups exited << 32) + units finished
   int* err;                // device status bits (see rv_device_status)
   int n_tokens;
   int n_heads;
@@ -49,7 +46,7 @@ struct AttnArgs {
   int n_units;             // n_heads * q_tiles
   int n_queues;
   int E;                   // key tiles per chunk
-  int seq;                 // launch sequence number
+  int safe;                // 1: placement not verified, use device-scope fences
   int unit_base[kMaxQueues + 1];
   int n_chunks[kMaxQueues];
   int chunk_base[kMaxQueues];
