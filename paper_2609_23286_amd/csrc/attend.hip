@@ -7,17 +7,20 @@
 //
 // Design (CDNA4):
 // * Work unit = (head, 128-query tile); 4 wave64s, 32 queries each.  Key/value tiles of
-//   64 rows are staged in LDS, row-major with 144-byte rows, double-buffered: the next
-//   tile's global loads are in flight while the current one is computed.
+//   64 rows go straight from global memory into LDS (global_load_lds_dwordx4), row-major
+//   with an XOR swizzle, double-buffered: the next tile streams in while the current
+//   one is computed.
 // * Scores are formed transposed, S^T = K Q^T (v_mfma_f32_32x32x16_bf16), so each lane
 //   owns one query column: softmax max/sum are in-lane plus one exchange between the
 //   two 32-lane halves sharing a query.  The output is accumulated transposed too,
 //   O^T += V^T P^T: P^T is the score accumulator itself (its 16 rows per lane are the
 //   8+8 keys the B operand wants), and V^T comes straight from the row-major V tile
 //   through ds_read_b64_tr_b16 transposing reads.
-// * Online softmax in base 2 with 1/sqrt(64) folded into one FMA; the running maximum
-//   is raised only when a tile exceeds it by more than 2^8, so accumulator rescales are
-//   rare (exact either way: the LSE uses the maximum the sums were taken against).
+// * Online softmax in base 2 with 1/sqrt(64) folded into one FMA.  Probabilities are
+//   taken against a running reference that is only raised when a tile could overflow
+//   (tile sums >= 2^64), so neither tile maxima nor accumulator rescales are computed in
+//   the common case (exact either way: the LSE uses the reference the sums were taken
+//   against).
 // * Scheduling: 1041 queries x 16 heads is only 144 units, too few for 256 CUs, so each
 //   unit's key range is split (stream-K).  Units are dealt to one queue per XCD; each
 //   queue's (unit, key tile) iterations are cut into equal chunks, one per workgroup,
@@ -40,12 +43,12 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int BQ = kAttnBQ;
 constexpr int BK = kAttnBK;
 constexpr int D = kHeadDim;
-constexpr int LDS_STRIDE = D + 8;               // 144-byte rows
-constexpr int TILE = BK * LDS_STRIDE;           // one K or V tile, in bf16 elements
+constexpr int TILE = BK * D;                    // one K or V tile: 64 rows x 128 bytes
 constexpr int STAGE = 2 * TILE;                 // K tile then V tile
+constexpr int NSTAGE = 4;                       // LDS ring: two tiles computed, two in flight
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kScaleLog2 = 1.44269504088896341f * 0.125f;  // log2(e) / sqrt(64)
-constexpr float kRescaleSlack = 8.0f;
+constexpr float kOverflowGuard = 18446744073709551616.0f;  // 2^64
 constexpr float kNegBig = -1.0e30f;
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -76,9 +79,19 @@ __device__ __forceinline__ float half_sum(float x) {
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// LDS tile layout: 64 rows of 128 bytes, no padding.  The 16-byte chunk c of row r is
+// stored at chunk c ^ ((r >> 1) & 7) of that row: any 16 consecutive rows then map a
+// given logical chunk to 16 distinct (bank half, chunk) slots, so the 16-byte K reads
+// (one row per lane) and the transposing V reads (4 rows x 32 bytes per 16 lanes) are
+// free of bank conflicts.
+__device__ __forceinline__ int swz(int row, int chunk) { return row * D + ((chunk ^ ((row >> 1) & 7)) << 3); }
+
 // Key/value rows of one head: the memory segment (row stride 64) followed by the frame
-// (row stride H*64).  Per thread: the element offsets of its two rows (tid/8 and
-// tid/8 + 32, 16-byte chunk tid % 8) in either segment, fixed for the whole segment.
+// (row stride H*64).  Tiles go straight from global memory to LDS
+// (global_load_lds_dwordx4: lane l of a wave writes 16 bytes at the wave's LDS base +
+// 16 l), so each thread fetches the global chunk that belongs at its LDS slot: thread
+// tid fills physical chunk tid % 8 of rows tid / 8 and tid / 8 + 32, i.e. the global
+// chunk (tid % 8) ^ ((row >> 1) & 7) of those rows.
 struct TileCursor {
   const uint16_t* km;
   const uint16_t* vm;
@@ -89,18 +102,22 @@ struct TileCursor {
   int off_c0, off_c1;      // thread offsets inside a frame tile
 };
 
-// One thread's share of a tile.  Rows past the end of a segment re-read its last row
-// (always in bounds); their scores are masked, so their contents never matter.
-struct Staged {
-  uint4 k0, k1, v0, v1;
-};
-
 __device__ __forceinline__ int tile_valid(const AttnArgs& a, int t) {
   return t < a.nt_mem ? (int)min((int64_t)BK, a.mem_len - (int64_t)t * BK)
                       : min(BK, a.n_tokens - (t - a.nt_mem) * BK);
 }
 
-__device__ __forceinline__ Staged load_tile(const AttnArgs& a, const TileCursor& tc, int t, int tid) {
+typedef __attribute__((address_space(3))) void lds_void;
+
+
+__device__ __forceinline__ void lds_load16(const uint16_t* g, uint16_t* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((const void*)g, (lds_void*)lds_wave_base, 16, 0, 0);
+}
+
+// Issue tile t's K and V loads into `stage` (completion: vmcnt + barrier).  Rows past the
+// end of a segment re-read its last row (always in bounds); their scores are masked.
+__device__ __forceinline__ void load_tile(const AttnArgs& a, const TileCursor& tc, int t, int tid,
+                                          uint16_t* stage) {
   const uint16_t *kb, *vb;
   int o0, o1;
   if (t < a.nt_mem) {  // uniform branch
@@ -111,8 +128,8 @@ __device__ __forceinline__ Staged load_tile(const AttnArgs& a, const TileCursor&
     const int64_t rows = a.mem_len - (int64_t)t * BK;
     if (rows < BK) {  // ragged last memory tile
       const int r = tid >> 3, c = tid & 7, last = (int)rows - 1;
-      o0 = min(r, last) * D + c * 8;
-      o1 = min(r + 32, last) * D + c * 8;
+      o0 = min(r, last) * D + ((c ^ ((r >> 1) & 7)) << 3);
+      o1 = min(r + 32, last) * D + ((c ^ (((r + 32) >> 1) & 7)) << 3);
     }
   } else {
     const int tc_i = t - a.nt_mem;
@@ -124,24 +141,16 @@ __device__ __forceinline__ Staged load_tile(const AttnArgs& a, const TileCursor&
     if (rows < BK) {  // ragged last frame tile
       const int r = tid >> 3, c = tid & 7, last = rows - 1;
       const int rs = a.n_heads * D;
-      o0 = min(r, last) * rs + c * 8;
-      o1 = min(r + 32, last) * rs + c * 8;
+      o0 = min(r, last) * rs + ((c ^ ((r >> 1) & 7)) << 3);
+      o1 = min(r + 32, last) * rs + ((c ^ (((r + 32) >> 1) & 7)) << 3);
     }
   }
-  Staged st;
-  st.k0 = *reinterpret_cast<const uint4*>(kb + o0);
-  st.k1 = *reinterpret_cast<const uint4*>(kb + o1);
-  st.v0 = *reinterpret_cast<const uint4*>(vb + o0);
-  st.v1 = *reinterpret_cast<const uint4*>(vb + o1);
-  return st;
-}
-
-__device__ __forceinline__ void store_tile(uint16_t* stage, int tid, const Staged& st) {
-  const int r = tid >> 3, c = tid & 7;
-  *reinterpret_cast<uint4*>(&stage[r * LDS_STRIDE + c * 8]) = st.k0;
-  *reinterpret_cast<uint4*>(&stage[(r + 32) * LDS_STRIDE + c * 8]) = st.k1;
-  *reinterpret_cast<uint4*>(&stage[TILE + r * LDS_STRIDE + c * 8]) = st.v0;
-  *reinterpret_cast<uint4*>(&stage[TILE + (r + 32) * LDS_STRIDE + c * 8]) = st.v1;
+  // wave w fills rows 8w .. 8w+7 (first load) and 32 + 8w .. (second load)
+  const int w8 = (tid >> 6) * 8 * D;
+  lds_load16(kb + o0, stage + w8);
+  lds_load16(kb + o1, stage + 32 * D + w8);
+  lds_load16(vb + o0, stage + TILE + w8);
+  lds_load16(vb + o1, stage + TILE + 32 * D + w8);
 }
 
 struct SoftmaxState {
@@ -158,8 +167,8 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
   f32x16 s0 = {}, s1 = {};
 #pragma unroll
   for (int ds = 0; ds < 4; ++ds) {
-    const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&stage[l32 * LDS_STRIDE + ds * 16 + half * 8]);
-    const bf16x8 kb = *reinterpret_cast<const bf16x8*>(&stage[(32 + l32) * LDS_STRIDE + ds * 16 + half * 8]);
+    const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&stage[swz(l32, ds * 2 + half)]);
+    const bf16x8 kb = *reinterpret_cast<const bf16x8*>(&stage[swz(32 + l32, ds * 2 + half)]);
     s0 = mfma32(ka, qf[ds], s0);
     s1 = mfma32(kb, qf[ds], s1);
   }
@@ -175,18 +184,12 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
       s1[r] = fmaf(__saturatef(key + 32.0f - fv), kNegBig, s1[r]);
     }
   }
-  float mx = fmaxf(s0[0], s1[0]);
-#pragma unroll
-  for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-  const float m_cand = half_max(mx) * kScaleLog2;
-  if (__any(m_cand > sm.m + kRescaleSlack)) {
-    const float m_new = fmaxf(sm.m, m_cand);
-    const float alpha = __builtin_amdgcn_exp2f(sm.m - m_new);
-    sm.l *= alpha;
-    sm.o0 *= alpha;
-    sm.o1 *= alpha;
-    sm.m = m_new;
-  }
+  // P = 2^(z*log2e/8 - m) against the running reference m.  Softmax does not depend on
+  // the reference, so the tile maximum is only needed when some p could overflow: a
+  // lane whose tile sum reaches 2^64 (or inf; every p starts as inf while m is unset)
+  // makes the wave take the exact path -- raise m to the tile maximum, rescale the
+  // accumulators, recompute P.  Terms far below the reference underflow to 0, exactly
+  // as they would relative to the true maximum.
   bf16x8 p[4];
   float rsum = 0.f;
 #pragma unroll
@@ -197,6 +200,26 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
     p[r >> 3][r & 7] = (__bf16)e0;
     p[2 + (r >> 3)][r & 7] = (__bf16)e1;
   }
+  if (__any(!(rsum < kOverflowGuard))) {
+    float mx = fmaxf(s0[0], s1[0]);
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+    const float m_new = fmaxf(sm.m, half_max(mx) * kScaleLog2);
+    const float alpha = __builtin_amdgcn_exp2f(sm.m - m_new);
+    sm.l *= alpha;
+    sm.o0 *= alpha;
+    sm.o1 *= alpha;
+    sm.m = m_new;
+    rsum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], kScaleLog2, -sm.m));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], kScaleLog2, -sm.m));
+      rsum += e0 + e1;
+      p[r >> 3][r & 7] = (__bf16)e0;
+      p[2 + (r >> 3)][r & 7] = (__bf16)e1;
+    }
+  }
   sm.l += rsum;
 
   // V^T operand through transposing LDS reads.  Within each 16-lane group, lane i
@@ -206,16 +229,17 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
   // lane half hh, slots 0..3 are keys ks*16 + 4hh + r, slots 4..7 keys ks*16 + 8 + 4hh + r.
   const uint16_t* vt = stage + TILE;
   const int g = lane >> 4, i16 = lane & 15, rr = i16 >> 2, jj = i16 & 3, hh = g >> 1;
-  const int col = 16 * (g & 1) + 4 * jj;
+  const int col = 16 * (g & 1) + 4 * jj;  // logical column (elements) within a 32-dim block
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
     const int row = ks * 16 + 4 * hh + rr;
 #pragma unroll
     for (int db = 0; db < 2; ++db) {
+      const int lcol = db * 32 + col;
       const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_i16x4*)(vt + row * LDS_STRIDE + db * 32 + col));
+          (lds_i16x4*)(vt + swz(row, lcol >> 3) + (lcol & 7)));
       const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_i16x4*)(vt + (row + 8) * LDS_STRIDE + db * 32 + col));
+          (lds_i16x4*)(vt + swz(row + 8, lcol >> 3) + (lcol & 7)));
       const i16x8 w = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       const bf16x8 va = __builtin_bit_cast(bf16x8, w);
       if (db == 0)
@@ -316,10 +340,11 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
     tc.kc = a.K + (int64_t)h * D;
     tc.vc = a.V + (int64_t)h * D;
     tc.cur_tile = (int64_t)BK * rs;
-    tc.off_m0 = r * D + c8;
-    tc.off_m1 = (r + 32) * D + c8;
-    tc.off_c0 = r * rs + c8;
-    tc.off_c1 = (r + 32) * rs + c8;
+    const int g0 = (c8 ^ (((r >> 1) & 7) << 3)), g1 = (c8 ^ ((((r + 32) >> 1) & 7) << 3));
+    tc.off_m0 = r * D + g0;
+    tc.off_m1 = (r + 32) * D + g1;
+    tc.off_c0 = r * rs + g0;
+    tc.off_c1 = (r + 32) * rs + g1;
   }
 
   // B operand of S^T = K Q^T: this lane's query, head dims ds*16 + half*8 .. +7.
@@ -335,18 +360,21 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   sm.o0 = f32x16{};
   sm.o1 = f32x16{};
 
-  {
-    const Staged st = load_tile(a, tc, t0, tid);
-    store_tile(lds, tid, st);
-  }
+  // Ring of NSTAGE (4) tiles, two computed per barrier: tile t lives in stage t % 4.  The
+  // next pair streams into the two stages the previous pair used (freed at the last
+  // barrier) while this pair is computed.
+  load_tile(a, tc, t0, tid, lds + (t0 % NSTAGE) * STAGE);
+  if (t0 + 1 < t1) load_tile(a, tc, t0 + 1, tid, lds + ((t0 + 1) % NSTAGE) * STAGE);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  for (int t = t0; t < t1; t = uniform(t + 1)) {
-    const int buf = (t - t0) & 1;
-    // prefetch the next tile (the last iteration re-reads its own tile into the idle
-    // buffer: branch-free, so the staged values stay in registers)
-    const Staged st = load_tile(a, tc, min(t + 1, t1 - 1), tid);
-    if (wave_active) tile_compute(lds + buf * STAGE, qf, lane, tile_valid(a, t), sm);
-    store_tile(lds + (buf ^ 1) * STAGE, tid, st);
+  for (int t = t0; t < t1; t = uniform(t + 2)) {
+    if (t + 2 < t1) load_tile(a, tc, t + 2, tid, lds + ((t + 2) % NSTAGE) * STAGE);
+    if (t + 3 < t1) load_tile(a, tc, t + 3, tid, lds + ((t + 3) % NSTAGE) * STAGE);
+    if (wave_active) {
+      tile_compute(lds + (t % NSTAGE) * STAGE, qf, lane, tile_valid(a, t), sm);
+      if (t + 1 < t1) tile_compute(lds + ((t + 1) % NSTAGE) * STAGE, qf, lane, tile_valid(a, t + 1), sm);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
@@ -408,7 +436,7 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
 }
 
 __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+  __shared__ __attribute__((aligned(16))) uint16_t lds[NSTAGE * STAGE];
   __shared__ int s_val;
   const int tid = threadIdx.x;
 
