@@ -19,6 +19,8 @@ context equals the stream's mean context) and extrapolated to frames/s.
 Prints one JSON line on stdout; progress goes to stderr.
 """
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -29,6 +31,13 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_2609_23286_amd", "csrc")
+# Kernel -> the sources whose text decides its memory traffic; counters recorded for
+# other sources are stale and are not reported.
+KERNEL_SOURCES = {"attn_fwd_kernel": ("attend.hip", "rv_internal.h", "rv_host.cpp"),
+                  "admit_kernel": ("admit.hip", "rv_internal.h", "rv_host.cpp")}
+COPY_CALIBRATION_BYTES = 256 << 20   # read and written once by the calibration copy
 
 
 def log(*a):
@@ -49,6 +58,107 @@ def admit_bytes(N, H, d, n_q, k):
             + N * H * 4 * 2          # saliency written, then read by the selection
             + 2 * k * H * d * 2 * 2  # K and V rows read and appended
             + k * H * 8)             # provenance
+
+
+def kernel_source_hash(kernel):
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(kernel, workload):
+    return os.path.join(PROFILES, f"{kernel}__{workload}__hbm_traffic.md")
+
+
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter summary, or None when there is
+    none or the kernel's sources changed since it was taken."""
+    try:
+        text = open(traffic_path(kernel, workload)).read()
+    except OSError:
+        return None
+    kv = {}
+    for line in text.splitlines():
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].split(": ", 1)
+            kv[k.strip("` ")] = v.strip("` ")
+    if kv.get("source_hash") != kernel_source_hash(kernel):
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def summarize_pmc(fetch_dir, write_dir, workload):
+    """Reduce two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; counter CSVs) of this
+    benchmark started with --copy-calibration into per-launch HBM traffic.  The
+    calibration copy reads and writes COPY_CALIBRATION_BYTES once; the counters'
+    readings for it give the factors that turn KiB per dispatch into bytes."""
+    import csv
+
+    def per_kernel(d, counter):
+        out = {}
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] != counter:
+                    continue
+                name = r["Kernel_Name"]
+                out.setdefault(name, []).append(float(r["Counter_Value"]))
+        return out
+
+    fetch, write = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+
+    def find(d, key):
+        hits = [v for k, v in d.items() if key in k]
+        if not hits:
+            raise SystemExit(f"no dispatch of {key} in the counter CSVs")
+        return hits[0]
+
+    copy_key = "neg_kernel"
+    cf = max(find(fetch, copy_key))
+    cw = max(find(write, copy_key))
+    f_scale = COPY_CALIBRATION_BYTES / (cf * 1024.0)
+    w_scale = COPY_CALIBRATION_BYTES / (cw * 1024.0)
+    for kernel in KERNEL_SOURCES:
+        fv, wv = find(fetch, kernel), find(write, kernel)
+        f_kib, w_kib = sum(fv) / len(fv), sum(wv) / len(wv)
+        total = f_kib * 1024.0 * f_scale + w_kib * 1024.0 * w_scale
+        lines = [
+            f"# {kernel}: HBM traffic per launch, {workload}",
+            "",
+            "Two counter passes over the whole benchmark (one per counter), each with the",
+            "calibration copy of 256 MiB run first:",
+            "",
+            "```",
+            "cd /tmp && export TMPDIR=/tmp",
+            "timeout -s KILL 600 rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/fetch -o fetch -- \\",
+            "    python /root/repo/bench.py --no-cpu-baseline --copy-calibration",
+            "timeout -s KILL 600 rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/write -o write -- \\",
+            "    python /root/repo/bench.py --no-cpu-baseline --copy-calibration",
+            "python /root/repo/bench.py --pmc-summary <out>/fetch <out>/write",
+            "```",
+            "",
+            f"- dispatches: {len(fv)} (FETCH_SIZE pass), {len(wv)} (WRITE_SIZE pass)",
+            f"- fetch_kib_per_dispatch_mean: {f_kib:.1f}",
+            f"- write_kib_per_dispatch_mean: {w_kib:.1f}",
+            f"- copy_fetch_kib: {cf:.1f} (for {COPY_CALIBRATION_BYTES} bytes read)",
+            f"- copy_write_kib: {cw:.1f} (for {COPY_CALIBRATION_BYTES} bytes written)",
+            f"- fetch_scale: {f_scale:.4f}",
+            f"- write_scale: {w_scale:.4f}",
+            f"- hbm_bytes_per_launch: {total:.0f}",
+            f"- source_hash: {kernel_source_hash(kernel)}",
+            "",
+            "The source hash covers " + ", ".join(KERNEL_SOURCES[kernel]) + "; the benchmark",
+            "reports this traffic only while those files are unchanged.",
+        ]
+        path = traffic_path(kernel, workload)
+        with open(path, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+        print(f"{kernel}: {f_kib:.1f} KiB fetched, {w_kib:.1f} KiB written per dispatch -> "
+              f"{total / 1e6:.2f} MB per launch ({path})")
 
 
 def cpu_baseline(cfg, mean_ctx, n_frames):
@@ -83,7 +193,14 @@ def main():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--config", default="vitl_stack_1000")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run a 256 MiB device copy before the stream (HBM counter calibration)")
+    p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="summarise two rocprofv3 --pmc runs into profiles/ and exit")
     args = p.parse_args()
+    if args.pmc_summary:
+        summarize_pmc(*args.pmc_summary, args.config)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this path has no multi-GPU mode "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
@@ -107,6 +224,13 @@ def main():
         f"device free {free / 1e9:.1f} of {total / 1e9:.1f} GB")
     if T * frame_bytes > free - 8e9:
         raise SystemExit("not enough device memory to keep every frame's inputs resident")
+
+    if args.copy_calibration:
+        x = torch.ones(COPY_CALIBRATION_BYTES // 4, dtype=torch.float32, device=dev)
+        y = torch.empty_like(x)
+        torch.neg(x, out=y)
+        torch.cuda.synchronize()
+        del x, y
 
     # ---- inputs: every frame resident in HBM --------------------------------------
     t0 = time.perf_counter()
@@ -178,6 +302,8 @@ def main():
     t_start = time.perf_counter()
     for t in range(T):
         run_frame(t, events[t])
+        if (t + 1) % 250 == 0:
+            log(f"enqueued {t + 1} frames")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     rv.device_status()
@@ -220,12 +346,14 @@ def main():
                    "frames": T, "sampled_queries": n_q},
         "roofline": {"kernel": "attn_fwd_kernel", "bound": "mfma", "achieved": achieved_tf,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved_tf / PEAK_BF16_TFLOPS,
-                     "traffic": None, "avg_launch_us": attn_avg_s * 1e6,
+                     "traffic": recorded_traffic("attn_fwd_kernel", cfg.name),
+                     "avg_launch_us": attn_avg_s * 1e6,
                      "algorithmic_flops_per_launch": flops / n_attn},
         "phases": {"attention_ms": attn_ms, "admission_ms": admit_ms,
                    "admission_roofline": {"kernel": "admit_kernel", "bound": "hbm", "achieved": admit_gbs,
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": admit_gbs / PEAK_HBM_GBS,
+                                          "traffic": recorded_traffic("admit_kernel", cfg.name),
                                           "algorithmic_bytes_per_launch": bytes_admit / T}},
     }
     if not args.no_cpu_baseline:

@@ -22,9 +22,13 @@
 //   the common case (exact either way: the LSE uses the reference the sums were taken
 //   against).
 // * Scheduling: 1041 queries x 16 heads is only 144 units, too few for 256 CUs, so each
-//   unit's key range is split (stream-K).  Units are dealt to one queue per XCD; each
-//   queue's (unit, key tile) iterations are cut into equal chunks, one per workgroup,
-//   and the workgroup ids of a queue are the ones the hardware places on that XCD
+//   unit's key range is split.  Units are dealt to one queue per XCD (whole heads where
+//   possible); each queue's (unit, key tile) iterations, laid out with a stride of U
+//   tiles per unit, are cut into equal chunks of E tiles, one per workgroup.  With
+//   U = T (the unit's tile count) this is stream-K: chunks may straddle units.  With
+//   U = k E >= T every unit is cut into k aligned pieces, so the workgroups holding the
+//   query tiles of one head walk the same key tiles at the same time and share them in
+//   L2.  The workgroup ids of a queue are the ones the hardware places on that XCD
 //   (ids are dealt round-robin over the XCDs; verified at start-up and by every
 //   workgroup).  All partial results of a unit are thus written and merged under one
 //   L2: a contributor waits for its stores to reach L2 and bumps the unit's counter;
@@ -173,7 +177,7 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
     s1 = mfma32(kb, qf[ds], s1);
   }
   // accumulator entry r of this lane: key 8*(r/4) + 4*half + r%4 (+32 in s1)
-  if (valid < BK) {
+  if (__builtin_expect(valid < BK, 0)) {
     // keys >= valid get -1e30: sat(key + 1 - valid) is 1 exactly for them, 0 otherwise
     // (arithmetic masking keeps the 32 lane masks out of scalar registers)
     const float fv = (float)(valid - 4 * half - 1);
@@ -251,13 +255,40 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
 }
 
 // Merge every partial of `unit` (contributor chunks c_first..c_last of queue q, in
-// chunk order) and write the final output rows and LSE.  Thread -> (row, 32 dims); all
-// partial loads are issued before any is consumed.
-constexpr int kMergeMax = 8;
+// chunk order) and write the final output rows and LSE.  Thread -> (row, 32 dims).
+// Partials are taken eight at a time: their (m, l) pairs in one round trip, then their
+// rows kMergeBatch partials at a time; loads are unconditional (indices clamped, surplus
+// weights zero) so that each batch is in flight together.
+constexpr int kMergeGroup = 8;
+constexpr int kMergeBatch = 1;   // partials whose rows are in flight together
 
+// Partial slot of chunk c's segment of unit ui: slot 0 if the chunk starts inside the
+// unit, slot 1 if it began in an earlier unit.
 __device__ __forceinline__ const float* slot_ptr(const AttnArgs& a, int q, int c, int ui) {
-  const int slot = 2 * (a.chunk_base[q] + c) + ((int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1);
+  const int slot = 2 * (a.chunk_base[q] + c) + ((int64_t)c * a.E >= (int64_t)ui * a.U ? 0 : 1);
   return a.part + (int64_t)slot * kAttnSlotFloats;
+}
+
+template <int NB>
+__device__ __forceinline__ void merge_rows(const float* const* ps, const float* w, int row, int dh,
+                                           float (&acc)[32]) {
+  float4 v[NB][8];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const float4* po = reinterpret_cast<const float4*>(ps[j] + row * D + dh);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[j][e] = po[e];
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc[4 * e] = fmaf(w[j], v[j][e].x, acc[4 * e]);
+      acc[4 * e + 1] = fmaf(w[j], v[j][e].y, acc[4 * e + 1]);
+      acc[4 * e + 2] = fmaf(w[j], v[j][e].z, acc[4 * e + 2]);
+      acc[4 * e + 3] = fmaf(w[j], v[j][e].w, acc[4 * e + 3]);
+    }
+  }
 }
 
 __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_first, int c_last) {
@@ -270,44 +301,33 @@ __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_fir
   float acc[32];
 #pragma unroll
   for (int e = 0; e < 32; ++e) acc[e] = 0.f;
-  for (int c0 = c_first; c0 <= c_last; c0 += kMergeMax) {
-    const int n = min(kMergeMax, c_last - c0 + 1);
-    float mv[kMergeMax], lv[kMergeMax];
+  for (int c0 = c_first; c0 <= c_last; c0 += kMergeGroup) {
+    const int n = min(kMergeGroup, c_last - c0 + 1);
+    const float* ps[kMergeGroup];
+    float mv[kMergeGroup], lv[kMergeGroup];
 #pragma unroll
-    for (int j = 0; j < kMergeMax; ++j) {
-      if (j < n) {
-        const float* ps = slot_ptr(a, q, c0 + j, ui);
-        mv[j] = ps[BQ * D + row];
-        lv[j] = ps[BQ * D + BQ + row];
-      } else {
-        mv[j] = kNegBig;
-        lv[j] = 0.f;
-      }
+    for (int j = 0; j < kMergeGroup; ++j) {
+      ps[j] = slot_ptr(a, q, min(c0 + j, c_last), ui);
+      mv[j] = ps[j][BQ * D + row];
+      lv[j] = ps[j][BQ * D + BQ + row];
     }
     float m_new = mmax;
 #pragma unroll
-    for (int j = 0; j < kMergeMax; ++j) m_new = fmaxf(m_new, mv[j]);
+    for (int j = 0; j < kMergeGroup; ++j) m_new = fmaxf(m_new, mv[j]);  // clamped copies repeat a real one
     const float scale = __builtin_amdgcn_exp2f(mmax - m_new);
     L *= scale;
 #pragma unroll
     for (int e = 0; e < 32; ++e) acc[e] *= scale;
     mmax = m_new;
+    float w[kMergeGroup];
 #pragma unroll
-    for (int j = 0; j < kMergeMax; ++j) {
-      if (j < n) {
-        const float w = __builtin_amdgcn_exp2f(mv[j] - mmax);
-        L += w * lv[j];
-        const float4* po = reinterpret_cast<const float4*>(slot_ptr(a, q, c0 + j, ui) + row * D + dh);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float4 v = po[e];
-          acc[4 * e] += w * v.x;
-          acc[4 * e + 1] += w * v.y;
-          acc[4 * e + 2] += w * v.z;
-          acc[4 * e + 3] += w * v.w;
-        }
-      }
+    for (int j = 0; j < kMergeGroup; ++j) {
+      w[j] = j < n ? __builtin_amdgcn_exp2f(mv[j] - mmax) : 0.f;
+      L = fmaf(w[j], lv[j], L);
     }
+#pragma unroll
+    for (int b = 0; b < kMergeGroup; b += kMergeBatch)
+      if (b == 0 || b < n) merge_rows<kMergeBatch>(ps + b, w + b, row, dh, acc);
   }
   const float inv = 1.f / L;
   uint16_t* op = a.out + ((int64_t)qi * a.n_heads + h) * D + dh;
@@ -322,7 +342,7 @@ __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_fir
 __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int ui, int t0, int t1, uint16_t* lds,
                                int* s_flag) {
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = uniform(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
   unit = uniform(unit);
   t0 = uniform(t0);
@@ -396,7 +416,7 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   }
 
   // Partial result: publish, then the last contributor of the unit merges.
-  const int seg = (int64_t)c * a.E >= (int64_t)ui * a.T ? 0 : 1;
+  const int seg = (int64_t)c * a.E >= (int64_t)ui * a.U ? 0 : 1;
   float* ps = a.part + (int64_t)(2 * (a.chunk_base[q] + c) + seg) * kAttnSlotFloats;
   if (wave_active) {
     const int row = wave * 32 + l32;
@@ -420,8 +440,8 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   }
   __syncthreads();
-  const int c_first = (int)(((int64_t)ui * a.T) / a.E);
-  const int c_last = (int)(((int64_t)(ui + 1) * a.T - 1) / a.E);
+  const int c_first = (int)(((int64_t)ui * a.U) / a.E);
+  const int c_last = (int)(((int64_t)ui * a.U + a.T - 1) / a.E);
   if (tid == 0) *s_flag = atomicAdd(&a.unit_ctr[unit], 1) == c_last - c_first;
   __syncthreads();
   const bool last = *s_flag != 0;
@@ -450,15 +470,19 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
     __hip_atomic_fetch_or(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   if (c >= a.n_chunks[q]) return;
   const int ub = a.unit_base[q];
-  const int total = (a.unit_base[q + 1] - ub) * a.T;
+  const int total = (a.unit_base[q + 1] - ub) * a.U;
   int it = c * a.E;
   const int it_end = min(total, it + a.E);
   while (it < it_end) {
-    const int ui = it / a.T;
-    const int t0 = it - ui * a.T;
-    const int seg_end = min(it_end, (ui + 1) * a.T);
+    const int ui = it / a.U;
+    const int t0 = it - ui * a.U;
+    if (t0 >= a.T) {  // padding after the unit's last tile (split mode)
+      it = (ui + 1) * a.U;
+      continue;
+    }
+    const int seg_end = min(it_end, ui * a.U + a.T);
     process_segment(a, q, c, ub + ui, ui, t0, t0 + (seg_end - it), lds, &s_val);
-    it = seg_end;
+    it = (seg_end == ui * a.U + a.T) ? (ui + 1) * a.U : seg_end;
   }
 }
 

@@ -197,11 +197,15 @@ rv_status device_qidx(Workspace* ws, const rv_qsub& q, const int32_t** ptr, int*
   return RV_OK;
 }
 
-// Stream-K plan of one attention launch: units (head, 128-query tile) dealt in
-// contiguous ranges to the per-XCD queues; each queue's (unit, key tile) iterations cut
-// into chunks of E tiles, about kAttnWgPerCu chunks per CU.
+// Work plan of one attention launch: units (head, 128-query tile) are dealt in
+// contiguous ranges to the per-XCD queues, and each queue's (unit, key tile) iterations
+// are cut into chunks of E tiles, one per workgroup, about kAttnWgPerCu per CU.
+// k-way split: each unit's key range is cut into k aligned pieces (iteration stride
+// U = k E per unit), so the workgroups on one head's query tiles stream the same key
+// tiles together.  Stream-K: U = T, chunks may straddle units.  RV_ATTN_SPLIT forces
+// one (0: stream-K, k > 0: k-way).
 struct AttnPlan {
-  int q_tiles, nt_mem, T, n_units, E, grid, total_chunks;
+  int q_tiles, nt_mem, T, U, n_units, E, grid, total_chunks;
   int unit_base[rv::kMaxQueues + 1];
   int n_chunks[rv::kMaxQueues];
   int chunk_base[rv::kMaxQueues];
@@ -216,19 +220,38 @@ AttnPlan plan_attention(const Workspace& ws, int n_tokens, int64_t mem_len, int 
   const int nq = ws.n_queues;
   const int wg_per_queue =
       std::max(1, env_int("RV_ATTN_WG_PER_CU", rv::kAttnWgPerCu) * ws.n_cus / nq);
-  int64_t max_total = 0;
+  int max_units = 0;
   for (int q = 0; q <= nq; ++q) p.unit_base[q] = (int)((int64_t)q * p.n_units / nq);
-  for (int q = 0; q < nq; ++q)
-    max_total = std::max<int64_t>(max_total, (int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.T);
+  for (int q = 0; q < nq; ++q) max_units = std::max(max_units, p.unit_base[q + 1] - p.unit_base[q]);
   const int e_min = std::max(1, env_int("RV_ATTN_MIN_CHUNK", 2));
-  p.E = (int)std::max<int64_t>(e_min, ceil_div(max_total, wg_per_queue));
+  // Stream-K balances the tiles exactly but pays, per chunk that straddles two units,
+  // a second pipeline start and publish (a few tiles' time); the aligned split leaves
+  // some workgroup slots idle.  Take the split while its chunks are at most
+  // kSplitSlackTiles longer than stream-K's.
+  constexpr int kSplitSlackTiles = 6;
+  int k = env_int("RV_ATTN_SPLIT", -1);
+  if (k < 0) {
+    k = wg_per_queue / std::max(1, max_units);
+    const int64_t e_sk = ceil_div((int64_t)max_units * p.T, wg_per_queue);
+    if (k >= 1 && ceil_div(p.T, k) > e_sk + env_int("RV_ATTN_SPLIT_SLACK", kSplitSlackTiles)) k = 0;
+  }
+  if (k >= 1) {
+    p.E = (int)std::max<int64_t>(e_min, ceil_div(p.T, k));
+    k = (int)ceil_div(p.T, p.E);  // pieces that hold tiles
+    p.U = k * p.E;
+  } else {
+    p.U = p.T;
+    p.E = (int)std::max<int64_t>(e_min, ceil_div((int64_t)max_units * p.T, wg_per_queue));
+  }
   p.total_chunks = 0;
+  int max_chunks = 0;
   for (int q = 0; q < nq; ++q) {
-    p.n_chunks[q] = (int)ceil_div((int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.T, p.E);
+    p.n_chunks[q] = (int)ceil_div((int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.U, p.E);
     p.chunk_base[q] = p.total_chunks;
     p.total_chunks += p.n_chunks[q];
+    max_chunks = std::max(max_chunks, p.n_chunks[q]);
   }
-  p.grid = nq * wg_per_queue;
+  p.grid = nq * max_chunks;
   return p;
 }
 
@@ -533,6 +556,7 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   a.q_tiles = p.q_tiles;
   a.nt_mem = p.nt_mem;
   a.T = p.T;
+  a.U = p.U;
   a.n_units = p.n_units;
   a.n_queues = ws->n_queues;
   a.E = p.E;

@@ -43,6 +43,7 @@ struct AttnArgs {
   int q_tiles;
   int nt_mem;              // key tiles of the memory segment
   int T;                   // key tiles per unit (memory + frame)
+  int U;                   // iteration stride per unit: T (stream-K) or k * E >= T (k-way split)
   int n_units;             // n_heads * q_tiles
   int n_queues;
   int E;                   // key tiles per chunk

@@ -90,19 +90,28 @@ def test_attend_and_saliency_match_oracle(rv, N, H, M, sigma):
     assert (np.abs(sal - sal_o) <= SAL_RTOL * sal_o).all()
 
 
-@pytest.mark.parametrize("wg_per_cu,min_chunk", [("1", "1"), ("2", "2"), ("4", "1"), ("1", "100000")])
-def test_stream_k_plans_agree_with_oracle(rv, wg_per_cu, min_chunk, monkeypatch):
-    """Stream-K plans (chunks of one key tile, of a few, whole units) change only the
-    rounding order of the partial merges."""
+PLANS = [  # (workgroups per CU, minimum chunk, split: -1 auto, 0 stream-K, k > 0 k-way)
+    ("1", "1", "0"), ("2", "2", "0"), ("4", "1", "0"), ("1", "100000", "0"),
+    ("2", "2", "-1"), ("1", "1", "1"), ("2", "1", "7"), ("2", "1", "64"), ("4", "3", "-1"),
+]
+
+
+@pytest.mark.parametrize("wg_per_cu,min_chunk,split", PLANS)
+def test_work_plans_agree_with_oracle(rv, wg_per_cu, min_chunk, split, monkeypatch):
+    """Work plans (stream-K chunks of one key tile, of a few, whole units; aligned k-way
+    splits with k = 1, several, more pieces than tiles) change only the rounding order
+    of the partial merges."""
     monkeypatch.setenv("RV_ATTN_WG_PER_CU", wg_per_cu)
     monkeypatch.setenv("RV_ATTN_MIN_CHUNK", min_chunk)
-    N, H, M = 333, 4, 1500
-    Q, K, V = frame(7, N, H)
-    memK, memV = memory_rows(8, H, M)
-    out, lse, _ = run_attend(rv, Q, K, V, memK, memV, qsub_for(N), with_saliency=False)
-    out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M)
-    assert np.abs(out - out_o).max() <= OUT_ATOL
-    assert np.abs(lse - lse_o).max() <= LSE_ATOL
+    monkeypatch.setenv("RV_ATTN_SPLIT", split)
+    for N, H, M in ((333, 4, 1500), (1041, 16, 3000), (65, 1, 0)):
+        print(f"plan {wg_per_cu}/{min_chunk}/{split}: N={N} H={H} M={M}", flush=True)
+        Q, K, V = frame(7 + N, N, H)
+        memK, memV = memory_rows(8 + N, H, M)
+        out, lse, _ = run_attend(rv, Q, K, V, memK, memV, qsub_for(N), with_saliency=False)
+        out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M)
+        assert np.abs(out - out_o).max() <= OUT_ATOL
+        assert np.abs(lse - lse_o).max() <= LSE_ATOL
 
 
 def test_saliency_is_bit_reproducible(rv):
