@@ -1,23 +1,29 @@
 // admit.hip -- LSE-saliency, per-head top-k and memory append, gfx950.
 //
-// One workgroup (8 wave64s) owns one (layer, head): it computes the saliency of all N
-// keys of the frame, selects, and appends, with no communication between workgroups.
+// Two launches per call, each spread over the whole chip:
 //
-// Saliency (Sec. 3.3, saliency score and the A_ij equation): for key j of the frame,
+// sal_kernel (Sec. 3.3, saliency score and the A_ij equation): for key j of the frame,
 //   S_j = sum over sampled queries i of exp(q_i . k_j / 8 - LSE_i),
 // with the LSE the attention pass saved, so every term is an exact attention
-// probability and no score matrix is stored.  The sampled query rows and their LSE are
-// staged in LDS once.  A wave takes 128 keys at a time (four 32-key blocks whose K rows
-// stay in registers) and sweeps all sampled queries in blocks of 32 with
-// v_mfma_f32_32x32x16_bf16 (Z = Q~ K^T, each lane owning one key column); the
-// exponentials are summed in fp32 in a fixed order -- in-lane, then across the two lane
-// halves -- so S is bit-reproducible with no atomics.
+// probability and no score matrix is stored.  A (layer, head) is split over
+// `sal_groups` workgroups of 4 wave64s (about three per CU over the launch), each taking
+// a contiguous range of 32-key blocks.  The sampled query rows and their LSE are staged
+// in LDS once per workgroup; each wave then takes its blocks two at a time (K rows in
+// registers) and sweeps the sampled queries in blocks of 32 with
+// v_mfma_f32_32x32x16_bf16 (Z = Q~ K^T, each lane owning one key column).  The
+// exponentials are summed in fp32 in a fixed order -- in-lane, over query blocks, then
+// across the two lane halves -- so S is bit-reproducible with no atomics.  The work is
+// VALU-bound: one FMA, one exp and one add per (query, key).
 //
-// Selection (Sec. 3.3 Eq. 6, head-specific retention): the `budget` largest S_j, equal
-// values ordered by lower index: an MSB-first radix select over the fp32 bit patterns
-// (order-preserving for S >= 0) finds the exact threshold value and how many of its
-// ties to take; block scans then emit the chosen indices in ascending order.  The chosen
-// K/V rows are copied to the memory arena at rows mem_len.. with their provenance.
+// select_kernel (Sec. 3.3 Eq. 6, head-specific retention): one workgroup per
+// (layer, head) takes the `budget` largest S_j, equal values ordered by lower index.
+// The order is that of the 64-bit key (bits of S, ~j): fp32 bit patterns order like
+// the values for S >= 0.  Budgets up to kWaveTopK: each wave extracts the top `budget`
+// of its quarter by repeated wave-wide maxima, and the 4 x budget candidates are ranked
+// against each other.  Larger budgets: an MSB-first radix select over the bit patterns
+// finds the threshold value and how many of its ties to take, and block scans emit the
+// indices.  Either way the indices come out ascending and the chosen K/V rows are copied
+// to the memory arena at rows mem_len.. with their provenance.
 #include "rv_internal.h"
 
 namespace rv {
@@ -27,26 +33,167 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int D = kHeadDim;
-constexpr int NT = kAdmitThreads;
+constexpr int NT = kAdmitThreads;  // 256
 constexpr int NW = NT / 64;
-constexpr int QS_STRIDE = D + 8;  // staged sampled-query rows, 144 bytes
+constexpr int kBlocksPerStep = 2;  // 32-key blocks a saliency wave holds at once
+constexpr int QS_STRIDE = D + 8;   // staged sampled-query rows, 144 bytes
+constexpr int kStageBatch = 12;    // 16-byte query-row loads in flight per thread
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kScaleLog2 = kLog2e * 0.125f;
 
-// Inclusive prefix sum over the workgroup's threads.
-__device__ int block_inclusive_scan(int v, int* s_wave) {
+static_assert(NT == 256, "the radix histogram has one bin per thread");
+
+// ---- saliency -----------------------------------------------------------------------
+
+__global__ __launch_bounds__(NT) void sal_kernel(AdmitArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int H = a.n_heads, N = a.n_tokens, tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, half = lane >> 5;
+  const int groups = a.sal_groups;
+  const int lh = blockIdx.x / groups, g = blockIdx.x - lh * groups;
+  const int layer = lh / H, h = lh - layer * H;
+  const AdmitLayer& L = a.layer[layer];
+  const int n_blocks = (N + 31) / 32;
+  const int per_group = (n_blocks + groups - 1) / groups;
+  const int blk0 = g * per_group, blk1 = min(n_blocks, blk0 + per_group);
+  if (blk0 >= blk1) return;  // uniform over the workgroup
+  const int nq_pad = (a.n_q + 31) & ~31;
+  float* s_lse2 = reinterpret_cast<float*>(smem);
+  uint16_t* s_q = a.stage_queries ? reinterpret_cast<uint16_t*>(smem + (size_t)nq_pad * 4) : nullptr;
+
+  // LSE of the sampled queries in log2 units (padding rows: +inf -> weight 0) and, when
+  // they fit, the sampled query rows (padding rows zero).  Loads are issued in batches
+  // of kStageBatch per thread before any is stored, so a batch costs one round trip.
+  auto q_token = [&](int i) {
+    const int qi = i / a.q_cols;
+    return a.q_base + qi * a.q_row_stride + (i - qi * a.q_cols) * a.q_col_stride;
+  };
+  // K rows (B operands, K^T) of a step's blocks: lane's key, dims ds*16 + half*8 ..;
+  // the first step's rows are requested before the staging, each next step's rows
+  // while the current step computes.
+  auto load_k = [&](int bb, bf16x8 (&kf)[kBlocksPerStep][4]) {
+#pragma unroll
+    for (int b = 0; b < kBlocksPerStep; ++b) {
+      const int j = min((bb + b) * 32 + l32, N - 1);  // past the frame or the range: result unused
+      const uint16_t* kp = L.K + ((int64_t)j * H + h) * D + half * 8;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds) kf[b][ds] = *reinterpret_cast<const bf16x8*>(kp + ds * 16);
+    }
+  };
+  bf16x8 kf[kBlocksPerStep][4], kn[kBlocksPerStep][4];
+  int bb = blk0 + wave * kBlocksPerStep;
+  if (bb < blk1) load_k(bb, kf);
+
+  for (int i0 = 0; i0 < nq_pad; i0 += NT * 4) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * NT + tid;
+      v[u] = i < a.n_q ? L.lse[(int64_t)h * N + q_token(i)] : __builtin_inff();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * NT + tid;
+      if (i < nq_pad) s_lse2[i] = v[u] * kLog2e;
+    }
+  }
+  if (s_q) {
+    for (int c0 = 0; c0 < nq_pad * 8; c0 += NT * kStageBatch) {
+      uint4 v[kStageBatch];
+#pragma unroll
+      for (int u = 0; u < kStageBatch; ++u) {
+        const int c = c0 + u * NT + tid, i = c >> 3, ch = c & 7;
+        v[u] = uint4{0u, 0u, 0u, 0u};
+        if (i < a.n_q) v[u] = *reinterpret_cast<const uint4*>(L.Q + ((int64_t)q_token(i) * H + h) * D + ch * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < kStageBatch; ++u) {
+        const int c = c0 + u * NT + tid, i = c >> 3, ch = c & 7;
+        if (i < nq_pad) *reinterpret_cast<uint4*>(&s_q[i * QS_STRIDE + ch * 8]) = v[u];
+      }
+    }
+  }
+  __syncthreads();
+
+  // Query row of sampled query qa for the A operand when the rows are not staged.
+  auto q_global = [&](int qa) -> const uint16_t* {
+    const int i = min(qa, a.n_q - 1);
+    const int qi = i / a.q_cols;
+    const int tok = a.q_base + qi * a.q_row_stride + (i - qi * a.q_cols) * a.q_col_stride;
+    return L.Q + ((int64_t)tok * H + h) * D + half * 8;
+  };
+
+  for (; bb < blk1; bb += NW * kBlocksPerStep) {
+    const int nb = min(kBlocksPerStep, blk1 - bb);
+    if (bb + NW * kBlocksPerStep < blk1) load_k(bb + NW * kBlocksPerStep, kn);
+    float acc[kBlocksPerStep] = {};
+    for (int qb = 0; qb < nq_pad; qb += 32) {
+      bf16x8 qf[4];
+      if (s_q) {
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds)
+          qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[(qb + l32) * QS_STRIDE + ds * 16 + half * 8]);
+      } else {
+        const uint16_t* qp = q_global(qb + l32);
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
+      }
+      // LSE of this lane's 16 accumulator rows: queries qb + 8*(r/4) + 4*half + r%4
+      float l2[16];
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const float4 v = *reinterpret_cast<const float4*>(&s_lse2[qb + 8 * r4 + 4 * half]);
+        l2[4 * r4] = v.x;
+        l2[4 * r4 + 1] = v.y;
+        l2[4 * r4 + 2] = v.z;
+        l2[4 * r4 + 3] = v.w;
+      }
+#pragma unroll
+      for (int b = 0; b < kBlocksPerStep; ++b) {
+        f32x16 z = {};
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds) z = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z, 0, 0, 0);
+        float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          s0 += __builtin_amdgcn_exp2f(fmaf(z[r], kScaleLog2, -l2[r]));
+          s1 += __builtin_amdgcn_exp2f(fmaf(z[r + 1], kScaleLog2, -l2[r + 1]));
+        }
+        acc[b] += s0 + s1;
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < kBlocksPerStep; ++b) {
+      const float tot = acc[b] + __shfl_xor(acc[b], 32);
+      const int j = (bb + b) * 32 + l32;
+      if (b < nb && half == 0 && j < N) L.sal[(int64_t)h * N + j] = tot;
+    }
+#pragma unroll
+    for (int b = 0; b < kBlocksPerStep; ++b)
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds) kf[b][ds] = kn[b][ds];
+  }
+}
+
+// ---- selection and append -----------------------------------------------------------
+
+// Exclusive prefix sum over the workgroup's threads (every thread must call it).
+__device__ int block_exclusive_scan(int v, int* s_wave) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
-    const int u = __shfl_up(v, off);
-    if (lane >= off) v += u;
+    const int u = __shfl_up(x, off);
+    if (lane >= off) x += u;
   }
-  if (lane == 63) s_wave[wave] = v;
+  if (lane == 63) s_wave[wave] = x;
   __syncthreads();
   int base = 0;
-  for (int w = 0; w < wave; ++w) base += s_wave[w];
+#pragma unroll
+  for (int w = 0; w < NW; ++w) base += w < wave ? s_wave[w] : 0;
   __syncthreads();
-  return v + base;
+  return base + x - v;
 }
 
 // Top-`budget` of sal[0..N) (ties -> lower index), ascending, into s_idx[0..budget).
@@ -54,7 +201,7 @@ __device__ void select_topk(const float* sal, int N, int budget, int32_t* s_idx)
   __shared__ unsigned int hist[256];
   __shared__ int s_wave[NW];
   __shared__ int s_bin, s_need;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
 
   if (budget >= N) {
     for (int j = tid; j < N; j += NT) s_idx[j] = j;
@@ -66,27 +213,40 @@ __device__ void select_topk(const float* sal, int N, int budget, int32_t* s_idx)
   unsigned int prefix = 0u, mask = 0u;
   int need = budget;
   for (int shift = 24; shift >= 0; shift -= 8) {
-    if (tid < 256) hist[tid] = 0u;
+    hist[tid] = 0u;  // NT == 256 bins
     __syncthreads();
     for (int j = tid; j < N; j += NT) {
       const unsigned int kj = __float_as_uint(sal[j]);
       if ((kj & mask) == prefix) atomicAdd(&hist[(kj >> shift) & 255u], 1u);
     }
     __syncthreads();
-    // thread i < 256 holds bin 255 - i: the inclusive scan counts digits >= bin
-    const int b = 255 - tid;
-    const int cnt = tid < 256 ? (int)hist[b] : 0;
-    const int ge = block_inclusive_scan(cnt, s_wave);
-    const int gt = ge - cnt;
-    if (tid < 256 && gt < need && need <= ge) {
-      s_bin = b;
-      s_need = need - gt;
+    if (tid < 64) {
+      // lane i holds bins 255-4i .. 252-4i (descending); suffix counts by a wave scan
+      unsigned int c[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) c[m] = hist[255 - 4 * lane - m];
+      const unsigned int tot = c[0] + c[1] + c[2] + c[3];
+      unsigned int x = tot;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const unsigned int u = __shfl_up(x, off);
+        if (lane >= off) x += u;
+      }
+      unsigned int ge = x - tot;  // elements in bins above this lane's first bin
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const unsigned int gt = ge;
+        ge += c[m];
+        if (gt < (unsigned int)need && (unsigned int)need <= ge) {
+          s_bin = 255 - 4 * lane - m;
+          s_need = need - (int)gt;
+        }
+      }
     }
     __syncthreads();
     prefix |= (unsigned int)s_bin << shift;
     mask |= 255u << shift;
     need = s_need;
-    __syncthreads();
   }
   const unsigned int tau = prefix;  // the budget-th largest value; take `need` of its ties
 
@@ -100,10 +260,10 @@ __device__ void select_topk(const float* sal, int N, int budget, int32_t* s_idx)
     n_gt += kj > tau;
     n_eq += kj == tau;
   }
-  const int eq_before = block_inclusive_scan(n_eq, s_wave) - n_eq;
+  const int eq_before = block_exclusive_scan(n_eq, s_wave);
   const int take_eq = max(0, min(n_eq, need - eq_before));
   const int n_sel = n_gt + take_eq;
-  int pos = block_inclusive_scan(n_sel, s_wave) - n_sel;
+  int pos = block_exclusive_scan(n_sel, s_wave);
   int eq_seen = eq_before;
   for (int j = j0; j < j1; ++j) {
     const unsigned int kj = __float_as_uint(sal[j]);
@@ -117,12 +277,116 @@ __device__ void select_topk(const float* sal, int N, int budget, int32_t* s_idx)
   __syncthreads();
 }
 
-// Select for (layer, h) from s_sal and append the chosen rows.
-__device__ void select_and_append(const AdmitArgs& a, const AdmitLayer& L, int h, const float* s_sal,
-                                  int32_t* s_idx) {
-  const int N = a.n_tokens, H = a.n_heads, k = a.budget, tid = threadIdx.x;
-  if (k == 0) return;
-  select_topk(s_sal, N, k, s_idx);
+// Order key of token j: saliency bits above, ~j below, so larger keys are larger
+// saliencies and, among equal ones, lower indices.  0 marks "no candidate".
+__device__ __forceinline__ uint64_t rank_key(float v, int j) {
+  return ((uint64_t)__float_as_uint(v) << 32) | (uint32_t)~(uint32_t)j;
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, 0xF, 0xF, false);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Maximum over the wave's 64 lanes: DPP within each 16-lane row (quad swaps, half
+// mirror, mirror), then the four row results read out as scalars.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+  x = max_u64(x, dpp_u64<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = max_u64(x, dpp_u64<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = max_u64(x, dpp_u64<0x141>(x));  // row_half_mirror
+  x = max_u64(x, dpp_u64<0x140>(x));  // row_mirror
+  return max_u64(max_u64(readlane_u64(x, 0), readlane_u64(x, 16)), max_u64(readlane_u64(x, 32), readlane_u64(x, 48)));
+}
+
+// Top-`budget` (budget <= kWaveTopK) of sal[0..N), ascending, into s_idx.  Wave w owns
+// tokens [w*Q, (w+1)*Q), lane l the tokens w*Q + l + 64 m (m < kLaneSlots), kept as
+// keys sorted in registers.  Each round the wave's best remaining key is found by a
+// wave-wide maximum and its lane drops it.  The 4 x budget winners are then ranked
+// among themselves.
+constexpr int kWaveTopK = 32;
+constexpr int kLaneSlots = 8;  // tokens per lane: the wave path takes N <= 4 * 64 * 8
+
+__device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx, uint64_t* s_cand) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Q = (N + NW - 1) / NW;
+  const int lo = min(N, wave * Q), hi = min(N, lo + Q);
+  uint64_t v[kLaneSlots];
+#pragma unroll
+  for (int m = 0; m < kLaneSlots; ++m) {
+    const int j = lo + lane + 64 * m;
+    v[m] = j < hi ? rank_key(sal[j], j) : 0;
+  }
+#pragma unroll
+  for (int i = 0; i < kLaneSlots - 1; ++i) {  // descending
+#pragma unroll
+    for (int m = 0; m < kLaneSlots - 1 - i; ++m) {
+      const uint64_t x = v[m], y = v[m + 1];
+      v[m] = x > y ? x : y;
+      v[m + 1] = x > y ? y : x;
+    }
+  }
+  for (int r = 0; r < budget; ++r) {
+    const uint64_t win = wave_max_u64(v[0]);
+    if (lane == 0) s_cand[wave * budget + r] = win;
+    if (win != 0 && win == v[0]) {  // this lane owns the winner (keys are distinct)
+#pragma unroll
+      for (int m = 0; m < kLaneSlots - 1; ++m) v[m] = v[m + 1];
+      v[kLaneSlots - 1] = 0;
+    }
+  }
+  __syncthreads();
+  // candidate c is chosen if fewer than `budget` candidates outrank it; its output slot
+  // is the number of chosen candidates with a lower token index
+  const int nc = NW * budget;
+  __shared__ int s_chosen[NW * kWaveTopK];
+  for (int c = tid; c < nc; c += NT) {
+    const uint64_t kc = s_cand[c];
+    int above = 0;
+    for (int u = 0; u < nc; ++u) above += s_cand[u] > kc;
+    s_chosen[c] = kc != 0 && above < budget;
+  }
+  __syncthreads();
+  for (int c = tid; c < nc; c += NT) {
+    if (!s_chosen[c]) continue;
+    const uint32_t jc = ~(uint32_t)s_cand[c];
+    int pos = 0;
+    for (int u = 0; u < nc; ++u) pos += s_chosen[u] && ~(uint32_t)s_cand[u] < jc;
+    s_idx[pos] = (int32_t)jc;
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(NT) void select_kernel(AdmitArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  __shared__ uint64_t s_cand[NW * kWaveTopK];
+  const int H = a.n_heads, N = a.n_tokens, k = a.budget, tid = threadIdx.x;
+  const int layer = blockIdx.x / H, h = blockIdx.x - layer * H;
+  const AdmitLayer& L = a.layer[layer];
+  float* s_sal = reinterpret_cast<float*>(smem);
+  int32_t* s_idx = reinterpret_cast<int32_t*>(smem + (((size_t)N * 4 + 15) & ~(size_t)15));
+
+  const float* gs = L.sal + (int64_t)h * N;
+  if ((N & 3) == 0) {
+    for (int j = tid; j < N / 4; j += NT)
+      reinterpret_cast<float4*>(s_sal)[j] = reinterpret_cast<const float4*>(gs)[j];
+  } else {
+    for (int j = tid; j < N; j += NT) s_sal[j] = gs[j];
+  }
+  __syncthreads();
+  if (k <= kWaveTopK && k < N && N <= NW * 64 * kLaneSlots)
+    select_small(s_sal, N, k, s_idx, s_cand);
+  else
+    select_topk(s_sal, N, k, s_idx);
   if (L.idx)
     for (int r = tid; r < k; r += NT) L.idx[(int64_t)h * k + r] = s_idx[r];
   // 16-byte chunks: 8 per K row, 8 per V row.
@@ -144,145 +408,62 @@ __device__ void select_and_append(const AdmitArgs& a, const AdmitLayer& L, int h
   }
 }
 
-// Saliency of all N keys of (layer, h) into s_sal (and L.sal).
-__device__ void saliency(const AdmitArgs& a, const AdmitLayer& L, int h, float* s_sal, float* s_lse2,
-                         uint16_t* s_q) {
-  const int N = a.n_tokens, H = a.n_heads, tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6, l32 = lane & 31, half = lane >> 5;
-  const int nq_pad = (a.n_q + 31) & ~31;
-  const bool staged = s_q != nullptr;
-
-  // LSE of the sampled queries in log2 units (padding rows: +inf -> weight 0), and the
-  // sampled query rows themselves (padding rows zero).
-  for (int i = tid; i < nq_pad; i += NT)
-    s_lse2[i] = i < a.n_q ? L.lse[(int64_t)h * N + a.qidx[i]] * kLog2e : __builtin_inff();
-  if (staged) {
-    for (int c = tid; c < nq_pad * 8; c += NT) {
-      const int i = c >> 3, ch = c & 7;
-      uint4 v = {0u, 0u, 0u, 0u};
-      if (i < a.n_q) v = *reinterpret_cast<const uint4*>(L.Q + ((int64_t)a.qidx[i] * H + h) * D + ch * 8);
-      *reinterpret_cast<uint4*>(&s_q[i * QS_STRIDE + ch * 8]) = v;
-    }
-  }
-  __syncthreads();
-
-  const int n_blocks = (N + 31) / 32;
-  const int n_groups = (n_blocks + 3) / 4;
-  for (int g = wave; g < n_groups; g += NW) {
-    // B operands (K^T) of up to four 32-key blocks: lane's key, dims ds*16 + half*8 ..
-    bf16x8 kf[4][4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int j = (4 * g + b) * 32 + l32;
-      if (j < N) {
-        const uint16_t* kp = L.K + ((int64_t)j * H + h) * D + half * 8;
-#pragma unroll
-        for (int ds = 0; ds < 4; ++ds) kf[b][ds] = *reinterpret_cast<const bf16x8*>(kp + ds * 16);
-      } else {
-#pragma unroll
-        for (int ds = 0; ds < 4; ++ds) kf[b][ds] = bf16x8{};
-      }
-    }
-    const int nb = min(4, n_blocks - 4 * g);
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int qb = 0; qb < nq_pad; qb += 32) {
-      bf16x8 qf[4];
-      const int qa = qb + l32;
-      if (staged) {
-#pragma unroll
-        for (int ds = 0; ds < 4; ++ds)
-          qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[qa * QS_STRIDE + ds * 16 + half * 8]);
-      } else if (qa < a.n_q) {
-        const uint16_t* qp = L.Q + ((int64_t)a.qidx[qa] * H + h) * D + half * 8;
-#pragma unroll
-        for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
-      } else {
-#pragma unroll
-        for (int ds = 0; ds < 4; ++ds) qf[ds] = bf16x8{};
-      }
-      // LSE of this lane's 16 accumulator rows: queries qb + 8*(r/4) + 4*half + r%4
-      float l2[16];
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const float4 v = *reinterpret_cast<const float4*>(&s_lse2[qb + 8 * r4 + 4 * half]);
-        l2[4 * r4] = v.x;
-        l2[4 * r4 + 1] = v.y;
-        l2[4 * r4 + 2] = v.z;
-        l2[4 * r4 + 3] = v.w;
-      }
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        if (b < nb) {
-          f32x16 z = {};
-#pragma unroll
-          for (int ds = 0; ds < 4; ++ds) z = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z, 0, 0, 0);
-          float s = 0.f;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) s += __builtin_amdgcn_exp2f(fmaf(z[r], kScaleLog2, -l2[r]));
-          acc[b] += s;
-        }
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const float tot = acc[b] + __shfl_xor(acc[b], 32);
-      const int j = (4 * g + b) * 32 + l32;
-      if (half == 0 && j < N) {
-        s_sal[j] = tot;
-        L.sal[(int64_t)h * N + j] = tot;
-      }
-    }
-  }
-  __syncthreads();
+size_t sal_lds_bytes(const AdmitArgs& a) {
+  const size_t nq_pad = (size_t)((a.n_q + 31) & ~31);
+  return nq_pad * 4 + (a.stage_queries ? nq_pad * QS_STRIDE * 2 : 0);
 }
 
-__global__ __launch_bounds__(NT) void admit_kernel(AdmitArgs a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int H = a.n_heads, N = a.n_tokens, tid = threadIdx.x;
-  const int layer = blockIdx.x / H, h = blockIdx.x % H;
-  const AdmitLayer& L = a.layer[layer];
-  float* s_sal = reinterpret_cast<float*>(smem);
-  unsigned char* rest = smem + (((size_t)N * 4 + 15) & ~(size_t)15);
+size_t select_lds_bytes(const AdmitArgs& a) {
+  return (((size_t)a.n_tokens * 4 + 15) & ~(size_t)15) + (size_t)a.budget * 4;
+}
 
-  if (a.mode == kModeSelect) {
-    for (int j = tid; j < N; j += NT) s_sal[j] = L.sal[(int64_t)h * N + j];
-    __syncthreads();
-  } else {
-    const int nq_pad = (a.n_q + 31) & ~31;
-    float* s_lse2 = reinterpret_cast<float*>(rest);
-    uint16_t* s_q = a.stage_queries ? reinterpret_cast<uint16_t*>(rest + (size_t)nq_pad * 4) : nullptr;
-    saliency(a, L, h, s_sal, s_lse2, s_q);
-    if (a.mode == kModeSaliency) return;
-  }
-  select_and_append(a, L, h, s_sal, reinterpret_cast<int32_t*>(rest));
+hipError_t set_lds_limit(const void* kernel, int* cached, int limit) {
+  if (*cached == limit) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, limit);
+  if (e == hipSuccess) *cached = limit;
+  return e;
 }
 
 }  // namespace
 
 size_t admit_lds_bytes(const AdmitArgs& a) {
-  const size_t sal = ((size_t)a.n_tokens * 4 + 15) & ~(size_t)15;
-  const size_t nq_pad = (size_t)((a.n_q + 31) & ~31);
-  size_t rest = (size_t)a.budget * 4;
-  if (a.mode != kModeSelect) {
-    size_t sal_rest = nq_pad * 4 + (a.stage_queries ? nq_pad * QS_STRIDE * 2 : 0);
-    rest = rest > sal_rest ? rest : sal_rest;
-  }
-  return sal + rest;
+  size_t need = 0;
+  if (a.mode & kModeSaliency) need = sal_lds_bytes(a);
+  if ((a.mode & kModeSelect) && select_lds_bytes(a) > need) need = select_lds_bytes(a);
+  return need;
 }
 
 int admit_max_dynamic_lds(int max_lds) { return max_lds - kAdmitStaticLdsMargin; }
 
+void plan_saliency(AdmitArgs* a, int n_lh, int n_cus, int max_lds) {
+  // About three 4-wave workgroups per CU over the launch, and at least one 32-key
+  // block per wave.
+  const int n_blocks = (a->n_tokens + 31) / 32;
+  const int max_groups = n_blocks / NW > 1 ? n_blocks / NW : 1;
+  int g = (3 * n_cus + n_lh - 1) / (n_lh > 0 ? n_lh : 1);
+  a->sal_groups = g < 1 ? 1 : (g > max_groups ? max_groups : g);
+  a->stage_queries = 1;
+  if (sal_lds_bytes(*a) > (size_t)admit_max_dynamic_lds(max_lds)) a->stage_queries = 0;
+}
+
 hipError_t launch_admit(const AdmitArgs& a, int max_lds, hipStream_t s) {
-  static int attr_set = 0;
+  static int sal_attr = 0, sel_attr = 0;
   const int limit = admit_max_dynamic_lds(max_lds);
-  if (attr_set != limit) {
-    hipError_t e = hipFuncSetAttribute((const void*)admit_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       limit);
+  if (a.mode & kModeSaliency) {
+    hipError_t e = set_lds_limit((const void*)sal_kernel, &sal_attr, limit);
     if (e != hipSuccess) return e;
-    attr_set = limit;
+    const unsigned grid = (unsigned)(a.n_layers * a.n_heads) * (unsigned)a.sal_groups;
+    hipLaunchKernelGGL(sal_kernel, dim3(grid), dim3(NT), sal_lds_bytes(a), s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(admit_kernel, dim3((unsigned)(a.n_layers * a.n_heads)), dim3(NT), admit_lds_bytes(a), s, a);
-  return hipGetLastError();
+  if ((a.mode & kModeSelect) && a.budget > 0) {
+    hipError_t e = set_lds_limit((const void*)select_kernel, &sel_attr, limit);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)(a.n_layers * a.n_heads)), dim3(NT), select_lds_bytes(a), s, a);
+    return hipGetLastError();
+  }
+  return hipSuccess;
 }
 
 }  // namespace rv

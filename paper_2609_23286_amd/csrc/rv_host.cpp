@@ -12,7 +12,6 @@
 #include <map>
 #include <mutex>
 #include <string>
-#include <tuple>
 #include <vector>
 
 #include "rv_internal.h"
@@ -65,7 +64,6 @@ struct Workspace {
   bool safe = false;         // workgroup placement not round-robin: device-scope fences
   float* sal = nullptr;      // saliency staging when the caller passes none
   size_t sal_floats = 0;
-  std::map<std::tuple<int, int, int, int>, std::pair<int32_t*, int>> qidx;  // per query subset
 };
 constexpr size_t kCtrlErrOffsetBytes = 0;
 constexpr size_t kCtrlBytes = 256;
@@ -158,12 +156,17 @@ rv_status current_ws(Workspace** out) {
   return RV_OK;
 }
 
-// Sampled query positions for a frame layout (Sec. 3.3, head-specific retention).
-std::vector<int32_t> qsub_positions(const rv_qsub& q) {
-  std::vector<int32_t> v;
-  for (int r = 0; r < q.grid_h; r += q.stride)
-    for (int c = 0; c < q.grid_w; c += q.stride) v.push_back(q.n_special + r * q.grid_w + c);
-  return v;
+// Sampled queries (Sec. 3.3, head-specific retention): query i of the subset is frame
+// token q_base + (i / q_cols) * q_row_stride + (i % q_cols) * q_col_stride, the
+// top-left patch of the i-th stride x stride window in row-major window order.
+void set_qsub(rv::AdmitArgs* b, const rv_qsub& q) {
+  const int rows = (q.grid_h + q.stride - 1) / q.stride;
+  const int cols = (q.grid_w + q.stride - 1) / q.stride;
+  b->n_q = rows * cols;
+  b->q_cols = cols > 0 ? cols : 1;
+  b->q_base = q.n_special;
+  b->q_row_stride = q.stride * q.grid_w;
+  b->q_col_stride = q.stride;
 }
 
 rv_status check_qsub(const rv_qsub* qs, int n_tokens) {
@@ -173,27 +176,6 @@ rv_status check_qsub(const rv_qsub* qs, int n_tokens) {
   if ((int64_t)qs->grid_h * qs->grid_w + qs->n_special != n_tokens)
     return fail(RV_ERR_INVALID, "query subset %dx%d+%d does not describe %d tokens", qs->grid_h,
                 qs->grid_w, qs->n_special, n_tokens);
-  return RV_OK;
-}
-
-rv_status device_qidx(Workspace* ws, const rv_qsub& q, const int32_t** ptr, int* n) {
-  auto key = std::make_tuple(q.grid_h, q.grid_w, q.n_special, q.stride);
-  auto it = ws->qidx.find(key);
-  if (it == ws->qidx.end()) {
-    std::vector<int32_t> v = qsub_positions(q);
-    int32_t* d = nullptr;
-    RV_HIP(hipMalloc(&d, std::max<size_t>(1, v.size()) * sizeof(int32_t)), "qidx alloc");
-    if (!v.empty()) {
-      hipError_t e = hipMemcpy(d, v.data(), v.size() * sizeof(int32_t), hipMemcpyHostToDevice);
-      if (e != hipSuccess) {
-        (void)hipFree(d);
-        return hip_fail(e, "qidx upload");
-      }
-    }
-    it = ws->qidx.emplace(key, std::make_pair(d, (int)v.size())).first;
-  }
-  *ptr = it->second.first;
-  *n = it->second.second;
   return RV_OK;
 }
 
@@ -531,12 +513,6 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   const AttnPlan p = plan_attention(*ws, n_tokens, mem_len, n_heads);
   st = reserve_attention(ws, p);
   if (st != RV_OK) return st;
-  const int32_t* qidx = nullptr;
-  int n_q = 0;
-  if (saliency) {
-    st = device_qidx(ws, *qs, &qidx, &n_q);
-    if (st != RV_OK) return st;
-  }
 
   rv::AttnArgs a{};
   a.Q = (const uint16_t*)Q;
@@ -575,14 +551,12 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
     b.layer[0].K = (const uint16_t*)K;
     b.layer[0].lse = lse;
     b.layer[0].sal = saliency;
-    b.qidx = qidx;
-    b.n_q = n_q;
+    set_qsub(&b, *qs);
     b.n_tokens = n_tokens;
     b.n_heads = n_heads;
     b.n_layers = 1;
     b.mode = rv::kModeSaliency;
-    b.stage_queries = 1;
-    if (rv::admit_lds_bytes(b) > (size_t)rv::admit_max_dynamic_lds(ws->max_lds)) b.stage_queries = 0;
+    rv::plan_saliency(&b, n_heads, ws->n_cus, ws->max_lds);
     RV_HIP(rv::launch_admit(b, ws->max_lds, s), "saliency launch");
   }
   return RV_OK;
@@ -657,18 +631,14 @@ rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const*
   Workspace* ws;
   st = current_ws(&ws);
   if (st != RV_OK) return st;
-  const int32_t* qidx = nullptr;
-  int n_q = 0;
-  st = device_qidx(ws, *qs, &qidx, &n_q);
-  if (st != RV_OK) return st;
   rv::AdmitArgs probe{};
+  set_qsub(&probe, *qs);
   probe.n_tokens = n_tokens;
-  probe.n_q = n_q;
   probe.budget = budget;
   probe.mode = rv::kModeBoth;
-  probe.stage_queries = 1;
+  probe.n_heads = H;
+  rv::plan_saliency(&probe, std::min(n_layers, rv::kMaxLayersPerLaunch) * H, ws->n_cus, ws->max_lds);
   const size_t lds_cap = (size_t)rv::admit_max_dynamic_lds(ws->max_lds);
-  if (rv::admit_lds_bytes(probe) > lds_cap) probe.stage_queries = 0;
   if (rv::admit_lds_bytes(probe) > lds_cap)
     return fail(RV_ERR_INVALID, "frame too large for the admission workgroup's LDS");
   const int chunk_layers = std::min(n_layers, rv::kMaxLayersPerLaunch);
@@ -702,7 +672,6 @@ rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const*
       L.mem_len = mems[l]->len;
       L.head_stride = mems[l]->cap;
     }
-    b.qidx = qidx;
     b.n_heads = H;
     b.n_layers = nl;
     b.frame_id = frame_id;

@@ -10,9 +10,7 @@ constexpr int kHeadDim = 64;     // head dimension supported by every kernel
 constexpr int kAttnBQ = 128;     // queries per attention workgroup (4 waves x 32)
 constexpr int kAttnBK = 64;      // keys per staged K/V tile
 constexpr int kAttnThreads = 256;
-constexpr int kMaxSplits = 16;   // split-KV partitions per (head, query tile)
-constexpr int kSalBK = 128;      // keys per saliency workgroup (4 waves x 32)
-constexpr int kAdmitThreads = 512;   // one workgroup per (layer, head)
+constexpr int kAdmitThreads = 256;  // saliency and selection workgroups
 constexpr int kMaxTokens = 16384;  // frame size limit (LDS-resident sampled queries and selected indices)
 constexpr int kMaxLayersPerLaunch = 24;
 
@@ -73,32 +71,39 @@ struct AdmitLayer {
 enum AdmitMode : int {
   kModeSaliency = 1,       // saliency only
   kModeSelect = 2,         // selection + append from a given saliency
-  kModeBoth = 3,           // saliency, then selection + append, in one workgroup per (layer, head)
+  kModeBoth = 3,           // saliency, then selection + append (two launches)
 };
 
 struct AdmitArgs {
   AdmitLayer layer[kMaxLayersPerLaunch];
-  const int32_t* qidx;     // [n_q] sampled query positions
-  int n_q;
+  int n_q;                 // sampled queries: token q_base + (i / q_cols) * q_row_stride
+  int q_cols;              //   + (i % q_cols) * q_col_stride for i < n_q
+  int q_base;
+  int q_row_stride;
+  int q_col_stride;
   int n_tokens;
   int n_heads;
   int n_layers;
   int budget;
   int frame_id;
   int mode;
-  int stage_queries;       // stage the sampled query rows in LDS
+  int stage_queries;       // saliency: stage the sampled query rows in LDS
+  int sal_groups;          // saliency: workgroups per (layer, head)
 };
 
 hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t s);
 // Records the hardware XCC id of each of n_blocks workgroups into ids (device memory).
 hipError_t launch_xcc_probe(int* ids, int n_blocks, hipStream_t s);
-// Dynamic LDS bytes the admission kernel needs for these arguments, and the most it may
-// use on a device whose per-workgroup LDS limit is max_lds (room is left for the
-// kernel's static LDS).
+// Dynamic LDS bytes the admission kernels need for these arguments (the larger of the
+// saliency and selection launches), and the most they may use on a device whose
+// per-workgroup LDS limit is max_lds (room is left for the kernels' static LDS).
 constexpr int kAdmitStaticLdsMargin = 4096;
 size_t admit_lds_bytes(const AdmitArgs& a);
 int admit_max_dynamic_lds(int max_lds);
 // max_lds: the device's LDS limit per workgroup (bytes), for the kernel attribute.
 hipError_t launch_admit(const AdmitArgs& a, int max_lds, hipStream_t s);
+// Saliency launch shape for n_lh (layer, head) pairs on a device with n_cus CUs: sets
+// a->sal_groups and a->stage_queries (rows staged when they fit max_lds).
+void plan_saliency(AdmitArgs* a, int n_lh, int n_cus, int max_lds);
 
 }  // namespace rv

@@ -124,20 +124,27 @@ def test_saliency_is_bit_reproducible(rv):
         assert (x == y).all()
 
 
-SELECT_CASES = [  # (N, H, budget)
-    (1, 1, 0), (1, 1, 1), (64, 2, 1), (100, 3, 7), (1041, 16, 10), (1041, 4, 1040),
-    (1041, 2, 1041), (5000, 2, 50), (16384, 1, 163),
+SELECT_CASES = [  # (N, H, budget, values): "ties" = nine levels, "spread" = continuous
+    (1, 1, 0, "ties"), (1, 1, 1, "ties"), (64, 2, 1, "ties"), (100, 3, 7, "ties"),
+    (1041, 16, 10, "ties"), (1041, 16, 10, "spread"), (1041, 4, 1040, "ties"),
+    (1041, 2, 1041, "ties"), (1374, 4, 13, "spread"), (300, 2, 33, "ties"),
+    (2048, 2, 32, "ties"), (2048, 2, 32, "spread"), (2049, 2, 32, "ties"), (3000, 1, 20, "spread"),
+    (5000, 2, 50, "ties"), (16384, 1, 163, "ties"),
 ]
 
 
-@pytest.mark.parametrize("N,H,budget", SELECT_CASES)
-def test_admit_matches_oracle_topk_on_given_saliency(rv, N, H, budget):
-    """rv_admit on a given saliency full of exact ties: the index set, its order, the
-    appended rows and their provenance must equal the oracle's exactly."""
+@pytest.mark.parametrize("N,H,budget,values", SELECT_CASES)
+def test_admit_matches_oracle_topk_on_given_saliency(rv, N, H, budget, values):
+    """rv_admit on a given saliency (full of exact ties, or continuous): the index set,
+    its order, the appended rows and their provenance must equal the oracle's exactly
+    (both wave-level and radix selection paths, on both sides of their boundary)."""
     import torch
-    print(f"admit N={N} H={H} budget={budget}", flush=True)
+    print(f"admit N={N} H={H} budget={budget} {values}", flush=True)
     rng = np.random.default_rng(N + budget)
-    sal = (rng.integers(0, 9, size=(H, N)).astype(np.float32) / 9.0)
+    if values == "ties":
+        sal = (rng.integers(0, 9, size=(H, N)).astype(np.float32) / 9.0)
+    else:
+        sal = rng.random(size=(H, N)).astype(np.float32) * np.float32(0.05)
     K, V, _ = frame(11, N, H)
     mem = rv.Memory(H, reserve_tokens=3, max_tokens=budget + 10)
     pre = memory_rows(12, H, 3)
