@@ -161,29 +161,28 @@ def summarize_pmc(fetch_dir, write_dir, workload):
               f"{total / 1e6:.2f} MB per launch ({path})")
 
 
-def cpu_baseline(cfg, mean_ctx, n_frames):
-    """Time the oracle on one layer of the frame whose context is the stream mean."""
-    import numpy as np
+def cpu_baseline(cfg, mean_ctx, n_frames, budget, qs):
+    """Time the oracle on one layer of a frame whose context is the stream's mean."""
     import oracle
     from paper_2609_23286_amd import synth
-    N, H, k = cfg.n_tokens, cfg.n_heads, cfg.budget
-    t_mid = int(round((mean_ctx - N) / k))
-    M = t_mid * k
+    N, H = cfg.n_tokens, cfg.n_heads
+    M = max(0, int(round(mean_ctx - N)))
+    t_mid = M // max(budget, 1)
     Q, K, V = synth.frame_qkv(cfg, 0, t_mid)
-    memK, memV = synth.memory_prefill(cfg, 0, M, M + k)
-    qidx = oracle.qsub_index(cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
-    omem = oracle.Memory(H, cfg.head_dim, M + k)
+    memK, memV = synth.memory_prefill(cfg, 0, M, M + budget)
+    qidx = oracle.qsub_index(*qs)
+    omem = oracle.Memory(H, cfg.head_dim, M + budget)
     omem.K[:], omem.V[:] = memK, memV
     omem.len = M
     t0 = time.perf_counter()
-    oracle.step(omem, Q, K, V, qidx, k)
+    oracle.step(omem, Q, K, V, qidx, budget)
     dt = time.perf_counter() - t0
     per_frame = dt * cfg.n_layers * (mean_ctx / (M + N))
     return {"value": 1.0 / per_frame, "unit": "frames/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": (f"one layer (16 heads, all {N} queries, saliency, top-{k}, append) of frame "
-                       f"{t_mid} (context {M + N}), {dt:.2f} s, scaled x{cfg.n_layers} layers and "
-                       f"to the {n_frames}-frame mean context {mean_ctx:.0f}")}
+            "sample": (f"one layer ({H} heads, all {N} queries, saliency, top-{budget}, append) at "
+                       f"context {M + N}, {dt:.2f} s, scaled x{cfg.n_layers} layers and to the "
+                       f"{n_frames}-frame mean context {mean_ctx:.0f}")}
 
 
 def main():
@@ -192,6 +191,13 @@ def main():
     p.add_argument("--steps", type=int, default=1000, help="frames timed (from an empty memory)")
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--config", default="vitl_stack_1000")
+    p.add_argument("--policy", choices=("all", "paper"), default="all",
+                   help="all: every layer regulated, no anchor (the configuration's setting); paper: "
+                        "layers 11-17 regulated, first frame kept whole in every layer (Sec. 4.1)")
+    p.add_argument("--stride", type=int, default=None, help="query window s (default: the config's, 2)")
+    p.add_argument("--gamma", type=float, default=None, help="retention rate: budget = floor(gamma N)")
+    p.add_argument("--shared", action="store_true",
+                   help="head-averaged selection (one top-k per layer) instead of head-specific")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run a 256 MiB device copy before the stream (HBM counter calibration)")
@@ -211,9 +217,15 @@ def main():
 
     cfg = synth.CONFIGS[args.config]
     L, H, N, d, k = cfg.n_layers, cfg.n_heads, cfg.n_tokens, cfg.head_dim, cfg.budget
+    if args.gamma is not None:
+        k = int(args.gamma * N)
+    stride = args.stride or cfg.stride
     T, W = args.steps, args.warmup
-    qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
-    n_q = len(range(0, cfg.grid_h, cfg.stride)) * len(range(0, cfg.grid_w, cfg.stride))
+    qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, stride)
+    n_q = len(range(0, cfg.grid_h, stride)) * len(range(0, cfg.grid_w, stride))
+    anchor = args.policy == "paper"
+    regulated = [l for l in range(L) if args.policy == "all" or 10 <= l <= 16]
+    admit_fn = "rv_admit_layers_shared" if args.shared else "rv_admit_layers"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -242,8 +254,24 @@ def main():
     torch.cuda.synchronize()
     log(f"generated {T} frames in {time.perf_counter() - t0:.1f} s")
 
-    cap = T * k + 64
+    base = (N if anchor else 0) + cfg.prefill
+    cap = base + T * k + 64
     mems = [rv.Memory(H, reserve_tokens=cap, max_tokens=cap) for _ in range(L)]
+
+    def prefill():
+        """Memory contents before frame 0: the configuration's prefilled rows, if any."""
+        for m in mems:
+            m.reset()
+        if cfg.prefill:
+            for l, m in enumerate(mems):
+                pk = torch.empty((H, cfg.prefill, d), dtype=torch.int16, device=dev)
+                pv = torch.empty_like(pk)
+                rv.gpu_normal(cfg.seed, synth.PREFILL_FRAME, l, synth.TAG_MEMK, pk, cfg.sigma)
+                rv.gpu_normal(cfg.seed, synth.PREFILL_FRAME, l, synth.TAG_MEMV, pv, cfg.sigma)
+                m.write(pk, pv)
+            torch.cuda.synchronize()
+
+    prefill()
     rv.reserve_workspace(N, H, L)
     out = torch.empty((L, N, H, d), dtype=torch.int16, device=dev)
     lse = torch.empty((L, H, N), dtype=torch.float32, device=dev)
@@ -271,6 +299,13 @@ def main():
         vpp = [fb[l, 2].data_ptr() for l in range(L)]
         frame_ptrs.append((qp, kp, vpp, arr(*qp), arr(*kp), arr(*vpp)))
 
+    reg_arr = lambda ptrs: (vp * len(regulated))(*[ptrs[l] for l in regulated])
+    reg_sal = reg_arr([sal[l].data_ptr() for l in range(L)])
+    reg_lse = reg_arr([lse[l].data_ptr() for l in range(L)])
+    reg_mem = reg_arr([m.handle.value for m in mems])
+    reg_frames = [(reg_arr(f[0]), reg_arr(f[1]), reg_arr(f[2])) for f in frame_ptrs]
+    admit = getattr(lib, admit_fn)
+
     def run_frame(t, ev=None):
         qp, kp, vpp, qa, ka, va = frame_ptrs[t]
         if ev is not None:
@@ -284,7 +319,13 @@ def main():
                 raise rv.RVError(st, lib.rv_last_error().decode())
         if ev is not None:
             ev[1].record(stream)
-        st = lib.rv_admit_layers(L, qa, ka, va, lse_arr, N, qref, k, mem_arr, t, sal_arr, None, s_h)
+        if anchor and t == 0:  # the global anchor: the first frame whole, in every layer (Eq. 4)
+            st = admit(L, qa, ka, va, lse_arr, N, qref, N, mem_arr, t, sal_arr, None, s_h)
+        elif regulated and k > 0:
+            rq, rk, rvv = reg_frames[t]
+            st = admit(len(regulated), rq, rk, rvv, reg_lse, N, qref, k, reg_mem, t, reg_sal, None, s_h)
+        else:
+            st = 0
         if st:
             raise rv.RVError(st, lib.rv_last_error().decode())
         if ev is not None:
@@ -294,8 +335,7 @@ def main():
     for t in range(min(W, T)):
         run_frame(t)
     torch.cuda.synchronize()
-    for m in mems:
-        m.reset()
+    prefill()
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(T)]
     torch.cuda.synchronize()
@@ -307,25 +347,51 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     rv.device_status()
-    assert all(m.len == T * k for m in mems)
+
+    def mem_len(l, t):
+        """Rows of layer l's memory when frame t is attended."""
+        n = cfg.prefill
+        if anchor and t > 0:
+            n += N
+        if l in regulated:
+            n += max(0, t - (1 if anchor else 0)) * k
+        return n
+
+    assert all(m.len == mem_len(l, T) for l, m in enumerate(mems))
 
     for f in sorted({0, T // 2, T - 1}):
         log(f"frame {f}: attention {events[f][0].elapsed_time(events[f][1]) * 1e3 / L:.1f} us/launch "
-            f"(context {f * k + N}), admission {events[f][1].elapsed_time(events[f][2]) * 1e3:.1f} us")
+            f"(context {mem_len(regulated[0] if regulated else 0, f) + N}), "
+            f"admission {events[f][1].elapsed_time(events[f][2]) * 1e3:.1f} us")
     attn_ms = sum(e[0].elapsed_time(e[1]) for e in events)
     admit_ms = sum(e[1].elapsed_time(e[2]) for e in events)
-    ctx = [t * k + N for t in range(T)]
-    flops = sum(attention_flops(N, H, d, c) for c in ctx) * L
+    flops = sum(attention_flops(N, H, d, mem_len(l, t) + N) for t in range(T) for l in range(L))
     n_attn = T * L
     attn_avg_s = attn_ms / 1e3 / n_attn
     achieved_tf = flops / n_attn / attn_avg_s / 1e12
-    bytes_admit = admit_bytes(N, H, d, n_q, k) * L * T
+    bytes_admit = sum(admit_bytes(N, H, d, n_q, N) * L if (anchor and t == 0)
+                      else admit_bytes(N, H, d, n_q, k) * len(regulated) for t in range(T))
     admit_gbs = bytes_admit / (admit_ms / 1e3) / 1e9
     log(f"timed {T} frames in {elapsed:.3f} s: attention {attn_ms:.1f} ms "
         f"({attn_avg_s * 1e6:.1f} us/launch, {achieved_tf:.1f} TFLOP/s), admission {admit_ms:.1f} ms "
         f"({admit_ms / T * 1e3:.1f} us/frame, {admit_gbs:.0f} GB/s)")
 
-    mean_ctx = sum(ctx) / T
+    mean_ctx = sum(mem_len(l, t) + N for t in range(T) for l in range(L)) / (T * L)
+    variant = []
+    if args.policy == "paper":
+        variant.append("paper layer policy: layers 11-17 regulated, first frame kept whole in every layer")
+    if stride != cfg.stride:
+        variant.append(f"{stride}x{stride} query windows")
+    if args.gamma is not None:
+        variant.append(f"gamma {args.gamma}")
+    if args.shared:
+        variant.append("head-averaged selection")
+    workload = (f"{cfg.name}: {L} layers x {H} heads x {d}, {N} tokens/frame ({cfg.grid_h}x{cfg.grid_w} "
+                f"patches + {cfg.n_special} special), budget {k}/head/frame, {stride}x{stride} query sampling, "
+                f"{T}-frame stream from " + (f"{cfg.prefill} prefilled memory rows" if cfg.prefill else "empty memory")
+                + "".join("; " + v for v in variant))
+    # counter profiles are recorded for the configurations' own settings only
+    wkey = cfg.name if not variant else None
     result = {
         "metric": "frames/sec (attend+saliency+admit, 24 layers) at 1000-frame stream",
         "value": T / elapsed,
@@ -339,26 +405,26 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded Philox streams of ViT-L token shape, 1% planted salient keys)",
-        "config": {"workload": f"{cfg.name}: {L} layers x {H} heads x {d}, {N} tokens/frame "
-                               f"({cfg.grid_h}x{cfg.grid_w} patches + {cfg.n_special} special), "
-                               f"budget {k}/head/frame, 2x2 query sampling, {T}-frame stream from empty memory",
-                   "layers": L, "heads": H, "head_dim": d, "tokens_per_frame": N, "budget": k,
-                   "frames": T, "sampled_queries": n_q},
+        "config": {"workload": workload, "layers": L, "heads": H, "head_dim": d, "tokens_per_frame": N,
+                   "budget": k, "frames": T, "sampled_queries": n_q, "query_window": stride,
+                   "regulated_layers": len(regulated), "anchor": anchor,
+                   "selection": "head-averaged" if args.shared else "head-specific",
+                   "prefill_rows": cfg.prefill},
         "roofline": {"kernel": "attn_fwd_kernel", "bound": "mfma", "achieved": achieved_tf,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved_tf / PEAK_BF16_TFLOPS,
-                     "traffic": recorded_traffic("attn_fwd_kernel", cfg.name),
+                     "traffic": recorded_traffic("attn_fwd_kernel", wkey) if wkey else None,
                      "avg_launch_us": attn_avg_s * 1e6,
                      "algorithmic_flops_per_launch": flops / n_attn},
         "phases": {"attention_ms": attn_ms, "admission_ms": admit_ms,
                    "admission_roofline": {"kernel": "admit_kernel", "bound": "hbm", "achieved": admit_gbs,
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": admit_gbs / PEAK_HBM_GBS,
-                                          "traffic": recorded_traffic("admit_kernel", cfg.name),
+                                          "traffic": recorded_traffic("admit_kernel", wkey) if wkey else None,
                                           "algorithmic_bytes_per_launch": bytes_admit / T}},
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a host sample ...")
-        result["cpu_baseline"] = cpu_baseline(cfg, mean_ctx, T)
+        result["cpu_baseline"] = cpu_baseline(cfg, mean_ctx, T, k, qs)
     for m in mems:
         m.close()
     print(json.dumps(result), flush=True)

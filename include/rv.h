@@ -45,7 +45,8 @@ typedef enum rv_status {
     RV_ERR_INVALID = 1,  /* bad argument: null pointer, size, unsupported shape */
     RV_ERR_OOM = 2,      /* a device allocation failed; state unchanged */
     RV_ERR_CAPACITY = 3, /* memory growth would exceed the rv_mem's max_tokens */
-    RV_ERR_HIP = 4       /* the HIP runtime reported an error */
+    RV_ERR_HIP = 4,      /* the HIP runtime reported an error */
+    RV_ERR_IO = 5        /* a file could not be read or written, or is not a memory snapshot */
 } rv_status;
 
 /* One layer's regulated KV memory ("context memory" M_t of Sec. 3.3 Eq. 4-6): K and V
@@ -113,6 +114,20 @@ rv_status rv_mem_write(rv_mem m, const void *K, const void *V, int64_t n_rows, i
  * host or device memory.  Synchronous with respect to the host. */
 rv_status rv_mem_read(rv_mem m, void *K, void *V, int32_t *prov, void *stream);
 
+/* Snapshot of a memory (checkpoint / resume of a stream): writes the valid rows of every
+ * head, with their provenance, to `path` (little-endian: 8-byte magic "RVMEMv1\0",
+ * int32 n_heads, int32 head_dim, int64 length, then K [n_heads][length][64] bf16,
+ * V likewise, provenance [n_heads][length][2] int32).  Synchronises the memory's
+ * device.  RV_ERR_IO if the file cannot be written. */
+rv_status rv_mem_save(rv_mem m, const char *path);
+
+/* Restores a snapshot written by rv_mem_save into m: the head count must match, the
+ * length must not exceed m's max_tokens; m grows as needed.  The file is read and
+ * checked completely before m changes, so on any failure (RV_ERR_IO for an unreadable
+ * or malformed file, RV_ERR_INVALID for a mismatch, RV_ERR_CAPACITY, RV_ERR_OOM) m is
+ * left unchanged.  Synchronous with respect to the host. */
+rv_status rv_mem_load(rv_mem m, const char *path);
+
 /* ---- the per-frame hot path ---------------------------------------------------------- */
 
 /* Temporal-causal attention of one frame over memory + frame (Sec. 3.1 Eq. 3): for
@@ -160,6 +175,17 @@ rv_status rv_admit_layers(int n_layers, const void *const *Q, const void *const 
                           const void *const *V, const float *const *lse, int n_tokens,
                           const rv_qsub *qs, int budget, const rv_mem *mems, int frame_id,
                           float *const *saliency_out, int32_t *const *idx_out, void *stream);
+
+/* Head-averaged admission, the arm without head-specific retention in the ablation of
+ * Sec. 4.5 (Table 4): exactly as rv_admit_layers, except that each layer selects once,
+ * on the sum over heads of the saliency (summed in head order; it ranks tokens as the
+ * mean over heads does, ties to the lower index), and every head appends the same
+ * tokens.  idx_out[l], if given, receives that selection in every head's row. */
+rv_status rv_admit_layers_shared(int n_layers, const void *const *Q, const void *const *K,
+                                 const void *const *V, const float *const *lse, int n_tokens,
+                                 const rv_qsub *qs, int budget, const rv_mem *mems, int frame_id,
+                                 float *const *saliency_out, int32_t *const *idx_out,
+                                 void *stream);
 
 /* Synchronises the current device and reports, then clears, the status bits the
  * library's kernels raise: RV_OK, or RV_ERR_HIP with rv_last_error() naming the

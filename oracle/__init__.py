@@ -138,6 +138,14 @@ def topk(sal, budget):
     return idx
 
 
+def topk_head_average(sal, budget):
+    """One top-``budget`` per layer on the saliency averaged over heads (the arm without
+    head-specific retention in the ablation of Sec. 4.5, Table 4): the mean over the
+    head axis in fp64, then the same ranking as ``topk`` (ties to the lower index)."""
+    mean = np.asarray(sal, dtype=np.float64).mean(axis=0, keepdims=True)
+    return topk(mean, budget)[0]
+
+
 class Memory:
     """The oracle's own KV memory: ``[H, capacity, d]`` bf16 patterns + length."""
 

@@ -366,45 +366,62 @@ __device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx
   __syncthreads();
 }
 
+// Head-specific retention (the paper's rule, Sec. 3.3): one workgroup per (layer, head)
+// ranks that head's saliency.  Shared selection (the arm without head-specific
+// retention in the ablation of Sec. 4.5, Table 4): one workgroup per layer ranks the
+// sum over heads of the saliencies (summed in head order; it orders tokens as the mean
+// does) and every head admits the same tokens.
 __global__ __launch_bounds__(NT) void select_kernel(AdmitArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ uint64_t s_cand[NW * kWaveTopK];
   const int H = a.n_heads, N = a.n_tokens, k = a.budget, tid = threadIdx.x;
-  const int layer = blockIdx.x / H, h = blockIdx.x - layer * H;
+  const int per_layer = a.shared_select ? 1 : H;
+  const int layer = blockIdx.x / per_layer, h_own = blockIdx.x - layer * per_layer;
   const AdmitLayer& L = a.layer[layer];
   float* s_sal = reinterpret_cast<float*>(smem);
   int32_t* s_idx = reinterpret_cast<int32_t*>(smem + (((size_t)N * 4 + 15) & ~(size_t)15));
 
-  const float* gs = L.sal + (int64_t)h * N;
-  if ((N & 3) == 0) {
-    for (int j = tid; j < N / 4; j += NT)
-      reinterpret_cast<float4*>(s_sal)[j] = reinterpret_cast<const float4*>(gs)[j];
+  if (a.shared_select) {
+    for (int j = tid; j < N; j += NT) {
+      float acc = 0.f;
+      for (int h = 0; h < H; ++h) acc += L.sal[(int64_t)h * N + j];
+      s_sal[j] = acc;
+    }
   } else {
-    for (int j = tid; j < N; j += NT) s_sal[j] = gs[j];
+    const float* gs = L.sal + (int64_t)h_own * N;
+    if ((N & 3) == 0) {
+      for (int j = tid; j < N / 4; j += NT)
+        reinterpret_cast<float4*>(s_sal)[j] = reinterpret_cast<const float4*>(gs)[j];
+    } else {
+      for (int j = tid; j < N; j += NT) s_sal[j] = gs[j];
+    }
   }
   __syncthreads();
   if (k <= kWaveTopK && k < N && N <= NW * 64 * kLaneSlots)
     select_small(s_sal, N, k, s_idx, s_cand);
   else
     select_topk(s_sal, N, k, s_idx);
-  if (L.idx)
-    for (int r = tid; r < k; r += NT) L.idx[(int64_t)h * k + r] = s_idx[r];
-  // 16-byte chunks: 8 per K row, 8 per V row.
-  for (int c = tid; c < k * 16; c += NT) {
-    const int r = c >> 4, part = c & 15, chunk = part & 7;
-    const int j = s_idx[r];
-    if (j < 0 || j >= N) continue;  // unreachable: the selection emits exactly k indices < N
-    const int64_t src = ((int64_t)j * H + h) * D + chunk * 8;
-    const int64_t dst = ((int64_t)h * L.head_stride + L.mem_len + r) * D + chunk * 8;
-    if (part < 8)
-      *reinterpret_cast<uint4*>(L.memK + dst) = *reinterpret_cast<const uint4*>(L.K + src);
-    else
-      *reinterpret_cast<uint4*>(L.memV + dst) = *reinterpret_cast<const uint4*>(L.V + src);
-  }
-  for (int r = tid; r < k; r += NT) {
-    int32_t* pv = L.prov + ((int64_t)h * L.head_stride + L.mem_len + r) * 2;
-    pv[0] = a.frame_id;
-    pv[1] = s_idx[r];
+  const int h0 = a.shared_select ? 0 : h_own, h1 = a.shared_select ? H : h_own + 1;
+  for (int h = h0; h < h1; ++h) {
+    if (L.idx)
+      for (int r = tid; r < k; r += NT) L.idx[(int64_t)h * k + r] = s_idx[r];
+    // 16-byte chunks: 8 per K row, 8 per V row.
+    for (int c = tid; c < k * 16; c += NT) {
+      const int r = c >> 4, part = c & 15, chunk = part & 7;
+      const int j = s_idx[r];
+      if (j < 0 || j >= N) continue;  // unreachable: the selection emits exactly k indices < N
+      const int64_t src = ((int64_t)j * H + h) * D + chunk * 8;
+      const int64_t dst = ((int64_t)h * L.head_stride + L.mem_len + r) * D + chunk * 8;
+      if (part < 8)
+        *reinterpret_cast<uint4*>(L.memK + dst) = *reinterpret_cast<const uint4*>(L.K + src);
+      else
+        *reinterpret_cast<uint4*>(L.memV + dst) = *reinterpret_cast<const uint4*>(L.V + src);
+    }
+    for (int r = tid; r < k; r += NT) {
+      int32_t* pv = L.prov + ((int64_t)h * L.head_stride + L.mem_len + r) * 2;
+      pv[0] = a.frame_id;
+      pv[1] = s_idx[r];
+    }
   }
 }
 
@@ -460,7 +477,8 @@ hipError_t launch_admit(const AdmitArgs& a, int max_lds, hipStream_t s) {
   if ((a.mode & kModeSelect) && a.budget > 0) {
     hipError_t e = set_lds_limit((const void*)select_kernel, &sel_attr, limit);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(select_kernel, dim3((unsigned)(a.n_layers * a.n_heads)), dim3(NT), select_lds_bytes(a), s, a);
+    const unsigned grid = (unsigned)(a.n_layers * (a.shared_select ? 1 : a.n_heads));
+    hipLaunchKernelGGL(select_kernel, dim3(grid), dim3(NT), select_lds_bytes(a), s, a);
     return hipGetLastError();
   }
   return hipSuccess;

@@ -454,6 +454,77 @@ rv_status rv_mem_read(rv_mem m, void* K, void* V, int32_t* prov, void* stream) {
   return RV_OK;
 }
 
+namespace {
+constexpr char kSnapMagic[8] = {'R', 'V', 'M', 'E', 'M', 'v', '1', '\0'};
+
+struct FileCloser {
+  FILE* f;
+  ~FileCloser() {
+    if (f) fclose(f);
+  }
+};
+}  // namespace
+
+rv_status rv_mem_save(rv_mem m, const char* path) {
+  if (!m || !path) return fail(RV_ERR_INVALID, "NULL argument");
+  rv_status st = check_device(m);
+  if (st != RV_OK) return st;
+  const size_t n = (size_t)m->n_heads * (size_t)m->len;
+  std::vector<uint16_t> K(n * rv::kHeadDim), V(n * rv::kHeadDim);
+  std::vector<int32_t> prov(n * 2);
+  st = rv_mem_read(m, K.data(), V.data(), prov.data(), nullptr);
+  if (st != RV_OK) return st;
+  FileCloser fc{fopen(path, "wb")};
+  if (!fc.f) return fail(RV_ERR_IO, "cannot open %s for writing", path);
+  const int32_t hdr[2] = {m->n_heads, rv::kHeadDim};
+  const int64_t len = m->len;
+  bool ok = fwrite(kSnapMagic, 1, 8, fc.f) == 8 && fwrite(hdr, 4, 2, fc.f) == 2 && fwrite(&len, 8, 1, fc.f) == 1;
+  ok = ok && fwrite(K.data(), 2, K.size(), fc.f) == K.size() && fwrite(V.data(), 2, V.size(), fc.f) == V.size() &&
+       fwrite(prov.data(), 4, prov.size(), fc.f) == prov.size();
+  if (!ok || fflush(fc.f) != 0) return fail(RV_ERR_IO, "cannot write %s", path);
+  return RV_OK;
+}
+
+rv_status rv_mem_load(rv_mem m, const char* path) {
+  if (!m || !path) return fail(RV_ERR_INVALID, "NULL argument");
+  rv_status st = check_device(m);
+  if (st != RV_OK) return st;
+  FileCloser fc{fopen(path, "rb")};
+  if (!fc.f) return fail(RV_ERR_IO, "cannot open %s", path);
+  char magic[8];
+  int32_t hdr[2];
+  int64_t len = -1;
+  if (fread(magic, 1, 8, fc.f) != 8 || memcmp(magic, kSnapMagic, 8) != 0 || fread(hdr, 4, 2, fc.f) != 2 ||
+      fread(&len, 8, 1, fc.f) != 1 || len < 0)
+    return fail(RV_ERR_IO, "%s is not a memory snapshot", path);
+  if (hdr[0] != m->n_heads || hdr[1] != rv::kHeadDim)
+    return fail(RV_ERR_INVALID, "snapshot has %d heads of %d, memory has %d of %d", hdr[0], hdr[1], m->n_heads,
+                rv::kHeadDim);
+  if (len > m->max_tokens) return fail(RV_ERR_CAPACITY, "snapshot of %lld rows exceeds max_tokens", (long long)len);
+  const size_t n = (size_t)m->n_heads * (size_t)len;
+  std::vector<uint16_t> K(n * rv::kHeadDim), V(n * rv::kHeadDim);
+  std::vector<int32_t> prov(n * 2);
+  if (fread(K.data(), 2, K.size(), fc.f) != K.size() || fread(V.data(), 2, V.size(), fc.f) != V.size() ||
+      fread(prov.data(), 4, prov.size(), fc.f) != prov.size() || fgetc(fc.f) != EOF)
+    return fail(RV_ERR_IO, "%s is truncated or has trailing bytes", path);
+  const int64_t keep = m->len;
+  m->len = 0;  // every row is overwritten: nothing to carry over on growth
+  st = arena_reserve(m, len, nullptr);
+  m->len = keep;
+  if (st != RV_OK) return st;
+  if (len > 0) {
+    const size_t row = rv::kHeadDim * 2;
+    hipError_t e = hipMemcpy2D(m->K, m->cap * row, K.data(), len * row, len * row, m->n_heads, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy2D(m->V, m->cap * row, V.data(), len * row, len * row, m->n_heads, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy2D(m->prov, m->cap * 8, prov.data(), len * 8, len * 8, m->n_heads, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "rv_mem_load copy");
+  }
+  m->len = len;
+  return RV_OK;
+}
+
 rv_status rv_reserve_workspace(int n_tokens, int n_heads, int n_layers) {
   if (n_tokens < 1 || n_tokens > rv::kMaxTokens || n_heads < 1 || n_layers < 1)
     return fail(RV_ERR_INVALID, "bad workspace sizes");
@@ -604,10 +675,14 @@ rv_status rv_admit(const float* saliency, int budget, const void* K, const void*
   return RV_OK;
 }
 
-rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const* K, const void* const* V,
-                          const float* const* lse, int n_tokens, const rv_qsub* qs, int budget,
-                          const rv_mem* mems, int frame_id, float* const* saliency_out,
-                          int32_t* const* idx_out, void* stream) {
+}  // extern "C"
+
+namespace {
+
+rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K, const void* const* V,
+                       const float* const* lse, int n_tokens, const rv_qsub* qs, int budget, const rv_mem* mems,
+                       int frame_id, float* const* saliency_out, int32_t* const* idx_out, void* stream,
+                       bool shared) {
   if (n_layers < 1 || n_layers > 4096) return fail(RV_ERR_INVALID, "n_layers must be in [1, 4096]");
   if (!Q || !K || !V || !lse || !mems) return fail(RV_ERR_INVALID, "NULL pointer array");
   if (n_tokens < 1 || n_tokens > rv::kMaxTokens)
@@ -637,6 +712,7 @@ rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const*
   probe.budget = budget;
   probe.mode = rv::kModeBoth;
   probe.n_heads = H;
+  probe.shared_select = shared ? 1 : 0;
   rv::plan_saliency(&probe, std::min(n_layers, rv::kMaxLayersPerLaunch) * H, ws->n_cus, ws->max_lds);
   const size_t lds_cap = (size_t)rv::admit_max_dynamic_lds(ws->max_lds);
   if (rv::admit_lds_bytes(probe) > lds_cap)
@@ -679,6 +755,26 @@ rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const*
   }
   for (int l = 0; l < n_layers; ++l) mems[l]->len += budget;
   return RV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const* K, const void* const* V,
+                          const float* const* lse, int n_tokens, const rv_qsub* qs, int budget,
+                          const rv_mem* mems, int frame_id, float* const* saliency_out,
+                          int32_t* const* idx_out, void* stream) {
+  return admit_layers(n_layers, Q, K, V, lse, n_tokens, qs, budget, mems, frame_id, saliency_out, idx_out,
+                      stream, false);
+}
+
+rv_status rv_admit_layers_shared(int n_layers, const void* const* Q, const void* const* K, const void* const* V,
+                                 const float* const* lse, int n_tokens, const rv_qsub* qs, int budget,
+                                 const rv_mem* mems, int frame_id, float* const* saliency_out,
+                                 int32_t* const* idx_out, void* stream) {
+  return admit_layers(n_layers, Q, K, V, lse, n_tokens, qs, budget, mems, frame_id, saliency_out, idx_out,
+                      stream, true);
 }
 
 }  // extern "C"

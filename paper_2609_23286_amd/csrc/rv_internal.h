@@ -89,6 +89,7 @@ struct AdmitArgs {
   int mode;
   int stage_queries;       // saliency: stage the sampled query rows in LDS
   int sal_groups;          // saliency: workgroups per (layer, head)
+  int shared_select;       // selection: one top-k per layer on the head sum, shared by all heads
 };
 
 hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t s);

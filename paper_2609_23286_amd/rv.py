@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librv.so")
 SYNTH_LIB_PATH = os.path.join(_HERE, "librv_synth.so")
 
-RV_OK, RV_ERR_INVALID, RV_ERR_OOM, RV_ERR_CAPACITY, RV_ERR_HIP = range(5)
+RV_OK, RV_ERR_INVALID, RV_ERR_OOM, RV_ERR_CAPACITY, RV_ERR_HIP, RV_ERR_IO = range(6)
 HEAD_DIM = 64
 
 
@@ -50,9 +50,13 @@ def _load():
         "rv_mem_reset": ([vp], i32),
         "rv_mem_write": ([vp, vp, vp, i64, i32, vp], i32),
         "rv_mem_read": ([vp, vp, vp, vp, vp], i32),
+        "rv_mem_save": ([vp, ctypes.c_char_p], i32),
+        "rv_mem_load": ([vp, ctypes.c_char_p], i32),
         "rv_attend_frame": ([vp, vp, vp, i32, vp, vp, i64, i64, i32, i32, P(rv_qsub), vp, vp, vp, vp], i32),
         "rv_admit": ([vp, i32, vp, vp, i32, vp, i32, vp, vp], i32),
         "rv_admit_layers": ([i32, P(vp), P(vp), P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp), vp], i32),
+        "rv_admit_layers_shared": ([i32, P(vp), P(vp), P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp),
+                                    vp], i32),
         "rv_reserve_workspace": ([i32, i32, i32], i32),
         "rv_device_status": ([], i32),
     }
@@ -175,6 +179,14 @@ class Memory:
                                 ctypes.c_void_p(prov.data_ptr()), _stream(stream)))
         return K, V, prov
 
+    def save(self, path):
+        """Write a snapshot (rows and provenance) to `path`."""
+        _check(_lib.rv_mem_save(self.handle, os.fsencode(path)))
+
+    def load(self, path):
+        """Replace the contents with a snapshot written by save()."""
+        _check(_lib.rv_mem_load(self.handle, os.fsencode(path)))
+
 
 def _host_or_dev_ptr(t):
     if not isinstance(t, torch.Tensor) or not t.is_contiguous() or t.element_size() != 2:
@@ -215,8 +227,10 @@ def admit(saliency, budget, K, V, mem, frame_id, idx_out=None, stream=None):
 
 
 def admit_layers(Q, K, V, lse, qs, budget, mems, frame_id, saliency_out=None, idx_out=None,
-                 stream=None):
-    """rv_admit_layers over lists of per-layer tensors and Memory objects."""
+                 stream=None, shared=False):
+    """rv_admit_layers (shared=False: head-specific retention) or rv_admit_layers_shared
+    (shared=True: one selection per layer on the head-summed saliency) over lists of
+    per-layer tensors and Memory objects."""
     L = len(mems)
     N, H, d = K[0].shape
     shp = (N, H, d)
@@ -228,7 +242,8 @@ def admit_layers(Q, K, V, lse, qs, budget, mems, frame_id, saliency_out=None, id
     q = qs if isinstance(qs, rv_qsub) else rv_qsub(*qs)
     sal = pack(saliency_out, (H, N), 4, "saliency_out") if saliency_out is not None else None
     idx = pack(idx_out, (H, budget), 4, "idx_out") if idx_out is not None else None
-    _check(_lib.rv_admit_layers(
+    fn = _lib.rv_admit_layers_shared if shared else _lib.rv_admit_layers
+    _check(fn(
         L, pack(Q, shp, 2, "Q"), pack(K, shp, 2, "K"), pack(V, shp, 2, "V"), pack(lse, (H, N), 4, "lse"),
         N, ctypes.byref(q), budget, arr(*[m.handle for m in mems]), frame_id, sal, idx, _stream(stream)))
 

@@ -73,6 +73,8 @@ def test_invalid_arguments_are_rejected_before_any_device_work():
     assert L.rv_admit(vp(1), 3, vp(1), vp(1), 10, None, 0, None, None) == rv.RV_ERR_INVALID
     assert L.rv_admit_layers(0, None, None, None, None, 10, None, 1, None, 0, None, None,
                              None) == rv.RV_ERR_INVALID
+    assert L.rv_mem_save(None, b"/tmp/x") == rv.RV_ERR_INVALID
+    assert L.rv_mem_load(None, b"/tmp/x") == rv.RV_ERR_INVALID
     # n_tokens == 0 is a no-op that succeeds without touching the device
     assert L.rv_attend_frame(None, None, None, 0, None, None, 0, 0, 16, 64, None, None, None,
                              None, None) == rv.RV_OK

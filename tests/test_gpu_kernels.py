@@ -8,8 +8,8 @@ import pytest
 
 import oracle
 from paper_2609_23286_amd import synth
-from util import (LSE_ATOL, OUT_ATOL, SAL_RTOL, bf16_to_f64, out_error_bound, to_dev,
-                  to_host_u16)
+from util import (LSE_ATOL, OUT_ATOL, SAL_RTOL, bf16_to_f64, check_index_sets, out_error_bound,
+                  to_dev, to_host_u16)
 
 pytestmark = pytest.mark.gpu
 
@@ -248,3 +248,116 @@ def test_gpu_generator_matches_cpu_generator(rv):
         Q, K, V = synth.frame_qkv(cfg, 0, frame_id)
         assert (got[0, 0] == Q).all() and (got[0, 2] == V).all()
         assert (got[0, 1] == K).all()
+
+
+def test_memory_snapshot_round_trip(rv, tmp_path):
+    """rv_mem_save / rv_mem_load: rows and provenance survive a round trip into a fresh
+    memory (which grows to fit); a mismatched head count, an oversized snapshot, a
+    truncated file and a foreign file are refused and leave the target unchanged."""
+    import torch
+    H, N, k = 3, 200, 7
+    mem = rv.Memory(H, reserve_tokens=4, max_tokens=100)
+    for t in range(5):
+        K, V, _ = frame(40 + t, N, H)
+        sal = torch.rand((H, N), device="cuda")
+        rv.admit(sal, k, to_dev(K), to_dev(V), mem, t)
+    rv.device_status()
+    path = tmp_path / "mem.rvm"
+    mem.save(path)
+    ref = [x.numpy().copy() for x in mem.read()]
+    fresh = rv.Memory(H, reserve_tokens=0, max_tokens=100)
+    fresh.load(path)
+    assert fresh.len == mem.len == 5 * k
+    for a, b in zip(ref, fresh.read()):
+        assert (a == b.numpy()).all()
+    small = rv.Memory(H, reserve_tokens=0, max_tokens=10)
+    other = rv.Memory(H + 1, reserve_tokens=0, max_tokens=100)
+    with pytest.raises(rv.RVError) as e:
+        small.load(path)
+    assert e.value.status == rv.RV_ERR_CAPACITY and small.len == 0
+    with pytest.raises(rv.RVError) as e:
+        other.load(path)
+    assert e.value.status == rv.RV_ERR_INVALID and other.len == 0
+    data = path.read_bytes()
+    (tmp_path / "cut.rvm").write_bytes(data[:-5])
+    (tmp_path / "foreign.rvm").write_bytes(b"not a snapshot at all")
+    for bad in ("cut.rvm", "foreign.rvm", "missing.rvm"):
+        with pytest.raises(rv.RVError) as e:
+            fresh.load(tmp_path / bad)
+        assert e.value.status == rv.RV_ERR_IO
+    assert fresh.len == 5 * k
+    for a, b in zip(ref, fresh.read()):
+        assert (a == b.numpy()).all()
+    for m in (mem, fresh, small, other):
+        m.close()
+
+
+def test_head_averaged_admission(rv):
+    """rv_admit_layers_shared: one selection per layer on the head-summed saliency, the
+    same tokens appended to every head.  The saliency itself is the head-specific one;
+    the selection must equal a CPU re-selection of the GPU's head sum (fp32, head order)
+    exactly, and the oracle's head-mean selection under the band rule."""
+    import torch
+    L, N, H, M, budget = 2, 1041, 16, 300, 10
+    qs = (28, 37, 5, 2)
+    qidx = oracle.qsub_index(*qs)
+    layers = []
+    for l in range(L):
+        Q, K, V = frame(70 + l, N, H)
+        memK, memV = memory_rows(80 + l, H, M)
+        mem = rv.Memory(H, reserve_tokens=M, max_tokens=M + budget)
+        mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+        Qd, Kd, Vd = to_dev(Q), to_dev(K), to_dev(V)
+        out = torch.empty_like(Qd)
+        lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
+        rv.attend_frame(Qd, Kd, Vd, mem, out, lse)
+        layers.append((Q, K, V, memK, memV, mem, Qd, Kd, Vd, lse))
+    sals = [torch.empty((H, N), dtype=torch.float32, device="cuda") for _ in range(L)]
+    idxs = [torch.empty((H, budget), dtype=torch.int32, device="cuda") for _ in range(L)]
+    rv.admit_layers([x[6] for x in layers], [x[7] for x in layers], [x[8] for x in layers],
+                    [x[9] for x in layers], qs, budget, [x[5] for x in layers], 3, sals, idxs, shared=True)
+    rv.device_status()
+    for l, (Q, K, V, memK, memV, mem, *_rest) in enumerate(layers):
+        idx = idxs[l].cpu().numpy()
+        assert (idx == idx[0]).all()                      # one selection for every head
+        sal = sals[l].cpu().numpy()
+        head_sum = np.zeros(N, dtype=np.float32)
+        for h in range(H):
+            head_sum += sal[h]
+        assert (idx[0] == oracle.topk(head_sum[None].astype(np.float64), budget)[0]).all()
+        _, lse_o = oracle.attend(Q, K, V, memK, memV, M)
+        sal_o = oracle.saliency(Q, K, lse_o, qidx)
+        assert (np.abs(sal - sal_o) <= SAL_RTOL * sal_o).all()
+        check_index_sets(idx[:1], sal_o.mean(axis=0, keepdims=True), budget)
+        mk, mv, prov = (x.numpy() for x in mem.read())
+        for h in range(H):
+            assert (mk[h, M:].view(np.uint16) == K[idx[0], h]).all()
+            assert (mv[h, M:].view(np.uint16) == V[idx[0], h]).all()
+            assert (prov[h, M:, 0] == 3).all() and (prov[h, M:, 1] == idx[0]).all()
+        mem.close()
+
+
+@pytest.mark.parametrize("stride", [1, 3, 4])
+def test_query_downsampling_factors(rv, stride):
+    """Saliency with s x s query windows (Table 6's factors 1, 3, 4 beside the default 2):
+    the sampled subset follows the same top-left rule, and saliency and selection match
+    the oracle."""
+    import torch
+    N, H, M, budget = 1041, 16, 700, 10
+    qs = (28, 37, 5, stride)
+    qidx = oracle.qsub_index(*qs)
+    print(f"stride {stride}: {len(qidx)} sampled queries", flush=True)
+    Q, K, V = frame(90 + stride, N, H)
+    memK, memV = memory_rows(95 + stride, H, M)
+    out, lse, sal = run_attend(rv, Q, K, V, memK, memV, qs)
+    _, lse_o = oracle.attend(Q, K, V, memK, memV, M)
+    sal_o = oracle.saliency(Q, K, lse_o, qidx)
+    assert (np.abs(sal - sal_o) <= SAL_RTOL * sal_o).all()
+    mem = rv.Memory(H, reserve_tokens=budget, max_tokens=budget)
+    idx = torch.empty((H, budget), dtype=torch.int32, device="cuda")
+    rv.admit(to_dev(sal.astype(np.float32)), budget, to_dev(K), to_dev(V), mem, 0, idx)
+    rv.device_status()
+    idx = idx.cpu().numpy()
+    assert (idx == oracle.topk(sal, budget)).all()
+    check_index_sets(idx, sal_o, budget)
+    mem.close()

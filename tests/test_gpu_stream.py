@@ -144,3 +144,45 @@ def test_full_size_frame_sampled_rows(rv, name, layer, M):
     for h in range(H):
         assert (mk[h, M:] == K[idx[h], h]).all() and (mv[h, M:] == V[idx[h], h]).all()
     mem.close()
+
+
+def test_layer_policy_stream(rv):
+    """The paper's layer partition (Sec. 3.3 Eq. 4-5, Sec. 4.1): the first frame is kept
+    whole in every layer (global anchor); afterwards only the regulated layers admit
+    tokens, the others attend over the anchor and the current frame alone.  Three layers
+    of the tiny stream, the middle one regulated, eight frames, against the oracle."""
+    import torch
+    cfg = synth.CONFIGS["tiny"]
+    H, N, k, L, T = cfg.n_heads, cfg.n_tokens, cfg.budget, 3, 8
+    regulated = {1}
+    qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
+    qidx = oracle.qsub_index(*qs)
+    cap = N + T * k
+    mems = [rv.Memory(H, reserve_tokens=cap, max_tokens=cap) for _ in range(L)]
+    omems = [oracle.Memory(H, cfg.head_dim, cap) for _ in range(L)]
+    for t in range(T):
+        for l in range(L):
+            Q, K, V = synth.frame_qkv(cfg, l, t)
+            admit = t == 0 or l in regulated
+            budget = N if t == 0 else k
+            if admit:
+                out, lse, sal, idx = gpu_frame_step(rv, mems[l], Q, K, V, qs, budget, t)
+                ref = oracle.step(omems[l], Q, K, V, qidx, budget)
+                assert (np.abs(sal - ref["sal"]) <= SAL_RTOL * ref["sal"]).all()
+                check_index_sets(idx, ref["sal"], budget)
+            else:
+                Qd, Kd, Vd = to_dev(Q), to_dev(K), to_dev(V)
+                outd = torch.empty_like(Qd)
+                lsed = torch.empty((H, N), dtype=torch.float32, device="cuda")
+                rv.attend_frame(Qd, Kd, Vd, mems[l], outd, lsed)
+                rv.device_status()
+                out = bf16_to_f64(to_host_u16(outd))
+                lse = lsed.cpu().numpy().astype(np.float64)
+                om = omems[l]
+                ro, rl = oracle.attend(Q, K, V, om.K, om.V, om.len)
+                ref = {"out": ro, "lse": rl}
+            assert np.abs(out - ref["out"]).max() <= OUT_ATOL
+            assert np.abs(lse - ref["lse"]).max() <= LSE_ATOL
+    for l in range(L):
+        assert mems[l].len == omems[l].len == (N + (T - 1) * k if l in regulated else N)
+        mems[l].close()

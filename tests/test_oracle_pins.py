@@ -279,3 +279,14 @@ def test_planted_keys_are_admitted():
     pos = synth.plant_positions(cfg.seed, 0, 0, cfg.n_heads, cfg.n_tokens, cfg.n_plant)
     hits = sum(len(set(idx[h]) & set(pos[h])) for h in range(cfg.n_heads))
     assert hits >= 0.95 * cfg.n_heads * cfg.n_plant
+
+
+def test_head_average_topk_matches_python_sort():
+    """The head-averaged selection is the stable sort of the head mean, by brute force."""
+    rng = np.random.default_rng(21)
+    H, n, k = 5, 60, 7
+    sal = rng.integers(0, 6, size=(H, n)).astype(np.float64) / 7.0
+    got = oracle.topk_head_average(sal, k)
+    mean = [sum(sal[h, j] for h in range(H)) / H for j in range(n)]
+    want = sorted(sorted(range(n), key=lambda j: (-mean[j], j))[:k])
+    assert list(got) == want
