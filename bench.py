@@ -36,7 +36,9 @@ CSRC = os.path.join(ROOT, "paper_2609_23286_amd", "csrc")
 # Kernel -> the sources whose text decides its memory traffic; counters recorded for
 # other sources are stale and are not reported.
 KERNEL_SOURCES = {"attn_fwd_kernel": ("attend.hip", "rv_internal.h", "rv_host.cpp"),
-                  "admit_kernel": ("admit.hip", "rv_internal.h", "rv_host.cpp")}
+                  "sal_kernel": ("admit.hip", "rv_internal.h", "rv_host.cpp"),
+                  "select_kernel": ("admit.hip", "rv_internal.h", "rv_host.cpp")}
+ADMISSION_KERNELS = ("sal_kernel", "select_kernel")  # one launch each per frame
 COPY_CALIBRATION_BYTES = 256 << 20   # read and written once by the calibration copy
 
 
@@ -90,6 +92,12 @@ def recorded_traffic(kernel, workload):
         return float(kv["hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def admission_traffic(workload):
+    """HBM bytes of one frame's admission (one saliency and one selection launch)."""
+    parts = [recorded_traffic(k, workload) for k in ADMISSION_KERNELS]
+    return None if any(p is None for p in parts) else sum(parts)
 
 
 def summarize_pmc(fetch_dir, write_dir, workload):
@@ -161,6 +169,49 @@ def summarize_pmc(fetch_dir, write_dir, workload):
               f"{total / 1e6:.2f} MB per launch ({path})")
 
 
+def summarize_trace(trace_dir, bench_json, workload):
+    """Write profiles/kernel_trace__<workload>.md from a rocprofv3 --kernel-trace --stats
+    run of this benchmark (its *_kernel_stats.csv) and the JSON line that run printed."""
+    import csv
+    stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not stats:
+        raise SystemExit(f"no kernel_stats.csv under {trace_dir}")
+    rows = list(csv.DictReader(open(stats[0])))
+    bench = json.loads(open(bench_json).read().strip().splitlines()[-1])
+
+    def short(name):
+        name = name.replace("rv::(anonymous namespace)::", "").replace("(anonymous namespace)::", "")
+        return name.split("(")[0]
+
+    avg = {short(r["Name"]): float(r["AverageNs"]) / 1e3 for r in rows}
+    lines = [f"# Kernel time summary: {workload} benchmark", "",
+             "Command (on the MI355X, from the repository root):", "", "```",
+             "cd /tmp && export TMPDIR=/tmp",
+             "rocprofv3 --kernel-trace --stats --output-format csv -d <out>/trace -o bench -- \\",
+             "    python /root/repo/bench.py --no-cpu-baseline > <out>/trace.json",
+             "python /root/repo/bench.py --trace-summary <out>/trace <out>/trace.json", "```", "",
+             "Kernel statistics (durations in ns; counts include the warm-up frames; the input",
+             "generator kernels run before the timed region):", "",
+             "| Kernel | Calls | Total ns | Average ns | % | Min ns | Max ns |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| `{short(r['Name'])}` | {r['Calls']} | {int(float(r['TotalDurationNs']))} | "
+                     f"{float(r['AverageNs']):.0f} | {float(r['Percentage']):.2f} | {r['MinNs']} | {r['MaxNs']} |")
+    adm = sum(avg.get(k, 0.0) for k in ADMISSION_KERNELS)
+    lines += ["", "The same run's benchmark line (HIP events on the compute stream):", "",
+              f"- frames/s: {bench['value']:.1f}",
+              f"- attention: {bench['roofline']['avg_launch_us']:.1f} us per launch (events) vs "
+              f"{avg.get('attn_fwd_kernel', 0.0):.1f} us (rocprofv3 average of attn_fwd_kernel)",
+              f"- admission: {bench['phases']['admission_ms'] / bench['steps'] * 1e3:.1f} us per frame (events; "
+              f"the pair also spans the launch gaps) vs {adm:.1f} us (rocprofv3 averages of "
+              + " + ".join(ADMISSION_KERNELS) + ")",
+              f"- attention roofline: {bench['roofline']['achieved']:.1f} TFLOP/s = "
+              f"{100 * bench['roofline']['frac']:.1f} % of {bench['roofline']['peak']}"]
+    path = os.path.join(PROFILES, f"kernel_trace__{workload}.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(f"wrote {path}")
+
+
 def cpu_baseline(cfg, mean_ctx, n_frames, budget, qs):
     """Time the oracle on one layer of a frame whose context is the stream's mean."""
     import oracle
@@ -203,7 +254,12 @@ def main():
                    help="run a 256 MiB device copy before the stream (HBM counter calibration)")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="summarise two rocprofv3 --pmc runs into profiles/ and exit")
+    p.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
+                   help="summarise a rocprofv3 --kernel-trace --stats run into profiles/ and exit")
     args = p.parse_args()
+    if args.trace_summary:
+        summarize_trace(*args.trace_summary, args.config)
+        return
     if args.pmc_summary:
         summarize_pmc(*args.pmc_summary, args.config)
         return
@@ -416,10 +472,11 @@ def main():
                      "avg_launch_us": attn_avg_s * 1e6,
                      "algorithmic_flops_per_launch": flops / n_attn},
         "phases": {"attention_ms": attn_ms, "admission_ms": admit_ms,
-                   "admission_roofline": {"kernel": "admit_kernel", "bound": "hbm", "achieved": admit_gbs,
+                   "admission_roofline": {"kernel": "sal_kernel + select_kernel", "bound": "hbm",
+                                          "achieved": admit_gbs,
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": admit_gbs / PEAK_HBM_GBS,
-                                          "traffic": recorded_traffic("admit_kernel", wkey) if wkey else None,
+                                          "traffic": admission_traffic(wkey) if wkey else None,
                                           "algorithmic_bytes_per_launch": bytes_admit / T}},
     }
     if not args.no_cpu_baseline:
