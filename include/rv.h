@@ -187,11 +187,9 @@ rv_status rv_admit_layers_shared(int n_layers, const void *const *Q, const void 
                                  float *const *saliency_out, int32_t *const *idx_out,
                                  void *stream);
 
-/* Synchronises the current device and reports, then clears, the status bits the
- * library's kernels raise: RV_OK, or RV_ERR_HIP with rv_last_error() naming the
- * condition (an attention workgroup found itself on another XCD than the round-robin
- * placement of workgroup ids the library verified at start-up, in which case that
- * launch's merged outputs may be wrong).  Test harnesses call it after each step. */
+/* Synchronises the current device and reports any error the HIP runtime recorded for
+ * earlier work (RV_ERR_HIP with the runtime's message).  Test harnesses call it after
+ * each step. */
 rv_status rv_device_status(void);
 
 /* Pre-allocates the current device's scratch workspace (split-KV partial results,

@@ -28,12 +28,11 @@
 //   U = T (the unit's tile count) this is stream-K: chunks may straddle units.  With
 //   U = k E >= T every unit is cut into k aligned pieces, so the workgroups holding the
 //   query tiles of one head walk the same key tiles at the same time and share them in
-//   L2.  The workgroup ids of a queue are the ones the hardware places on that XCD
-//   (ids are dealt round-robin over the XCDs; verified at start-up and by every
-//   workgroup).  All partial results of a unit are thus written and merged under one
-//   L2: a contributor waits for its stores to reach L2 and bumps the unit's counter;
-//   the last contributor merges the partials in chunk order (deterministic).  No
-//   device-wide cache flush is needed, and no workgroup waits on another.
+//   L2.  A chunk that covers a whole unit writes its output directly; otherwise it
+//   writes a partial result (unnormalised O, reference m, row sum l) to its slot and a
+//   second launch merges each split unit's partials in chunk order (deterministic; the
+//   kernel boundary is the only synchronisation, so results do not depend on where
+//   the hardware places the workgroups).
 #include "rv_internal.h"
 
 namespace rv {
@@ -255,12 +254,15 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
 }
 
 // Merge every partial of `unit` (contributor chunks c_first..c_last of queue q, in
-// chunk order) and write the final output rows and LSE.  Thread -> (row, 32 dims).
+// chunk order) and write the final output rows and LSE.  A partial is the chunk's
+// output normalised by its own row sum, in bf16, with its reference m and sum l; the
+// merge weights it by 2^(m - M) l (M the largest m).  Thread -> (row, 32 dims).
 // Partials are taken eight at a time: their (m, l) pairs in one round trip, then their
 // rows kMergeBatch partials at a time; loads are unconditional (indices clamped, surplus
 // weights zero) so that each batch is in flight together.
 constexpr int kMergeGroup = 8;
-constexpr int kMergeBatch = 1;   // partials whose rows are in flight together
+constexpr int kSlotStatsFloat = BQ * D / 2;  // slot: BQ x 64 bf16 rows, then m[BQ], l[BQ] (fp32)
+constexpr int kMergeBatch = 4;   // partials whose rows are in flight together
 
 // Partial slot of chunk c's segment of unit ui: slot 0 if the chunk starts inside the
 // unit, slot 1 if it began in an earlier unit.
@@ -272,21 +274,23 @@ __device__ __forceinline__ const float* slot_ptr(const AttnArgs& a, int q, int c
 template <int NB>
 __device__ __forceinline__ void merge_rows(const float* const* ps, const float* w, int row, int dh,
                                            float (&acc)[32]) {
-  float4 v[NB][8];
+  uint4 v[NB][4];  // 32 bf16 of the row's normalised partial output
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
-    const float4* po = reinterpret_cast<const float4*>(ps[j] + row * D + dh);
+    const uint4* po = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(ps[j]) + row * D + dh);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[j][e] = po[e];
+    for (int e = 0; e < 4; ++e) v[j][e] = po[e];
   }
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      acc[4 * e] = fmaf(w[j], v[j][e].x, acc[4 * e]);
-      acc[4 * e + 1] = fmaf(w[j], v[j][e].y, acc[4 * e + 1]);
-      acc[4 * e + 2] = fmaf(w[j], v[j][e].z, acc[4 * e + 2]);
-      acc[4 * e + 3] = fmaf(w[j], v[j][e].w, acc[4 * e + 3]);
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t wd[4] = {v[j][e].x, v[j][e].y, v[j][e].z, v[j][e].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[8 * e + 2 * i] = fmaf(w[j], __uint_as_float(wd[i] << 16), acc[8 * e + 2 * i]);
+        acc[8 * e + 2 * i + 1] = fmaf(w[j], __uint_as_float(wd[i] & 0xFFFF0000u), acc[8 * e + 2 * i + 1]);
+      }
     }
   }
 }
@@ -308,8 +312,8 @@ __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_fir
 #pragma unroll
     for (int j = 0; j < kMergeGroup; ++j) {
       ps[j] = slot_ptr(a, q, min(c0 + j, c_last), ui);
-      mv[j] = ps[j][BQ * D + row];
-      lv[j] = ps[j][BQ * D + BQ + row];
+      mv[j] = ps[j][kSlotStatsFloat + row];
+      lv[j] = ps[j][kSlotStatsFloat + BQ + row];
     }
     float m_new = mmax;
 #pragma unroll
@@ -319,11 +323,11 @@ __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_fir
 #pragma unroll
     for (int e = 0; e < 32; ++e) acc[e] *= scale;
     mmax = m_new;
-    float w[kMergeGroup];
+    float w[kMergeGroup];  // weight of each normalised partial: 2^(m - M) l
 #pragma unroll
     for (int j = 0; j < kMergeGroup; ++j) {
-      w[j] = j < n ? __builtin_amdgcn_exp2f(mv[j] - mmax) : 0.f;
-      L = fmaf(w[j], lv[j], L);
+      w[j] = j < n ? __builtin_amdgcn_exp2f(mv[j] - mmax) * lv[j] : 0.f;
+      L += w[j];
     }
 #pragma unroll
     for (int b = 0; b < kMergeGroup; b += kMergeBatch)
@@ -339,8 +343,7 @@ __device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_fir
 }
 
 // Key tiles t0..t1-1 of `unit` (queue-local index ui) as part of chunk c of queue q.
-__device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int ui, int t0, int t1, uint16_t* lds,
-                               int* s_flag) {
+__device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int ui, int t0, int t1, uint16_t* lds) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = uniform(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
@@ -415,59 +418,35 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
     return;
   }
 
-  // Partial result: publish, then the last contributor of the unit merges.
+  // Partial result: merged by the second launch.
   const int seg = (int64_t)c * a.E >= (int64_t)ui * a.U ? 0 : 1;
   float* ps = a.part + (int64_t)(2 * (a.chunk_base[q] + c) + seg) * kAttnSlotFloats;
   if (wave_active) {
+    // normalised partial output in bf16 (the merge weights it by 2^(m - M) l), m and l in fp32
     const int row = wave * 32 + l32;
-    float* po = ps + row * D + 4 * half;
+    const float inv = 1.f / l_tot;
+    uint16_t* po = reinterpret_cast<uint16_t*>(ps) + row * D + 4 * half;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      *reinterpret_cast<float4*>(po + 8 * j) =
-          make_float4(sm.o0[4 * j], sm.o0[4 * j + 1], sm.o0[4 * j + 2], sm.o0[4 * j + 3]);
-      *reinterpret_cast<float4*>(po + 32 + 8 * j) =
-          make_float4(sm.o1[4 * j], sm.o1[4 * j + 1], sm.o1[4 * j + 2], sm.o1[4 * j + 3]);
+      *reinterpret_cast<uint2*>(po + 8 * j) =
+          to_bf16x4(sm.o0[4 * j] * inv, sm.o0[4 * j + 1] * inv, sm.o0[4 * j + 2] * inv, sm.o0[4 * j + 3] * inv);
+      *reinterpret_cast<uint2*>(po + 32 + 8 * j) =
+          to_bf16x4(sm.o1[4 * j] * inv, sm.o1[4 * j + 1] * inv, sm.o1[4 * j + 2] * inv, sm.o1[4 * j + 3] * inv);
     }
     if (half == 0) {
-      ps[BQ * D + row] = sm.m;
-      ps[BQ * D + BQ + row] = l_tot;
+      ps[kSlotStatsFloat + row] = sm.m;
+      ps[kSlotStatsFloat + BQ + row] = l_tot;
     }
   }
-  if (a.safe) {
-    __threadfence();  // placement not verified: device-scope release
-  } else {
-    // release to the XCD's L2 (the vector L1 is write-through)
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
-  __syncthreads();
-  const int c_first = (int)(((int64_t)ui * a.U) / a.E);
-  const int c_last = (int)(((int64_t)ui * a.U + a.T - 1) / a.E);
-  if (tid == 0) *s_flag = atomicAdd(&a.unit_ctr[unit], 1) == c_last - c_first;
-  __syncthreads();
-  const bool last = *s_flag != 0;
-  __syncthreads();
-  if (!last) return;
-  if (a.safe)
-    __threadfence();  // device-scope acquire
-  else
-    asm volatile("buffer_inv sc0" ::: "memory");  // no stale vector-L1 lines
-  merge_unit(a, q, unit, ui, c_first, c_last);
-  if (tid == 0) a.unit_ctr[unit] = 0;  // ready for the next launch
 }
 
 __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[NSTAGE * STAGE];
-  __shared__ int s_val;
-  const int tid = threadIdx.x;
-
-  // Workgroup b serves queue b % n_queues, chunk b / n_queues.  The hardware deals
-  // workgroup ids round-robin over the XCDs (checked when the library starts), so all
-  // chunks of a queue share one L2; each workgroup verifies it against the XCC id it
-  // runs on and raises a status bit if not.
+  // Workgroup b serves queue b % n_queues, chunk b / n_queues.  Queues are per XCD (the
+  // hardware deals workgroup ids round-robin over the XCDs), which keeps the query
+  // tiles of a head under one L2; placement only affects speed, never results.
   const int q = (int)(blockIdx.x % (unsigned)a.n_queues);
   const int c = (int)(blockIdx.x / (unsigned)a.n_queues);
-  if (!a.safe && tid == 0 && a.xcc_queue[hw_xcc_id()] != q)
-    __hip_atomic_fetch_or(a.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   if (c >= a.n_chunks[q]) return;
   const int ub = a.unit_base[q];
   const int total = (a.unit_base[q + 1] - ub) * a.U;
@@ -481,9 +460,22 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
       continue;
     }
     const int seg_end = min(it_end, ui * a.U + a.T);
-    process_segment(a, q, c, ub + ui, ui, t0, t0 + (seg_end - it), lds, &s_val);
+    process_segment(a, q, c, ub + ui, ui, t0, t0 + (seg_end - it), lds);
     it = (seg_end == ui * a.U + a.T) ? (ui + 1) * a.U : seg_end;
   }
+}
+
+// Second launch: one workgroup per unit whose key range was split over several chunks
+// merges their partial results (the kernel boundary makes them visible on every XCD).
+__global__ __launch_bounds__(kAttnThreads) void attn_merge_kernel(AttnArgs a) {
+  const int unit = blockIdx.x;
+  int q = 0;
+  while (q + 1 < a.n_queues && unit >= a.unit_base[q + 1]) ++q;
+  const int ui = unit - a.unit_base[q];
+  const int c_first = (int)(((int64_t)ui * a.U) / a.E);
+  const int c_last = (int)(((int64_t)ui * a.U + a.T - 1) / a.E);
+  if (c_first == c_last) return;  // written whole by its only chunk
+  merge_unit(a, q, unit, ui, c_first, c_last);
 }
 
 __global__ void xcc_probe_kernel(int* ids) {
@@ -492,8 +484,11 @@ __global__ void xcc_probe_kernel(int* ids) {
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t s) {
+hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t s) {
   hipLaunchKernelGGL(attn_fwd_kernel, dim3(grid), dim3(kAttnThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !merge) return e;
+  hipLaunchKernelGGL(attn_merge_kernel, dim3(a.n_units), dim3(kAttnThreads), 0, s, a);
   return hipGetLastError();
 }
 

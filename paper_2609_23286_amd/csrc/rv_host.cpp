@@ -54,19 +54,12 @@ struct Workspace {
   bool ready = false;
   int n_cus = 0;
   int max_lds = 0;
-  int n_queues = 1;
-  int xcc_queue[16];
+  int n_queues = 1;          // attention work queues: one per XCD
   float* part = nullptr;     // attention partial slots
   size_t part_floats = 0;
-  int* unit_ctr = nullptr;   // attention unit counters (zero between launches)
-  size_t n_unit_ctr = 0;
-  int* ctrl = nullptr;       // device status bits
-  bool safe = false;         // workgroup placement not round-robin: device-scope fences
   float* sal = nullptr;      // saliency staging when the caller passes none
   size_t sal_floats = 0;
 };
-constexpr size_t kCtrlErrOffsetBytes = 0;
-constexpr size_t kCtrlBytes = 256;
 
 std::mutex g_ws_mu;
 std::map<int, Workspace> g_ws;
@@ -99,11 +92,10 @@ rv_status grow(T** p, size_t* have, size_t need, bool zero, const char* what) {
   return RV_OK;
 }
 
-// Learns where the hardware places workgroups: workgroup ids are expected to be dealt
-// round-robin over the XCDs (id b on the XCD of id b % n), which the attention kernel's
-// XCD-local merges rely on.  Also reads the CU count and the LDS limit, and allocates
-// the status block.  If placement is not round-robin the library uses device-scope
-// fences instead (correct, slower).
+// Reads the CU count and the LDS limit, and counts the XCDs (distinct XCC ids seen by
+// a probe launch): the attention kernel keeps one work queue per XCD so that the query
+// tiles of a head share an L2.  Placement only steers locality; results never depend
+// on it.
 rv_status init_device(Workspace* ws, int dev) {
   if (ws->ready) return RV_OK;
   RV_HIP(hipDeviceGetAttribute(&ws->n_cus, hipDeviceAttributeMultiprocessorCount, dev), "CU count");
@@ -116,32 +108,10 @@ rv_status init_device(Workspace* ws, int dev) {
   if (e == hipSuccess) e = hipMemcpy(ids.data(), d_ids, n_probe * sizeof(int), hipMemcpyDeviceToHost);
   (void)hipFree(d_ids);
   if (e != hipSuccess) return hip_fail(e, "placement probe");
-  // n = number of distinct XCC ids; round-robin iff ids[b] == ids[b % n] for all b
   std::vector<int> distinct;
   for (int id : ids)
     if (std::find(distinct.begin(), distinct.end(), id) == distinct.end()) distinct.push_back(id);
-  const int n = (int)distinct.size();
-  bool rr = n >= 1 && n <= rv::kMaxQueues;
-  for (int b = 0; rr && b < n; ++b)
-    for (int b2 = 0; b2 < b; ++b2) rr = rr && ids[b] != ids[b2];
-  for (int b = 0; rr && b < n_probe; ++b) rr = ids[b] == ids[b % n];
-  for (int i = 0; i < 16; ++i) ws->xcc_queue[i] = -1;
-  if (rr) {
-    ws->n_queues = n;
-    for (int qi = 0; qi < n; ++qi) ws->xcc_queue[ids[qi] & 15] = qi;
-    ws->safe = false;
-  } else {
-    ws->n_queues = 8;
-    ws->safe = true;
-  }
-  char* ctrl = nullptr;
-  RV_HIP(hipMalloc(&ctrl, kCtrlBytes), "status block");
-  e = hipMemset(ctrl, 0, kCtrlBytes);
-  if (e != hipSuccess) {
-    (void)hipFree(ctrl);
-    return hip_fail(e, "status block");
-  }
-  ws->ctrl = reinterpret_cast<int*>(ctrl);
+  ws->n_queues = std::max(1, std::min((int)distinct.size(), rv::kMaxQueues));
   ws->ready = true;
   return RV_OK;
 }
@@ -206,11 +176,10 @@ AttnPlan plan_attention(const Workspace& ws, int n_tokens, int64_t mem_len, int 
   for (int q = 0; q <= nq; ++q) p.unit_base[q] = (int)((int64_t)q * p.n_units / nq);
   for (int q = 0; q < nq; ++q) max_units = std::max(max_units, p.unit_base[q + 1] - p.unit_base[q]);
   const int e_min = std::max(1, env_int("RV_ATTN_MIN_CHUNK", 2));
-  // Stream-K balances the tiles exactly but pays, per chunk that straddles two units,
-  // a second pipeline start and publish (a few tiles' time); the aligned split leaves
-  // some workgroup slots idle.  Take the split while its chunks are at most
-  // kSplitSlackTiles longer than stream-K's.
-  constexpr int kSplitSlackTiles = 6;
+  // Stream-K balances the tiles exactly but pays, per chunk that straddles two units, a
+  // second pipeline start; the aligned split leaves some workgroup slots idle.  Take the
+  // split while its chunks are at most kSplitSlackTiles longer than stream-K's.
+  constexpr int kSplitSlackTiles = 1;
   int k = env_int("RV_ATTN_SPLIT", -1);
   if (k < 0) {
     k = wg_per_queue / std::max(1, max_units);
@@ -238,10 +207,8 @@ AttnPlan plan_attention(const Workspace& ws, int n_tokens, int64_t mem_len, int 
 }
 
 rv_status reserve_attention(Workspace* ws, const AttnPlan& p) {
-  rv_status st = grow(&ws->part, &ws->part_floats, (size_t)2 * p.total_chunks * rv::kAttnSlotFloats, false,
-                      "attention workspace");
-  if (st != RV_OK) return st;
-  return grow(&ws->unit_ctr, &ws->n_unit_ctr, (size_t)p.n_units, true, "attention counters");
+  return grow(&ws->part, &ws->part_floats, (size_t)2 * p.total_chunks * rv::kAttnSlotFloats, false,
+              "attention workspace");
 }
 
 }  // namespace
@@ -546,14 +513,8 @@ rv_status rv_device_status(void) {
   rv_status st = current_ws(&ws);
   if (st != RV_OK) return st;
   RV_HIP(hipDeviceSynchronize(), "device synchronisation");
-  int bits = 0;
-  char* err = reinterpret_cast<char*>(ws->ctrl) + kCtrlErrOffsetBytes;
-  RV_HIP(hipMemcpy(&bits, err, sizeof bits, hipMemcpyDeviceToHost), "status read");
-  if (bits == 0) return RV_OK;
-  RV_HIP(hipMemset(err, 0, sizeof bits), "status reset");
-  return fail(RV_ERR_HIP, "device status 0x%x:%s", bits,
-              (bits & 1) ? " an attention workgroup ran on another XCD than its id's round-robin "
-                           "placement (merged results may be wrong)" : "");
+  RV_HIP(hipGetLastError(), "device status");
+  return RV_OK;
 }
 
 rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
@@ -596,8 +557,6 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   a.out = (uint16_t*)out;
   a.lse = lse;
   a.part = ws->part;
-  a.unit_ctr = ws->unit_ctr;
-  a.err = reinterpret_cast<int*>(reinterpret_cast<char*>(ws->ctrl) + kCtrlErrOffsetBytes);
   a.n_tokens = n_tokens;
   a.n_heads = n_heads;
   a.q_tiles = p.q_tiles;
@@ -607,14 +566,14 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   a.n_units = p.n_units;
   a.n_queues = ws->n_queues;
   a.E = p.E;
-  a.safe = ws->safe ? 1 : 0;
   for (int q = 0; q <= ws->n_queues; ++q) a.unit_base[q] = p.unit_base[q];
   for (int q = 0; q < ws->n_queues; ++q) {
     a.n_chunks[q] = p.n_chunks[q];
     a.chunk_base[q] = p.chunk_base[q];
   }
-  for (int i = 0; i < 16; ++i) a.xcc_queue[i] = ws->xcc_queue[i];
-  RV_HIP(rv::launch_attention(a, p.grid, s), "attention launch");
+  // every unit whole in one chunk (no split) needs no merge launch
+  const bool split = (int64_t)p.E < p.T || p.U != p.T || (int64_t)p.T % p.E != 0;
+  RV_HIP(rv::launch_attention(a, p.grid, split, s), "attention launch");
 
   if (saliency) {
     rv::AdmitArgs b{};

@@ -34,8 +34,6 @@ struct AttnArgs {
   uint16_t* out;           // [N][H][64]
   float* lse;              // [H][N]
   float* part;             // partial slots, kAttnSlotFloats each
-  int* unit_ctr;           // [n_units] contributor counters, zero between launches
-  int* err;                // device status bits (see rv_device_status)
   int n_tokens;
   int n_heads;
   int q_tiles;
@@ -45,13 +43,11 @@ struct AttnArgs {
   int n_units;             // n_heads * q_tiles
   int n_queues;
   int E;                   // key tiles per chunk
-  int safe;                // 1: placement not verified, use device-scope fences
   int unit_base[kMaxQueues + 1];
   int n_chunks[kMaxQueues];
   int chunk_base[kMaxQueues];
-  int xcc_queue[16];       // hardware XCC id -> queue, -1 if unmapped
 };
-constexpr int kAttnSlotFloats = kAttnBQ * kHeadDim + 2 * kAttnBQ;
+constexpr int kAttnSlotFloats = kAttnBQ * kHeadDim / 2 + 2 * kAttnBQ;  // bf16 rows + m, l
 
 // One layer's share of the saliency / selection / append kernel.
 struct AdmitLayer {
@@ -92,7 +88,7 @@ struct AdmitArgs {
   int shared_select;       // selection: one top-k per layer on the head sum, shared by all heads
 };
 
-hipError_t launch_attention(const AttnArgs& a, int grid, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t s);
 // Records the hardware XCC id of each of n_blocks workgroups into ids (device memory).
 hipError_t launch_xcc_probe(int* ids, int n_blocks, hipStream_t s);
 // Dynamic LDS bytes the admission kernels need for these arguments (the larger of the
