@@ -36,6 +36,7 @@ CSRC = os.path.join(ROOT, "paper_2609_23286_amd", "csrc")
 # Kernel -> the sources whose text decides its memory traffic; counters recorded for
 # other sources are stale and are not reported.
 KERNEL_SOURCES = {"attn_fwd_kernel": ("attend.hip", "rv_internal.h", "rv_host.cpp"),
+                  "attn_merge_kernel": ("attend.hip", "rv_internal.h", "rv_host.cpp"),
                   "sal_kernel": ("admit.hip", "rv_internal.h", "rv_host.cpp"),
                   "select_kernel": ("admit.hip", "rv_internal.h", "rv_host.cpp")}
 ADMISSION_KERNELS = ("sal_kernel", "select_kernel")  # one launch each per frame
@@ -74,9 +75,9 @@ def traffic_path(kernel, workload):
     return os.path.join(PROFILES, f"{kernel}__{workload}__hbm_traffic.md")
 
 
-def recorded_traffic(kernel, workload):
-    """HBM bytes per launch from the committed counter summary, or None when there is
-    none or the kernel's sources changed since it was taken."""
+def recorded_counters(kernel, workload):
+    """(HBM bytes per launch, dispatches counted) from the committed counter summary, or
+    None when there is none or the kernel's sources changed since it was taken."""
     try:
         text = open(traffic_path(kernel, workload)).read()
     except OSError:
@@ -89,9 +90,23 @@ def recorded_traffic(kernel, workload):
     if kv.get("source_hash") != kernel_source_hash(kernel):
         return None
     try:
-        return float(kv["hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
+        return float(kv["hbm_bytes_per_launch"]), int(kv["dispatches"].split()[0])
+    except (KeyError, ValueError, IndexError):
         return None
+
+
+def recorded_traffic(kernel, workload):
+    rec = recorded_counters(kernel, workload)
+    return None if rec is None else rec[0]
+
+
+def attention_traffic(workload):
+    """HBM bytes of one layer's attention step: the forward launch plus, averaged over
+    the stream, the merge launch that split plans add."""
+    fwd, merge = recorded_counters("attn_fwd_kernel", workload), recorded_counters("attn_merge_kernel", workload)
+    if fwd is None or merge is None:
+        return None
+    return fwd[0] + merge[0] * merge[1] / fwd[1]
 
 
 def admission_traffic(workload):
@@ -184,6 +199,11 @@ def summarize_trace(trace_dir, bench_json, workload):
         return name.split("(")[0]
 
     avg = {short(r["Name"]): float(r["AverageNs"]) / 1e3 for r in rows}
+    total = {short(r["Name"]): float(r["TotalDurationNs"]) / 1e3 for r in rows}
+    calls = {short(r["Name"]): int(r["Calls"]) for r in rows}
+    # One attention step = attn_fwd_kernel, plus attn_merge_kernel for a split plan.
+    attn_step = ((total.get("attn_fwd_kernel", 0.0) + total.get("attn_merge_kernel", 0.0))
+                 / max(calls.get("attn_fwd_kernel", 1), 1))
     lines = [f"# Kernel time summary: {workload} benchmark", "",
              "Command (on the MI355X, from the repository root):", "", "```",
              "cd /tmp && export TMPDIR=/tmp",
@@ -199,8 +219,10 @@ def summarize_trace(trace_dir, bench_json, workload):
     adm = sum(avg.get(k, 0.0) for k in ADMISSION_KERNELS)
     lines += ["", "The same run's benchmark line (HIP events on the compute stream):", "",
               f"- frames/s: {bench['value']:.1f}",
-              f"- attention: {bench['roofline']['avg_launch_us']:.1f} us per launch (events) vs "
-              f"{avg.get('attn_fwd_kernel', 0.0):.1f} us (rocprofv3 average of attn_fwd_kernel)",
+              f"- attention: {bench['roofline']['avg_launch_us']:.1f} us per layer step (events around "
+              f"the forward launch and, for split plans, the merge launch) vs {attn_step:.1f} us "
+              f"(rocprofv3: attn_fwd_kernel + attn_merge_kernel time per attn_fwd_kernel call; "
+              f"attn_fwd_kernel alone averages {avg.get('attn_fwd_kernel', 0.0):.1f} us)",
               f"- admission: {bench['phases']['admission_ms'] / bench['steps'] * 1e3:.1f} us per frame (events; "
               f"the pair also spans the launch gaps) vs {adm:.1f} us (rocprofv3 averages of "
               + " + ".join(ADMISSION_KERNELS) + ")",
@@ -466,9 +488,10 @@ def main():
                    "regulated_layers": len(regulated), "anchor": anchor,
                    "selection": "head-averaged" if args.shared else "head-specific",
                    "prefill_rows": cfg.prefill},
-        "roofline": {"kernel": "attn_fwd_kernel", "bound": "mfma", "achieved": achieved_tf,
+        "roofline": {"kernel": "attn_fwd_kernel (+ attn_merge_kernel on split plans)", "bound": "mfma",
+                     "achieved": achieved_tf,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved_tf / PEAK_BF16_TFLOPS,
-                     "traffic": recorded_traffic("attn_fwd_kernel", wkey) if wkey else None,
+                     "traffic": attention_traffic(wkey) if wkey else None,
                      "avg_launch_us": attn_avg_s * 1e6,
                      "algorithmic_flops_per_launch": flops / n_attn},
         "phases": {"attention_ms": attn_ms, "admission_ms": admit_ms,

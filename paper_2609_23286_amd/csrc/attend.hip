@@ -56,6 +56,11 @@ constexpr float kNegBig = -1.0e30f;
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
+template <int P>
+struct StageConst {
+  static constexpr int value = P;
+};
+
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -94,66 +99,71 @@ __device__ __forceinline__ int swz(int row, int chunk) { return row * D + ((chun
 // (global_load_lds_dwordx4: lane l of a wave writes 16 bytes at the wave's LDS base +
 // 16 l), so each thread fetches the global chunk that belongs at its LDS slot: thread
 // tid fills physical chunk tid % 8 of rows tid / 8 and tid / 8 + 32, i.e. the global
-// chunk (tid % 8) ^ ((row >> 1) & 7) of those rows.
+// chunk (tid % 8) ^ ((row >> 1) & 7) of those rows.  Addresses are a wave-uniform base
+// plus a 32-bit per-thread byte offset fixed for the whole segment; the last tile of
+// each part re-reads its last row in place of the rows past the end (always in
+// bounds; their scores are masked).
 struct TileCursor {
-  const uint16_t* km;
-  const uint16_t* vm;
-  const uint16_t* kc;
-  const uint16_t* vc;
-  int64_t cur_tile;        // elements between consecutive frame tiles: 64 * H * 64
-  int off_m0, off_m1;      // thread offsets inside a memory tile
-  int off_c0, off_c1;      // thread offsets inside a frame tile
+  const char* km;          // memory K / V rows of this head
+  const char* vm;
+  const char* kc;          // the frame's K / V rows of this head
+  const char* vc;
+  int64_t cur_tile;        // bytes between consecutive frame tiles: 64 * H * 64 * 2
+  uint32_t off_m0, off_m1;     // thread byte offsets inside a full memory tile
+  uint32_t off_c0, off_c1;     // ... inside a full frame tile
+  uint32_t dt_m0, dt_m1;   // added for the last memory tile (rows clamped)
+  uint32_t dt_c0, dt_c1;   // added for the last frame tile
+  int nt_mem;              // memory tiles
+  int t_last;              // index of the unit's last tile
+  int mem_tail;            // valid rows of the last memory tile
+  int tok_tail;            // valid rows of the last frame tile
 };
 
-__device__ __forceinline__ int tile_valid(const AttnArgs& a, int t) {
-  return t < a.nt_mem ? (int)min((int64_t)BK, a.mem_len - (int64_t)t * BK)
-                      : min(BK, a.n_tokens - (t - a.nt_mem) * BK);
+__device__ __forceinline__ int tile_valid(const TileCursor& tc, int t) {
+  int v = BK;
+  if (t == tc.t_last) v = tc.tok_tail;
+  if (t == tc.nt_mem - 1) v = tc.mem_tail;
+  return v;
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-
-__device__ __forceinline__ void lds_load16(const uint16_t* g, uint16_t* lds_wave_base) {
+__device__ __forceinline__ void lds_load16(const char* g, uint16_t* lds_wave_base) {
   __builtin_amdgcn_global_load_lds((const void*)g, (lds_void*)lds_wave_base, 16, 0, 0);
 }
 
-// Issue tile t's K and V loads into `stage` (completion: vmcnt + barrier).  Rows past the
-// end of a segment re-read its last row (always in bounds); their scores are masked.
-__device__ __forceinline__ void load_tile(const AttnArgs& a, const TileCursor& tc, int t, int tid,
-                                          uint16_t* stage) {
-  const uint16_t *kb, *vb;
-  int o0, o1;
-  if (t < a.nt_mem) {  // uniform branch
-    kb = tc.km + (int64_t)t * (BK * D);
-    vb = tc.vm + (int64_t)t * (BK * D);
+// Issue tile t's K and V loads into ring stage S (completion: vmcnt + barrier).
+// `ldsw` is the LDS ring plus this wave's row block (rows 8w .. 8w+7 of a tile; the
+// second load of each operand fills rows 32 + 8w ..).
+template <int S>
+__device__ __forceinline__ void load_tile(const TileCursor& tc, int t, uint16_t* ldsw) {
+  const char *kb, *vb;
+  uint32_t o0, o1;
+  if (t < tc.nt_mem) {  // uniform branches
+    kb = tc.km + (int64_t)t * (BK * D * 2);
+    vb = tc.vm + (int64_t)t * (BK * D * 2);
     o0 = tc.off_m0;
     o1 = tc.off_m1;
-    const int64_t rows = a.mem_len - (int64_t)t * BK;
-    if (rows < BK) {  // ragged last memory tile
-      const int r = tid >> 3, c = tid & 7, last = (int)rows - 1;
-      o0 = min(r, last) * D + ((c ^ ((r >> 1) & 7)) << 3);
-      o1 = min(r + 32, last) * D + ((c ^ (((r + 32) >> 1) & 7)) << 3);
+    if (t == tc.nt_mem - 1) {  // (additive, so no select between two fields' addresses)
+      o0 += tc.dt_m0;
+      o1 += tc.dt_m1;
     }
   } else {
-    const int tc_i = t - a.nt_mem;
-    kb = tc.kc + (int64_t)tc_i * tc.cur_tile;
-    vb = tc.vc + (int64_t)tc_i * tc.cur_tile;
+    const int tc_i = t - tc.nt_mem;
+    kb = tc.kc + tc_i * tc.cur_tile;
+    vb = tc.vc + tc_i * tc.cur_tile;
     o0 = tc.off_c0;
     o1 = tc.off_c1;
-    const int rows = a.n_tokens - tc_i * BK;
-    if (rows < BK) {  // ragged last frame tile
-      const int r = tid >> 3, c = tid & 7, last = rows - 1;
-      const int rs = a.n_heads * D;
-      o0 = min(r, last) * rs + ((c ^ ((r >> 1) & 7)) << 3);
-      o1 = min(r + 32, last) * rs + ((c ^ (((r + 32) >> 1) & 7)) << 3);
+    if (t == tc.t_last) {
+      o0 += tc.dt_c0;
+      o1 += tc.dt_c1;
     }
   }
-  // wave w fills rows 8w .. 8w+7 (first load) and 32 + 8w .. (second load)
-  const int w8 = (tid >> 6) * 8 * D;
-  lds_load16(kb + o0, stage + w8);
-  lds_load16(kb + o1, stage + 32 * D + w8);
-  lds_load16(vb + o0, stage + TILE + w8);
-  lds_load16(vb + o1, stage + TILE + 32 * D + w8);
+  uint16_t* st = ldsw + S * STAGE;
+  lds_load16(kb + o0, st);
+  lds_load16(kb + o1, st + 32 * D);
+  lds_load16(vb + o0, st + TILE);
+  lds_load16(vb + o1, st + TILE + 32 * D);
 }
 
 struct SoftmaxState {
@@ -194,7 +204,7 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
   // accumulators, recompute P.  Terms far below the reference underflow to 0, exactly
   // as they would relative to the true maximum.
   bf16x8 p[4];
-  float rsum = 0.f;
+  float rsum = -0.f;  // -0 + x == x: the first add folds away
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], kScaleLog2, -sm.m));
@@ -213,7 +223,7 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
     sm.o0 *= alpha;
     sm.o1 *= alpha;
     sm.m = m_new;
-    rsum = 0.f;
+    rsum = -0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], kScaleLog2, -sm.m));
@@ -358,17 +368,27 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   TileCursor tc;
   {
     const int r = tid >> 3, c8 = (tid & 7) * 8, rs = a.n_heads * D;
-    tc.km = a.memK + (int64_t)h * a.head_stride * D;
-    tc.vm = a.memV + (int64_t)h * a.head_stride * D;
-    tc.kc = a.K + (int64_t)h * D;
-    tc.vc = a.V + (int64_t)h * D;
-    tc.cur_tile = (int64_t)BK * rs;
-    const int g0 = (c8 ^ (((r >> 1) & 7) << 3)), g1 = (c8 ^ ((((r + 32) >> 1) & 7) << 3));
-    tc.off_m0 = r * D + g0;
-    tc.off_m1 = (r + 32) * D + g1;
-    tc.off_c0 = r * rs + g0;
-    tc.off_c1 = (r + 32) * rs + g1;
+    tc.km = reinterpret_cast<const char*>(a.memK + (int64_t)h * a.head_stride * D);
+    tc.vm = reinterpret_cast<const char*>(a.memV + (int64_t)h * a.head_stride * D);
+    tc.kc = reinterpret_cast<const char*>(a.K + (int64_t)h * D);
+    tc.vc = reinterpret_cast<const char*>(a.V + (int64_t)h * D);
+    tc.cur_tile = (int64_t)BK * rs * 2;
+    tc.nt_mem = a.nt_mem;
+    tc.t_last = a.T - 1;
+    tc.mem_tail = a.nt_mem > 0 ? (int)(a.mem_len - (int64_t)(a.nt_mem - 1) * BK) : BK;
+    tc.tok_tail = a.n_tokens - (a.T - 1 - a.nt_mem) * BK;
+    const int r1 = r + 32;
+    const int g0 = (c8 ^ (((r >> 1) & 7) << 3)), g1 = (c8 ^ (((r1 >> 1) & 7) << 3));
+    tc.off_m0 = 2u * (uint32_t)(r * D + g0);
+    tc.off_m1 = 2u * (uint32_t)(r1 * D + g1);
+    tc.off_c0 = 2u * (uint32_t)(r * rs + g0);
+    tc.off_c1 = 2u * (uint32_t)(r1 * rs + g1);
+    tc.dt_m0 = 2u * (uint32_t)(min(r, tc.mem_tail - 1) * D + g0) - tc.off_m0;
+    tc.dt_m1 = 2u * (uint32_t)(min(r1, tc.mem_tail - 1) * D + g1) - tc.off_m1;
+    tc.dt_c0 = 2u * (uint32_t)(min(r, tc.tok_tail - 1) * rs + g0) - tc.off_c0;
+    tc.dt_c1 = 2u * (uint32_t)(min(r1, tc.tok_tail - 1) * rs + g1) - tc.off_c1;
   }
+  uint16_t* const ldsw = lds + wave * 8 * D;
 
   // B operand of S^T = K Q^T: this lane's query, head dims ds*16 + half*8 .. +7.
   bf16x8 qf[4];
@@ -383,22 +403,29 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   sm.o0 = f32x16{};
   sm.o1 = f32x16{};
 
-  // Ring of NSTAGE (4) tiles, two computed per barrier: tile t lives in stage t % 4.  The
-  // next pair streams into the two stages the previous pair used (freed at the last
-  // barrier) while this pair is computed.
-  load_tile(a, tc, t0, tid, lds + (t0 % NSTAGE) * STAGE);
-  if (t0 + 1 < t1) load_tile(a, tc, t0 + 1, tid, lds + ((t0 + 1) % NSTAGE) * STAGE);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  for (int t = t0; t < t1; t = uniform(t + 2)) {
-    if (t + 2 < t1) load_tile(a, tc, t + 2, tid, lds + ((t + 2) % NSTAGE) * STAGE);
-    if (t + 3 < t1) load_tile(a, tc, t + 3, tid, lds + ((t + 3) % NSTAGE) * STAGE);
+  // Ring of NSTAGE (4) tiles, two computed per barrier: tile t0 + j lives in stage j % 4,
+  // so every stage offset is a compile-time constant of the unrolled loop.  The next
+  // pair streams into the two stages the previous pair used (freed at the last barrier)
+  // while this pair is computed.
+  auto step = [&](auto phase, int t) {
+    constexpr int P = decltype(phase)::value;
+    if (t + 2 < t1) load_tile<(P + 2) % NSTAGE>(tc, t + 2, ldsw);
+    if (t + 3 < t1) load_tile<(P + 3) % NSTAGE>(tc, t + 3, ldsw);
     if (wave_active) {
-      tile_compute(lds + (t % NSTAGE) * STAGE, qf, lane, tile_valid(a, t), sm);
-      if (t + 1 < t1) tile_compute(lds + ((t + 1) % NSTAGE) * STAGE, qf, lane, tile_valid(a, t + 1), sm);
+      tile_compute(lds + P * STAGE, qf, lane, tile_valid(tc, t), sm);
+      if (t + 1 < t1) tile_compute(lds + (P + 1) * STAGE, qf, lane, tile_valid(tc, t + 1), sm);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  };
+  load_tile<0>(tc, t0, ldsw);
+  if (t0 + 1 < t1) load_tile<1>(tc, t0 + 1, ldsw);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  for (int t = t0; t < t1; t = uniform(t + 4)) {
+    step(StageConst<0>{}, t);
+    if (t + 2 >= t1) break;
+    step(StageConst<2>{}, t + 2);
   }
 
   const float l_tot = half_sum(sm.l);
