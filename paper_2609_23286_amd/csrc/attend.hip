@@ -263,16 +263,11 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
   }
 }
 
-// Merge every partial of `unit` (contributor chunks c_first..c_last of queue q, in
-// chunk order) and write the final output rows and LSE.  A partial is the chunk's
-// output normalised by its own row sum, in bf16, with its reference m and sum l; the
-// merge weights it by 2^(m - M) l (M the largest m).  Thread -> (row, 32 dims).
-// Partials are taken eight at a time: their (m, l) pairs in one round trip, then their
-// rows kMergeBatch partials at a time; loads are unconditional (indices clamped, surplus
-// weights zero) so that each batch is in flight together.
-constexpr int kMergeGroup = 8;
-constexpr int kSlotStatsFloat = BQ * D / 2;  // slot: BQ x 64 bf16 rows, then m[BQ], l[BQ] (fp32)
-constexpr int kMergeBatch = 4;   // partials whose rows are in flight together
+// Partial slots: chunk c's segment of a unit writes its output rows normalised by its
+// own row sum, in bf16 ([BQ][64]), then its reference m[BQ] and row sum l[BQ] (fp32).
+constexpr int kSlotStatsFloat = BQ * D / 2;
+constexpr int kMergeRows = 32;   // output rows per merge workgroup (8 threads per row)
+constexpr int kMergeMax = 8;     // partials whose loads are in flight together
 
 // Partial slot of chunk c's segment of unit ui: slot 0 if the chunk starts inside the
 // unit, slot 1 if it began in an earlier unit.
@@ -281,75 +276,58 @@ __device__ __forceinline__ const float* slot_ptr(const AttnArgs& a, int q, int c
   return a.part + (int64_t)slot * kAttnSlotFloats;
 }
 
-template <int NB>
-__device__ __forceinline__ void merge_rows(const float* const* ps, const float* w, int row, int dh,
-                                           float (&acc)[32]) {
-  uint4 v[NB][4];  // 32 bf16 of the row's normalised partial output
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const uint4* po = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(ps[j]) + row * D + dh);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v[j][e] = po[e];
-  }
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t wd[4] = {v[j][e].x, v[j][e].y, v[j][e].z, v[j][e].w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        acc[8 * e + 2 * i] = fmaf(w[j], __uint_as_float(wd[i] << 16), acc[8 * e + 2 * i]);
-        acc[8 * e + 2 * i + 1] = fmaf(w[j], __uint_as_float(wd[i] & 0xFFFF0000u), acc[8 * e + 2 * i + 1]);
-      }
-    }
-  }
-}
-
-__device__ void merge_unit(const AttnArgs& a, int q, int unit, int ui, int c_first, int c_last) {
+// Merge the partials of chunks c_first..c_last (in chunk order) for rows
+// rb*32 .. rb*32+31 of `unit` and write the final output rows and LSE.  Partial j is
+// weighted by 2^(m_j - M) l_j (M the largest m).  Thread -> (row, 8 dims); up to eight
+// partials' statistics and rows are loaded in one round trip (indices clamped, surplus
+// weights zero).
+__device__ void merge_rows(const AttnArgs& a, int q, int unit, int ui, int rb, int c_first, int c_last) {
   const int tid = threadIdx.x;
   const int h = unit / a.q_tiles, qt = unit % a.q_tiles;
-  const int row = tid >> 1, dh = (tid & 1) * 32;
+  const int row = rb * kMergeRows + (tid >> 3), d8 = (tid & 7) * 8;
   const int qi = qt * BQ + row;
   if (qi >= a.n_tokens) return;
   float mmax = kNegBig, L = 0.f;
-  float acc[32];
+  float acc[8];
 #pragma unroll
-  for (int e = 0; e < 32; ++e) acc[e] = 0.f;
-  for (int c0 = c_first; c0 <= c_last; c0 += kMergeGroup) {
-    const int n = min(kMergeGroup, c_last - c0 + 1);
-    const float* ps[kMergeGroup];
-    float mv[kMergeGroup], lv[kMergeGroup];
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  for (int c0 = c_first; c0 <= c_last; c0 += kMergeMax) {
+    const int n = min(kMergeMax, c_last - c0 + 1);
+    float mv[kMergeMax], lv[kMergeMax];
+    uint4 v[kMergeMax];
 #pragma unroll
-    for (int j = 0; j < kMergeGroup; ++j) {
-      ps[j] = slot_ptr(a, q, min(c0 + j, c_last), ui);
-      mv[j] = ps[j][kSlotStatsFloat + row];
-      lv[j] = ps[j][kSlotStatsFloat + BQ + row];
+    for (int j = 0; j < kMergeMax; ++j) {
+      const float* ps = slot_ptr(a, q, min(c0 + j, c_last), ui);
+      mv[j] = ps[kSlotStatsFloat + row];
+      lv[j] = ps[kSlotStatsFloat + BQ + row];
+      v[j] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(ps) + row * D + d8);
     }
     float m_new = mmax;
 #pragma unroll
-    for (int j = 0; j < kMergeGroup; ++j) m_new = fmaxf(m_new, mv[j]);  // clamped copies repeat a real one
+    for (int j = 0; j < kMergeMax; ++j) m_new = fmaxf(m_new, mv[j]);  // clamped copies repeat a real one
     const float scale = __builtin_amdgcn_exp2f(mmax - m_new);
     L *= scale;
 #pragma unroll
-    for (int e = 0; e < 32; ++e) acc[e] *= scale;
+    for (int e = 0; e < 8; ++e) acc[e] *= scale;
     mmax = m_new;
-    float w[kMergeGroup];  // weight of each normalised partial: 2^(m - M) l
 #pragma unroll
-    for (int j = 0; j < kMergeGroup; ++j) {
-      w[j] = j < n ? __builtin_amdgcn_exp2f(mv[j] - mmax) * lv[j] : 0.f;
-      L += w[j];
+    for (int j = 0; j < kMergeMax; ++j) {
+      const float w = j < n ? __builtin_amdgcn_exp2f(mv[j] - mmax) * lv[j] : 0.f;
+      L += w;
+      const uint32_t wd[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[2 * i] = fmaf(w, __uint_as_float(wd[i] << 16), acc[2 * i]);
+        acc[2 * i + 1] = fmaf(w, __uint_as_float(wd[i] & 0xFFFF0000u), acc[2 * i + 1]);
+      }
     }
-#pragma unroll
-    for (int b = 0; b < kMergeGroup; b += kMergeBatch)
-      if (b == 0 || b < n) merge_rows<kMergeBatch>(ps + b, w + b, row, dh, acc);
   }
   const float inv = 1.f / L;
-  uint16_t* op = a.out + ((int64_t)qi * a.n_heads + h) * D + dh;
-#pragma unroll
-  for (int e = 0; e < 8; ++e)
-    *reinterpret_cast<uint2*>(op + 4 * e) =
-        to_bf16x4(acc[4 * e] * inv, acc[4 * e + 1] * inv, acc[4 * e + 2] * inv, acc[4 * e + 3] * inv);
-  if (dh == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (mmax + __log2f(L)) * kLn2;
+  uint16_t* op = a.out + ((int64_t)qi * a.n_heads + h) * D + d8;
+  const uint2 lo = to_bf16x4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+  const uint2 hi = to_bf16x4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+  *reinterpret_cast<uint4*>(op) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  if (d8 == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (mmax + __log2f(L)) * kLn2;
 }
 
 // Key tiles t0..t1-1 of `unit` (queue-local index ui) as part of chunk c of queue q.
@@ -492,17 +470,18 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
   }
 }
 
-// Second launch: one workgroup per unit whose key range was split over several chunks
-// merges their partial results (the kernel boundary makes them visible on every XCD).
+// Second launch: for every unit whose key range was split over several chunks, four
+// workgroups (32 rows each) merge the partial results (the kernel boundary makes them
+// visible on every XCD).
 __global__ __launch_bounds__(kAttnThreads) void attn_merge_kernel(AttnArgs a) {
-  const int unit = blockIdx.x;
+  const int unit = blockIdx.x / (BQ / kMergeRows), rb = blockIdx.x % (BQ / kMergeRows);
   int q = 0;
   while (q + 1 < a.n_queues && unit >= a.unit_base[q + 1]) ++q;
   const int ui = unit - a.unit_base[q];
   const int c_first = (int)(((int64_t)ui * a.U) / a.E);
   const int c_last = (int)(((int64_t)ui * a.U + a.T - 1) / a.E);
   if (c_first == c_last) return;  // written whole by its only chunk
-  merge_unit(a, q, unit, ui, c_first, c_last);
+  merge_rows(a, q, unit, ui, rb, c_first, c_last);
 }
 
 __global__ void xcc_probe_kernel(int* ids) {
@@ -515,7 +494,7 @@ hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t
   hipLaunchKernelGGL(attn_fwd_kernel, dim3(grid), dim3(kAttnThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !merge) return e;
-  hipLaunchKernelGGL(attn_merge_kernel, dim3(a.n_units), dim3(kAttnThreads), 0, s, a);
+  hipLaunchKernelGGL(attn_merge_kernel, dim3(a.n_units * (BQ / kMergeRows)), dim3(kAttnThreads), 0, s, a);
   return hipGetLastError();
 }
 
