@@ -187,6 +187,50 @@ rv_status rv_admit_layers_shared(int n_layers, const void *const *Q, const void 
                                  float *const *saliency_out, int32_t *const *idx_out,
                                  void *stream);
 
+/* ---- staged frame: the frame's keys and values written straight into the arena ---------
+ *
+ * A producer (the layer's K/V projection) can write the frame's K and V directly into
+ * the memory's arena, past its valid rows, instead of into separate [n][H][64] tensors.
+ * Attention then reads one contiguous key range per head (memory rows followed by the
+ * frame), the saliency reads the frame's keys from there, and admission (Sec. 3.3 Eq. 6)
+ * becomes an in-place compaction: the selected rows move down to the end of the memory
+ * and the rest of the staged rows are dropped.  Given the same K and V, attention
+ * results equal the frame entry points' within the same error bounds, and bit for bit
+ * when the memory length is a multiple of 64 (the 64-key tiles then coincide; otherwise
+ * the frame's keys start mid-tile and the fp32 sums run in another order); admission
+ * given the same LSE is bit-identical. */
+
+/* Stages a frame of n_tokens rows: ensures capacity >= length + n_tokens (growing, and so
+ * moving, the arenas if needed: RV_ERR_CAPACITY / RV_ERR_OOM leave m unchanged) and
+ * returns the device address of row `length` of head 0 in the K and V arenas and the
+ * row stride between heads.  Row j of head h of the frame goes to
+ * K_tail + (h * head_stride_tokens + j) * 64 (bf16), likewise for V.  The length is not
+ * changed; any call that grows m drops the staged rows.  Outputs may be NULL. */
+rv_status rv_mem_stage(rv_mem m, int n_tokens, void **K_tail, void **V_tail,
+                       int64_t *head_stride_tokens, void *stream);
+
+/* rv_mem_stage, then copies a frame given as [n_tokens][n_heads][64] bf16 K, V (device
+ * memory) into the staged rows, on `stream`. */
+rv_status rv_mem_stage_frame(rv_mem m, const void *K, const void *V, int n_tokens, void *stream);
+
+/* rv_attend_frame (Sec. 3.1 Eq. 3, Sec. 3.3 LSE and saliency) for a frame staged in m:
+ * the keys and values of head h are arena rows 0 .. length + n_tokens - 1 of m, i.e. the
+ * memory followed by the staged frame.  Q, out: [n_tokens][n_heads][64] bf16; lse,
+ * saliency (NULL, or with qs): [n_heads][n_tokens] fp32.  RV_ERR_INVALID if fewer than
+ * n_tokens rows are staged (capacity < length + n_tokens). */
+rv_status rv_attend_staged(const void *Q, int n_tokens, rv_mem m, const rv_qsub *qs, void *out,
+                           float *lse, float *saliency, void *stream);
+
+/* rv_admit_layers (Sec. 3.3 saliency and Eq. 6) for frames staged in mems: layer l's
+ * saliency uses the staged keys of mems[l]; its `budget` selected rows (ascending token
+ * order) are compacted in place to rows length .. length + budget - 1 with provenance
+ * (frame_id, token) and the length grows by `budget`.  No memory grows here; every
+ * layer must have n_tokens rows staged (RV_ERR_INVALID otherwise). */
+rv_status rv_admit_staged_layers(int n_layers, const void *const *Q, const float *const *lse,
+                                 int n_tokens, const rv_qsub *qs, int budget, const rv_mem *mems,
+                                 int frame_id, float *const *saliency_out, int32_t *const *idx_out,
+                                 void *stream);
+
 /* Synchronises the current device and reports any error the HIP runtime recorded for
  * earlier work (RV_ERR_HIP with the runtime's message).  Test harnesses call it after
  * each step. */

@@ -76,7 +76,7 @@ __global__ __launch_bounds__(NT) void sal_kernel(AdmitArgs a) {
 #pragma unroll
     for (int b = 0; b < kBlocksPerStep; ++b) {
       const int j = min((bb + b) * 32 + l32, N - 1);  // past the frame or the range: result unused
-      const uint16_t* kp = L.K + ((int64_t)j * H + h) * D + half * 8;
+      const uint16_t* kp = L.K + (int64_t)j * L.kv_row + (int64_t)h * L.kv_head + half * 8;
 #pragma unroll
       for (int ds = 0; ds < 4; ++ds) kf[b][ds] = *reinterpret_cast<const bf16x8*>(kp + ds * 16);
     }
@@ -406,16 +406,39 @@ __global__ __launch_bounds__(NT) void select_kernel(AdmitArgs a) {
     if (L.idx)
       for (int r = tid; r < k; r += NT) L.idx[(int64_t)h * k + r] = s_idx[r];
     // 16-byte chunks: 8 per K row, 8 per V row.
-    for (int c = tid; c < k * 16; c += NT) {
-      const int r = c >> 4, part = c & 15, chunk = part & 7;
-      const int j = s_idx[r];
-      if (j < 0 || j >= N) continue;  // unreachable: the selection emits exactly k indices < N
-      const int64_t src = ((int64_t)j * H + h) * D + chunk * 8;
-      const int64_t dst = ((int64_t)h * L.head_stride + L.mem_len + r) * D + chunk * 8;
-      if (part < 8)
-        *reinterpret_cast<uint4*>(L.memK + dst) = *reinterpret_cast<const uint4*>(L.K + src);
-      else
-        *reinterpret_cast<uint4*>(L.memV + dst) = *reinterpret_cast<const uint4*>(L.V + src);
+    if (!a.in_place) {
+      for (int c = tid; c < k * 16; c += NT) {
+        const int r = c >> 4, part = c & 15, chunk = part & 7;
+        const int j = s_idx[r];
+        if (j < 0 || j >= N) continue;  // unreachable: the selection emits exactly k indices < N
+        const int64_t src = (int64_t)j * L.kv_row + (int64_t)h * L.kv_head + chunk * 8;
+        const int64_t dst = ((int64_t)h * L.head_stride + L.mem_len + r) * D + chunk * 8;
+        if (part < 8)
+          *reinterpret_cast<uint4*>(L.memK + dst) = *reinterpret_cast<const uint4*>(L.K + src);
+        else
+          *reinterpret_cast<uint4*>(L.memV + dst) = *reinterpret_cast<const uint4*>(L.V + src);
+      }
+    } else {
+      // Compaction inside the arena: the staged row idx[r] moves to row mem_len + r.
+      // Indices ascend, so idx[r] >= r: passes of NT / 16 rows in ascending order read
+      // all of a pass's sources before writing its destinations, and no later pass reads
+      // a row an earlier one wrote (its sources lie at or past its own destinations).
+      for (int r0 = 0; r0 < k; r0 += NT / 16) {
+        const int r = r0 + (tid >> 4), part = tid & 15, chunk = part & 7;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        int64_t dst = -1;
+        if (r < k) {
+          const int j = s_idx[r];
+          if (j >= 0 && j < N) {  // always: the selection emits exactly k indices < N
+            const int64_t src = (int64_t)j * L.kv_row + (int64_t)h * L.kv_head + chunk * 8;
+            v = *reinterpret_cast<const uint4*>((part < 8 ? L.K : L.V) + src);
+            dst = ((int64_t)h * L.head_stride + L.mem_len + r) * D + chunk * 8;
+          }
+        }
+        __syncthreads();
+        if (dst >= 0) *reinterpret_cast<uint4*>((part < 8 ? L.memK : L.memV) + dst) = v;
+        __syncthreads();
+      }
     }
     for (int r = tid; r < k; r += NT) {
       int32_t* pv = L.prov + ((int64_t)h * L.head_stride + L.mem_len + r) * 2;
@@ -482,6 +505,32 @@ hipError_t launch_admit(const AdmitArgs& a, int max_lds, hipStream_t s) {
     return hipGetLastError();
   }
   return hipSuccess;
+}
+
+namespace {
+
+// One thread per 16-byte chunk of the frame (8 per row of 64 bf16), in the frame's order.
+__global__ __launch_bounds__(256) void stage_kernel(uint16_t* dK, uint16_t* dV, int64_t head_stride,
+                                                    const uint16_t* K, const uint16_t* V, int n, int H) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= (int64_t)n * H * 8) return;
+  const int chunk = (int)(c & 7);
+  const int64_t row = c >> 3;  // token * H + head
+  const int h = (int)(row % H);
+  const int64_t j = row / H;
+  const int64_t d = ((int64_t)h * head_stride + j) * D + chunk * 8;
+  *reinterpret_cast<uint4*>(dK + d) = reinterpret_cast<const uint4*>(K)[c];
+  *reinterpret_cast<uint4*>(dV + d) = reinterpret_cast<const uint4*>(V)[c];
+}
+
+}  // namespace
+
+hipError_t launch_stage(uint16_t* dK, uint16_t* dV, int64_t head_stride, const uint16_t* K, const uint16_t* V,
+                        int n, int H, hipStream_t s) {
+  const int64_t chunks = (int64_t)n * H * 8;
+  hipLaunchKernelGGL(stage_kernel, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, dK, dV, head_stride,
+                     K, V, n, H);
+  return hipGetLastError();
 }
 
 }  // namespace rv

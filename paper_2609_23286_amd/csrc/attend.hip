@@ -354,7 +354,7 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
     tc.nt_mem = a.nt_mem;
     tc.t_last = a.T - 1;
     tc.mem_tail = a.nt_mem > 0 ? (int)(a.mem_len - (int64_t)(a.nt_mem - 1) * BK) : BK;
-    tc.tok_tail = a.n_tokens - (a.T - 1 - a.nt_mem) * BK;
+    tc.tok_tail = a.T > a.nt_mem ? a.n_fkeys - (a.T - 1 - a.nt_mem) * BK : BK;
     const int r1 = r + 32;
     const int g0 = (c8 ^ (((r >> 1) & 7) << 3)), g1 = (c8 ^ (((r1 >> 1) & 7) << 3));
     tc.off_m0 = 2u * (uint32_t)(r * D + g0);

@@ -163,11 +163,12 @@ struct AttnPlan {
   int chunk_base[rv::kMaxQueues];
 };
 
-AttnPlan plan_attention(const Workspace& ws, int n_tokens, int64_t mem_len, int n_heads) {
+// n_tokens queries; keys: mem_len memory rows, then n_fkeys frame rows.
+AttnPlan plan_attention(const Workspace& ws, int n_tokens, int n_fkeys, int64_t mem_len, int n_heads) {
   AttnPlan p{};
   p.q_tiles = (int)ceil_div(n_tokens, rv::kAttnBQ);
   p.nt_mem = (int)ceil_div(mem_len, rv::kAttnBK);
-  p.T = p.nt_mem + (int)ceil_div(n_tokens, rv::kAttnBK);
+  p.T = p.nt_mem + (int)ceil_div(n_fkeys, rv::kAttnBK);
   p.n_units = p.q_tiles * n_heads;
   const int nq = ws.n_queues;
   const int wg_per_queue =
@@ -500,7 +501,7 @@ rv_status rv_reserve_workspace(int n_tokens, int n_heads, int n_layers) {
   rv_status st = current_ws(&ws);
   if (st != RV_OK) return st;
   // the chunk count of a plan does not grow with the context: plan a long one
-  const AttnPlan p = plan_attention(*ws, n_tokens, (int64_t)1 << 20, n_heads);
+  const AttnPlan p = plan_attention(*ws, n_tokens, n_tokens, (int64_t)1 << 20, n_heads);
   st = reserve_attention(ws, p);
   if (st != RV_OK) return st;
   return grow(&ws->sal, &ws->sal_floats,
@@ -517,32 +518,23 @@ rv_status rv_device_status(void) {
   return RV_OK;
 }
 
-rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
-                          const void* memV, int64_t mem_len, int64_t head_stride_tokens, int n_heads,
-                          int head_dim, const rv_qsub* qs, void* out, float* lse, float* saliency,
-                          void* stream) {
-  if (n_tokens < 0 || n_tokens > rv::kMaxTokens)
-    return fail(RV_ERR_INVALID, "n_tokens must be in [0, %d] (got %d)", rv::kMaxTokens, n_tokens);
-  if (n_heads < 1) return fail(RV_ERR_INVALID, "n_heads must be >= 1");
-  if (head_dim != rv::kHeadDim) return fail(RV_ERR_INVALID, "head_dim must be 64 (got %d)", head_dim);
-  if (mem_len < 0) return fail(RV_ERR_INVALID, "mem_len must be >= 0");
-  if (mem_len > 0 && (!memK || !memV)) return fail(RV_ERR_INVALID, "memK/memV NULL with mem_len > 0");
-  if (mem_len > 0 && head_stride_tokens < mem_len)
-    return fail(RV_ERR_INVALID, "head_stride_tokens (%lld) < mem_len (%lld)", (long long)head_stride_tokens,
-                (long long)mem_len);
-  if (n_tokens == 0) return RV_OK;
-  if (!Q || !K || !V || !out || !lse) return fail(RV_ERR_INVALID, "Q, K, V, out and lse are required");
-  if (saliency) {
-    rv_status st = check_qsub(qs, n_tokens);
-    if (st != RV_OK) return st;
-  }
-  hipStream_t s = (hipStream_t)stream;
+}  // extern "C"
+
+namespace {
+
+// Attention (+ saliency) launch shared by the frame and staged entry points.  Keys: the
+// mem_len rows of memK/memV, then n_fkeys frame rows of K/V ([n][H][64]).  The saliency's
+// keys are the frame's rows j at sK + j * s_row + h * s_head.  Arguments are checked.
+rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens, int n_fkeys, const void* memK,
+                      const void* memV, int64_t mem_len, int64_t head_stride_tokens, int n_heads,
+                      const rv_qsub* qs, void* out, float* lse, float* saliency, const void* sK, int64_t s_row,
+                      int64_t s_head, hipStream_t s) {
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace* ws;
   rv_status st = current_ws(&ws);
   if (st != RV_OK) return st;
 
-  const AttnPlan p = plan_attention(*ws, n_tokens, mem_len, n_heads);
+  const AttnPlan p = plan_attention(*ws, n_tokens, n_fkeys, mem_len, n_heads);
   st = reserve_attention(ws, p);
   if (st != RV_OK) return st;
 
@@ -558,6 +550,7 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   a.lse = lse;
   a.part = ws->part;
   a.n_tokens = n_tokens;
+  a.n_fkeys = n_fkeys;
   a.n_heads = n_heads;
   a.q_tiles = p.q_tiles;
   a.nt_mem = p.nt_mem;
@@ -578,7 +571,9 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   if (saliency) {
     rv::AdmitArgs b{};
     b.layer[0].Q = (const uint16_t*)Q;
-    b.layer[0].K = (const uint16_t*)K;
+    b.layer[0].K = (const uint16_t*)sK;
+    b.layer[0].kv_row = s_row;
+    b.layer[0].kv_head = s_head;
     b.layer[0].lse = lse;
     b.layer[0].sal = saliency;
     set_qsub(&b, *qs);
@@ -590,6 +585,82 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
     RV_HIP(rv::launch_admit(b, ws->max_lds, s), "saliency launch");
   }
   return RV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
+                          const void* memV, int64_t mem_len, int64_t head_stride_tokens, int n_heads,
+                          int head_dim, const rv_qsub* qs, void* out, float* lse, float* saliency,
+                          void* stream) {
+  if (n_tokens < 0 || n_tokens > rv::kMaxTokens)
+    return fail(RV_ERR_INVALID, "n_tokens must be in [0, %d] (got %d)", rv::kMaxTokens, n_tokens);
+  if (n_heads < 1) return fail(RV_ERR_INVALID, "n_heads must be >= 1");
+  if (head_dim != rv::kHeadDim) return fail(RV_ERR_INVALID, "head_dim must be 64 (got %d)", head_dim);
+  if (mem_len < 0) return fail(RV_ERR_INVALID, "mem_len must be >= 0");
+  if (mem_len > 0 && (!memK || !memV)) return fail(RV_ERR_INVALID, "memK/memV NULL with mem_len > 0");
+  if (mem_len > 0 && head_stride_tokens < mem_len)
+    return fail(RV_ERR_INVALID, "head_stride_tokens (%lld) < mem_len (%lld)", (long long)head_stride_tokens,
+                (long long)mem_len);
+  if (n_tokens == 0) return RV_OK;
+  if (!Q || !K || !V || !out || !lse) return fail(RV_ERR_INVALID, "Q, K, V, out and lse are required");
+  if (saliency) {
+    rv_status st = check_qsub(qs, n_tokens);
+    if (st != RV_OK) return st;
+  }
+  return attend_impl(Q, K, V, n_tokens, n_tokens, memK, memV, mem_len, head_stride_tokens, n_heads, qs, out, lse,
+                     saliency, K, (int64_t)n_heads * rv::kHeadDim, rv::kHeadDim, (hipStream_t)stream);
+}
+
+rv_status rv_mem_stage(rv_mem m, int n_tokens, void** K_tail, void** V_tail, int64_t* head_stride_tokens,
+                       void* stream) {
+  if (!m) return fail(RV_ERR_INVALID, "memory is NULL");
+  if (n_tokens < 1 || n_tokens > rv::kMaxTokens)
+    return fail(RV_ERR_INVALID, "n_tokens must be in [1, %d] (got %d)", rv::kMaxTokens, n_tokens);
+  rv_status st = check_device(m);
+  if (st != RV_OK) return st;
+  {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    st = arena_reserve(m, m->len + n_tokens, (hipStream_t)stream);
+    if (st != RV_OK) return st;
+  }
+  if (K_tail) *K_tail = m->K + m->len * rv::kHeadDim;
+  if (V_tail) *V_tail = m->V + m->len * rv::kHeadDim;
+  if (head_stride_tokens) *head_stride_tokens = m->cap;
+  return RV_OK;
+}
+
+rv_status rv_mem_stage_frame(rv_mem m, const void* K, const void* V, int n_tokens, void* stream) {
+  if (!K || !V) return fail(RV_ERR_INVALID, "K and V are required");
+  rv_status st = rv_mem_stage(m, n_tokens, nullptr, nullptr, nullptr, stream);
+  if (st != RV_OK) return st;
+  RV_HIP(rv::launch_stage(m->K + m->len * rv::kHeadDim, m->V + m->len * rv::kHeadDim, m->cap,
+                          (const uint16_t*)K, (const uint16_t*)V, n_tokens, m->n_heads, (hipStream_t)stream),
+         "stage launch");
+  return RV_OK;
+}
+
+rv_status rv_attend_staged(const void* Q, int n_tokens, rv_mem m, const rv_qsub* qs, void* out, float* lse,
+                           float* saliency, void* stream) {
+  if (!m) return fail(RV_ERR_INVALID, "memory is NULL");
+  if (n_tokens < 1 || n_tokens > rv::kMaxTokens)
+    return fail(RV_ERR_INVALID, "n_tokens must be in [1, %d] (got %d)", rv::kMaxTokens, n_tokens);
+  if (!Q || !out || !lse) return fail(RV_ERR_INVALID, "Q, out and lse are required");
+  rv_status st = check_device(m);
+  if (st != RV_OK) return st;
+  if (m->cap < m->len + n_tokens)
+    return fail(RV_ERR_INVALID, "no staged frame: capacity %lld < length %lld + n_tokens %d (call rv_mem_stage)",
+                (long long)m->cap, (long long)m->len, n_tokens);
+  if (saliency) {
+    st = check_qsub(qs, n_tokens);
+    if (st != RV_OK) return st;
+  }
+  const uint16_t* kt = m->K + m->len * rv::kHeadDim;
+  const uint16_t* vt = m->V + m->len * rv::kHeadDim;
+  return attend_impl(Q, kt, vt, n_tokens, 0, m->K, m->V, m->len + n_tokens, m->cap, m->n_heads, qs, out, lse,
+                     saliency, kt, rv::kHeadDim, m->cap * rv::kHeadDim, (hipStream_t)stream);
 }
 
 rv_status rv_admit(const float* saliency, int budget, const void* K, const void* V, int n_tokens, rv_mem m,
@@ -614,6 +685,8 @@ rv_status rv_admit(const float* saliency, int budget, const void* K, const void*
   rv::AdmitArgs b{};
   b.layer[0].K = (const uint16_t*)K;
   b.layer[0].V = (const uint16_t*)V;
+  b.layer[0].kv_row = (int64_t)m->n_heads * rv::kHeadDim;
+  b.layer[0].kv_head = rv::kHeadDim;
   b.layer[0].sal = const_cast<float*>(saliency);
   b.layer[0].idx = idx_out;
   b.layer[0].memK = m->K;
@@ -638,12 +711,14 @@ rv_status rv_admit(const float* saliency, int budget, const void* K, const void*
 
 namespace {
 
+// staged: the frame's K, V are the rows each memory staged past its length (K, V
+// unused); the selected rows are compacted in place.
 rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K, const void* const* V,
                        const float* const* lse, int n_tokens, const rv_qsub* qs, int budget, const rv_mem* mems,
                        int frame_id, float* const* saliency_out, int32_t* const* idx_out, void* stream,
-                       bool shared) {
+                       bool shared, bool staged) {
   if (n_layers < 1 || n_layers > 4096) return fail(RV_ERR_INVALID, "n_layers must be in [1, 4096]");
-  if (!Q || !K || !V || !lse || !mems) return fail(RV_ERR_INVALID, "NULL pointer array");
+  if (!Q || (!staged && (!K || !V)) || !lse || !mems) return fail(RV_ERR_INVALID, "NULL pointer array");
   if (n_tokens < 1 || n_tokens > rv::kMaxTokens)
     return fail(RV_ERR_INVALID, "n_tokens must be in [1, %d] (got %d)", rv::kMaxTokens, n_tokens);
   if (budget < 0 || budget > n_tokens)
@@ -652,13 +727,15 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
   if (st != RV_OK) return st;
   const int H = mems[0] ? mems[0]->n_heads : 0;
   for (int l = 0; l < n_layers; ++l) {
-    if (!Q[l] || !K[l] || !V[l] || !lse[l] || !mems[l])
+    if (!Q[l] || (!staged && (!K[l] || !V[l])) || !lse[l] || !mems[l])
       return fail(RV_ERR_INVALID, "layer %d: NULL tensor or memory", l);
     if (mems[l]->n_heads != H) return fail(RV_ERR_INVALID, "layer %d: head count differs", l);
     st = check_device(mems[l]);
     if (st != RV_OK) return st;
     if (mems[l]->len + budget > mems[l]->max_tokens)
       return fail(RV_ERR_CAPACITY, "layer %d: memory would exceed max_tokens", l);
+    if (staged && mems[l]->cap < mems[l]->len + n_tokens)
+      return fail(RV_ERR_INVALID, "layer %d: no staged frame (call rv_mem_stage)", l);
   }
   hipStream_t s = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(g_ws_mu);
@@ -683,8 +760,8 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
     st = grow(&ws->sal, &ws->sal_floats, (size_t)chunk_layers * H * n_tokens, false, "saliency workspace");
     if (st != RV_OK) return st;
   }
-  // growth for every layer before anything is enqueued
-  for (int l = 0; l < n_layers; ++l) {
+  // growth for every layer before anything is enqueued (a staged memory has its room)
+  for (int l = 0; !staged && l < n_layers; ++l) {
     st = arena_reserve(mems[l], mems[l]->len + budget, s);
     if (st != RV_OK) return st;
   }
@@ -696,8 +773,17 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
       const int l = l0 + i;
       rv::AdmitLayer& L = b.layer[i];
       L.Q = (const uint16_t*)Q[l];
-      L.K = (const uint16_t*)K[l];
-      L.V = (const uint16_t*)V[l];
+      if (staged) {
+        L.K = mems[l]->K + mems[l]->len * rv::kHeadDim;
+        L.V = mems[l]->V + mems[l]->len * rv::kHeadDim;
+        L.kv_row = rv::kHeadDim;
+        L.kv_head = mems[l]->cap * rv::kHeadDim;
+      } else {
+        L.K = (const uint16_t*)K[l];
+        L.V = (const uint16_t*)V[l];
+        L.kv_row = (int64_t)H * rv::kHeadDim;
+        L.kv_head = rv::kHeadDim;
+      }
       L.lse = lse[l];
       L.sal = (saliency_out && saliency_out[l]) ? saliency_out[l] : ws->sal + (size_t)i * H * n_tokens;
       L.idx = idx_out ? idx_out[l] : nullptr;
@@ -710,6 +796,7 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
     b.n_heads = H;
     b.n_layers = nl;
     b.frame_id = frame_id;
+    b.in_place = staged ? 1 : 0;
     RV_HIP(rv::launch_admit(b, ws->max_lds, s), "admit_layers launch");
   }
   for (int l = 0; l < n_layers; ++l) mems[l]->len += budget;
@@ -725,7 +812,7 @@ rv_status rv_admit_layers(int n_layers, const void* const* Q, const void* const*
                           const rv_mem* mems, int frame_id, float* const* saliency_out,
                           int32_t* const* idx_out, void* stream) {
   return admit_layers(n_layers, Q, K, V, lse, n_tokens, qs, budget, mems, frame_id, saliency_out, idx_out,
-                      stream, false);
+                      stream, false, false);
 }
 
 rv_status rv_admit_layers_shared(int n_layers, const void* const* Q, const void* const* K, const void* const* V,
@@ -733,7 +820,14 @@ rv_status rv_admit_layers_shared(int n_layers, const void* const* Q, const void*
                                  const rv_mem* mems, int frame_id, float* const* saliency_out,
                                  int32_t* const* idx_out, void* stream) {
   return admit_layers(n_layers, Q, K, V, lse, n_tokens, qs, budget, mems, frame_id, saliency_out, idx_out,
-                      stream, true);
+                      stream, true, false);
+}
+
+rv_status rv_admit_staged_layers(int n_layers, const void* const* Q, const float* const* lse, int n_tokens,
+                                 const rv_qsub* qs, int budget, const rv_mem* mems, int frame_id,
+                                 float* const* saliency_out, int32_t* const* idx_out, void* stream) {
+  return admit_layers(n_layers, Q, nullptr, nullptr, lse, n_tokens, qs, budget, mems, frame_id, saliency_out,
+                      idx_out, stream, false, true);
 }
 
 }  // extern "C"

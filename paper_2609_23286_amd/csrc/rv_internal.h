@@ -34,7 +34,9 @@ struct AttnArgs {
   uint16_t* out;           // [N][H][64]
   float* lse;              // [H][N]
   float* part;             // partial slots, kAttnSlotFloats each
-  int n_tokens;
+  int n_tokens;            // queries (and, unless staged, the frame's keys)
+  int n_fkeys;             // keys of the frame segment: n_tokens, or 0 when the frame's
+                           // keys are staged in the arena and counted in mem_len
   int n_heads;
   int q_tiles;
   int nt_mem;              // key tiles of the memory segment
@@ -52,8 +54,10 @@ constexpr int kAttnSlotFloats = kAttnBQ * kHeadDim / 2 + 2 * kAttnBQ;  // bf16 r
 // One layer's share of the saliency / selection / append kernel.
 struct AdmitLayer {
   const uint16_t* Q;       // [N][H][64]   (saliency)
-  const uint16_t* K;       // [N][H][64]   (saliency, append)
-  const uint16_t* V;       // [N][H][64]   (append)
+  const uint16_t* K;       // frame keys: row j of head h at K + j * kv_row + h * kv_head
+  const uint16_t* V;       //   (saliency, append); V likewise (append)
+  int64_t kv_row;          // elements between a head's consecutive frame rows
+  int64_t kv_head;         // elements between heads' rows of one token
   const float* lse;        // [H][N]       (saliency)
   float* sal;              // [H][N]       written by saliency, read by selection
   int32_t* idx;            // [H][budget]  optional output
@@ -86,9 +90,15 @@ struct AdmitArgs {
   int stage_queries;       // saliency: stage the sampled query rows in LDS
   int sal_groups;          // saliency: workgroups per (layer, head)
   int shared_select;       // selection: one top-k per layer on the head sum, shared by all heads
+  int in_place;            // selection: K, V are the staged rows of the destination arena, so
+                           //   the append is an in-place compaction (read before write)
 };
 
 hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t s);
+// Copies a frame's K, V ([n][H][64] bf16) to staged arena rows: row j of head h goes to
+// dK / dV + (h * head_stride + j) * 64.
+hipError_t launch_stage(uint16_t* dK, uint16_t* dV, int64_t head_stride, const uint16_t* K, const uint16_t* V,
+                        int n, int H, hipStream_t s);
 // Records the hardware XCC id of each of n_blocks workgroups into ids (device memory).
 hipError_t launch_xcc_probe(int* ids, int n_blocks, hipStream_t s);
 // Dynamic LDS bytes the admission kernels need for these arguments (the larger of the

@@ -57,6 +57,10 @@ def _load():
         "rv_admit_layers": ([i32, P(vp), P(vp), P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp), vp], i32),
         "rv_admit_layers_shared": ([i32, P(vp), P(vp), P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp),
                                     vp], i32),
+        "rv_mem_stage": ([vp, i32, P(vp), P(vp), P(i64), vp], i32),
+        "rv_mem_stage_frame": ([vp, vp, vp, i32, vp], i32),
+        "rv_attend_staged": ([vp, i32, vp, P(rv_qsub), vp, vp, vp, vp], i32),
+        "rv_admit_staged_layers": ([i32, P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp), vp], i32),
         "rv_reserve_workspace": ([i32, i32, i32], i32),
         "rv_device_status": ([], i32),
     }
@@ -179,6 +183,21 @@ class Memory:
                                 ctypes.c_void_p(prov.data_ptr()), _stream(stream)))
         return K, V, prov
 
+    def stage(self, n_tokens, stream=None):
+        """rv_mem_stage: room for a frame of n_tokens rows past the valid ones; returns
+        (K_tail, V_tail, head_stride) device addresses / row stride."""
+        k, v, hs = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_int64()
+        _check(_lib.rv_mem_stage(self.handle, n_tokens, ctypes.byref(k), ctypes.byref(v), ctypes.byref(hs),
+                                 _stream(stream)))
+        return k.value, v.value, hs.value
+
+    def stage_frame(self, K, V, stream=None):
+        """rv_mem_stage_frame: stage a frame given as [N, H, 64] bf16 K, V tensors."""
+        N = K.shape[0]
+        shp = (N, self.n_heads, HEAD_DIM)
+        _check(_lib.rv_mem_stage_frame(self.handle, _ptr(K, shp, 2, "K"), _ptr(V, shp, 2, "V"), N,
+                                       _stream(stream)))
+
     def save(self, path):
         """Write a snapshot (rows and provenance) to `path`."""
         _check(_lib.rv_mem_save(self.handle, os.fsencode(path)))
@@ -216,6 +235,34 @@ def attend_frame(Q, K, V, mem, out, lse, saliency=None, qs=None, stream=None,
         ctypes.byref(q) if q is not None else None,
         _ptr(out, shp, 2, "out"), _ptr(lse, (H, N), 4, "lse"),
         _ptr(saliency, (H, N), 4, "saliency"), _stream(stream)))
+
+
+def attend_staged(Q, mem, out, lse, saliency=None, qs=None, stream=None):
+    """rv_attend_staged: attention of Q [N, H, 64] over mem's rows and its staged frame."""
+    N, H, d = Q.shape
+    q = qs if qs is None or isinstance(qs, rv_qsub) else rv_qsub(*qs)
+    _check(_lib.rv_attend_staged(
+        _ptr(Q, (N, H, d), 2, "Q"), N, mem.handle, ctypes.byref(q) if q is not None else None,
+        _ptr(out, (N, H, d), 2, "out"), _ptr(lse, (H, N), 4, "lse"), _ptr(saliency, (H, N), 4, "saliency"),
+        _stream(stream)))
+
+
+def admit_staged_layers(Q, lse, qs, budget, mems, frame_id, saliency_out=None, idx_out=None, stream=None):
+    """rv_admit_staged_layers over lists of per-layer Q [N, H, 64], lse [H, N] and Memory
+    objects whose frames are staged."""
+    L = len(mems)
+    N, H, d = Q[0].shape
+    arr = ctypes.c_void_p * L
+
+    def pack(ts, shape, itemsize, what):
+        return arr(*[_ptr(t, shape, itemsize, f"{what}[{i}]") for i, t in enumerate(ts)])
+
+    q = qs if isinstance(qs, rv_qsub) else rv_qsub(*qs)
+    sal = pack(saliency_out, (H, N), 4, "saliency_out") if saliency_out is not None else None
+    idx = pack(idx_out, (H, budget), 4, "idx_out") if idx_out is not None else None
+    _check(_lib.rv_admit_staged_layers(
+        L, pack(Q, (N, H, d), 2, "Q"), pack(lse, (H, N), 4, "lse"), N, ctypes.byref(q), budget,
+        arr(*[m.handle for m in mems]), frame_id, sal, idx, _stream(stream)))
 
 
 def admit(saliency, budget, K, V, mem, frame_id, idx_out=None, stream=None):

@@ -361,3 +361,105 @@ def test_query_downsampling_factors(rv, stride):
     assert (idx == oracle.topk(sal, budget)).all()
     check_index_sets(idx, sal_o, budget)
     mem.close()
+
+
+STAGED_CASES = [  # (N, H, M, budget): ragged tails, empty memory, tile-aligned and
+                  # unaligned memories, budgets whose selected rows overlap their
+                  # destinations during the in-place compaction
+    (1, 1, 0, 1), (65, 2, 0, 30), (130, 3, 257, 5), (300, 4, 200, 150), (300, 2, 64, 300),
+    (200, 2, 128, 199), (1041, 16, 1000, 10), (1041, 16, 1024, 10),
+]
+
+
+@pytest.mark.parametrize("N,H,M,budget", STAGED_CASES)
+def test_staged_frame_matches_oracle_and_frame_path(rv, N, H, M, budget):
+    """A frame staged in the arena (rv_mem_stage_frame, rv_attend_staged): out, LSE and
+    saliency within the oracle tolerances, and bit for bit the frame path's when M is a
+    multiple of 64.  rv_admit_staged_layers (in-place compaction) against rv_admit_layers
+    on the same LSE: saliency, selection, arena rows and provenance bit for bit."""
+    import torch
+    print(f"staged N={N} H={H} M={M} budget={budget}", flush=True)
+    L = 2
+    qs = qsub_for(N)
+    qidx = oracle.qsub_index(*qs)
+    staged_mems, frame_mems, Qs, Ks, Vs, lses = [], [], [], [], [], []
+    for l in range(L):
+        Q, K, V = frame(300 + l + N, N, H)
+        memK, memV = memory_rows(400 + l + M, H, M)
+        pair = []
+        for _ in range(2):
+            mem = rv.Memory(H, reserve_tokens=M + 3, max_tokens=M + N + 64)
+            if M:
+                mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+            pair.append(mem)
+        Qd, Kd, Vd = to_dev(Q), to_dev(K), to_dev(V)
+        out = torch.empty_like(Qd)
+        lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
+        sal = torch.empty((H, N), dtype=torch.float32, device="cuda")
+        pair[0].stage_frame(Kd, Vd)   # grows the arena (reserve was M + 3)
+        rv.attend_staged(Qd, pair[0], out, lse, sal, qs)
+        rv.device_status()
+        out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M)
+        sal_o = oracle.saliency(Q, K, lse_o, qidx)
+        out_h = bf16_to_f64(to_host_u16(out))
+        lse_h = lse.cpu().numpy().astype(np.float64)
+        sal_h = sal.cpu().numpy().astype(np.float64)
+        assert np.abs(out_h - out_o).max() <= OUT_ATOL
+        assert np.abs(lse_h - lse_o).max() <= LSE_ATOL
+        assert (np.abs(sal_h - sal_o) <= SAL_RTOL * sal_o).all()
+        if M % 64 == 0:
+            out_f = torch.empty_like(Qd)
+            lse_f = torch.empty_like(lse)
+            sal_f = torch.empty_like(sal)
+            rv.attend_frame(Qd, Kd, Vd, pair[1], out_f, lse_f, sal_f, qs)
+            torch.cuda.synchronize()
+            assert (out_f == out).all() and (lse_f == lse).all() and (sal_f == sal).all()
+        staged_mems.append(pair[0]); frame_mems.append(pair[1])
+        Qs.append(Qd); Ks.append(Kd); Vs.append(Vd); lses.append(lse)
+    res = []
+    for staged in (True, False):
+        sals = [torch.empty((H, N), dtype=torch.float32, device="cuda") for _ in range(L)]
+        idxs = [torch.empty((H, budget), dtype=torch.int32, device="cuda") for _ in range(L)]
+        if staged:
+            rv.admit_staged_layers(Qs, lses, qs, budget, staged_mems, 7, sals, idxs)
+            mems = staged_mems
+        else:
+            rv.admit_layers(Qs, Ks, Vs, lses, qs, budget, frame_mems, 7, sals, idxs)
+            mems = frame_mems
+        rv.device_status()
+        res.append(([x.cpu() for x in sals], [x.cpu() for x in idxs], [m.read() for m in mems],
+                    [m.len for m in mems]))
+    for l in range(L):
+        assert (res[0][0][l] == res[1][0][l]).all()
+        assert (res[0][1][l] == res[1][1][l]).all()
+        assert res[0][3][l] == res[1][3][l] == M + budget
+        assert all((x == y).all() for x, y in zip(res[0][2][l], res[1][2][l]))
+    # the compacted rows are the selected frame rows (layer 0)
+    Q, K, V = frame(300 + N, N, H)
+    Kr, Vr, prov = res[0][2][0]
+    sel = res[0][1][0].numpy()
+    for h in range(H):
+        assert (Kr[h, M:].numpy().view(np.uint16) == K[sel[h], h]).all()
+        assert (Vr[h, M:].numpy().view(np.uint16) == V[sel[h], h]).all()
+        assert (prov[h, M:, 0].numpy() == 7).all() and (prov[h, M:, 1].numpy() == sel[h]).all()
+    for m in staged_mems + frame_mems:
+        m.close()
+
+
+def test_staged_calls_need_a_staged_frame(rv):
+    """rv_attend_staged / rv_admit_staged_layers refuse a memory with no room staged."""
+    import torch
+    H, N = 2, 64
+    mem = rv.Memory(H, reserve_tokens=0, max_tokens=1000)
+    Q = torch.zeros((N, H, 64), dtype=torch.int16, device="cuda")
+    out = torch.empty_like(Q)
+    lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
+    with pytest.raises(rv.RVError) as e:
+        rv.attend_staged(Q, mem, out, lse)
+    assert e.value.status == rv.RV_ERR_INVALID
+    with pytest.raises(rv.RVError):
+        rv.admit_staged_layers([Q], [lse], (1, N, 0, 2), 1, [mem], 0)
+    assert mem.len == 0
+    k, v, hs = mem.stage(N)
+    assert k and v and hs >= N and mem.len == 0
+    mem.close()
