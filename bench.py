@@ -271,6 +271,10 @@ def main():
     p.add_argument("--gamma", type=float, default=None, help="retention rate: budget = floor(gamma N)")
     p.add_argument("--shared", action="store_true",
                    help="head-averaged selection (one top-k per layer) instead of head-specific")
+    p.add_argument("--staged", action="store_true",
+                   help="stage each frame's K/V in the memory arenas (rv_mem_stage_frame, timed as its "
+                        "own phase), attend over the contiguous arena (rv_attend_staged) and admit by "
+                        "in-place compaction (rv_admit_staged_layers)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run a 256 MiB device copy before the stream (HBM counter calibration)")
@@ -304,6 +308,8 @@ def main():
     anchor = args.policy == "paper"
     regulated = [l for l in range(L) if args.policy == "all" or 10 <= l <= 16]
     admit_fn = "rv_admit_layers_shared" if args.shared else "rv_admit_layers"
+    if args.staged and args.shared:
+        raise SystemExit("--staged supports head-specific selection only")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -333,7 +339,7 @@ def main():
     log(f"generated {T} frames in {time.perf_counter() - t0:.1f} s")
 
     base = (N if anchor else 0) + cfg.prefill
-    cap = base + T * k + 64
+    cap = base + T * k + 64 + (N if args.staged else 0)
     mems = [rv.Memory(H, reserve_tokens=cap, max_tokens=cap) for _ in range(L)]
 
     def prefill():
@@ -386,22 +392,39 @@ def main():
 
     def run_frame(t, ev=None):
         qp, kp, vpp, qa, ka, va = frame_ptrs[t]
+        if args.staged:  # the producer's part: the frame's K/V into each arena's tail
+            if ev is not None:
+                ev[3].record(stream)
+            for l in range(L):
+                st = lib.rv_mem_stage_frame(mems[l].handle, vp(kp[l]), vp(vpp[l]), N, s_h)
+                if st:
+                    raise rv.RVError(st, lib.rv_last_error().decode())
         if ev is not None:
             ev[0].record(stream)
         for l in range(L):
-            mk, mv, hs = views[l]
-            st = lib.rv_attend_frame(vp(qp[l]), vp(kp[l]), vp(vpp[l]), N, vp(mk), vp(mv),
-                                     lib.rv_mem_len(mems[l].handle), hs, H, d, None, out_p[l], lse_p[l],
-                                     None, s_h)
+            if args.staged:
+                st = lib.rv_attend_staged(vp(qp[l]), N, mems[l].handle, None, out_p[l], lse_p[l], None, s_h)
+            else:
+                mk, mv, hs = views[l]
+                st = lib.rv_attend_frame(vp(qp[l]), vp(kp[l]), vp(vpp[l]), N, vp(mk), vp(mv),
+                                         lib.rv_mem_len(mems[l].handle), hs, H, d, None, out_p[l], lse_p[l],
+                                         None, s_h)
             if st:
                 raise rv.RVError(st, lib.rv_last_error().decode())
         if ev is not None:
             ev[1].record(stream)
         if anchor and t == 0:  # the global anchor: the first frame whole, in every layer (Eq. 4)
-            st = admit(L, qa, ka, va, lse_arr, N, qref, N, mem_arr, t, sal_arr, None, s_h)
+            if args.staged:
+                st = lib.rv_admit_staged_layers(L, qa, lse_arr, N, qref, N, mem_arr, t, sal_arr, None, s_h)
+            else:
+                st = admit(L, qa, ka, va, lse_arr, N, qref, N, mem_arr, t, sal_arr, None, s_h)
         elif regulated and k > 0:
             rq, rk, rvv = reg_frames[t]
-            st = admit(len(regulated), rq, rk, rvv, reg_lse, N, qref, k, reg_mem, t, reg_sal, None, s_h)
+            if args.staged:
+                st = lib.rv_admit_staged_layers(len(regulated), rq, reg_lse, N, qref, k, reg_mem, t, reg_sal,
+                                                None, s_h)
+            else:
+                st = admit(len(regulated), rq, rk, rvv, reg_lse, N, qref, k, reg_mem, t, reg_sal, None, s_h)
         else:
             st = 0
         if st:
@@ -415,7 +438,7 @@ def main():
     torch.cuda.synchronize()
     prefill()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(T)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(T)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for t in range(T):
@@ -443,6 +466,7 @@ def main():
             f"admission {events[f][1].elapsed_time(events[f][2]) * 1e3:.1f} us")
     attn_ms = sum(e[0].elapsed_time(e[1]) for e in events)
     admit_ms = sum(e[1].elapsed_time(e[2]) for e in events)
+    stage_ms = sum(e[3].elapsed_time(e[0]) for e in events) if args.staged else None
     flops = sum(attention_flops(N, H, d, mem_len(l, t) + N) for t in range(T) for l in range(L))
     n_attn = T * L
     attn_avg_s = attn_ms / 1e3 / n_attn
@@ -464,6 +488,9 @@ def main():
         variant.append(f"gamma {args.gamma}")
     if args.shared:
         variant.append("head-averaged selection")
+    if args.staged:
+        variant.append("frames staged in the arenas by a copy kernel (timed as staging_ms, inside the "
+                       "wall clock), attention over the contiguous arena, admission by in-place compaction")
     workload = (f"{cfg.name}: {L} layers x {H} heads x {d}, {N} tokens/frame ({cfg.grid_h}x{cfg.grid_w} "
                 f"patches + {cfg.n_special} special), budget {k}/head/frame, {stride}x{stride} query sampling, "
                 f"{T}-frame stream from " + (f"{cfg.prefill} prefilled memory rows" if cfg.prefill else "empty memory")
@@ -487,6 +514,7 @@ def main():
                    "budget": k, "frames": T, "sampled_queries": n_q, "query_window": stride,
                    "regulated_layers": len(regulated), "anchor": anchor,
                    "selection": "head-averaged" if args.shared else "head-specific",
+                   "staged_frames": bool(args.staged),
                    "prefill_rows": cfg.prefill},
         "roofline": {"kernel": "attn_fwd_kernel (+ attn_merge_kernel on split plans)", "bound": "mfma",
                      "achieved": achieved_tf,
@@ -494,7 +522,7 @@ def main():
                      "traffic": attention_traffic(wkey) if wkey else None,
                      "avg_launch_us": attn_avg_s * 1e6,
                      "algorithmic_flops_per_launch": flops / n_attn},
-        "phases": {"attention_ms": attn_ms, "admission_ms": admit_ms,
+        "phases": {"attention_ms": attn_ms, "admission_ms": admit_ms, "staging_ms": stage_ms,
                    "admission_roofline": {"kernel": "sal_kernel + select_kernel", "bound": "hbm",
                                           "achieved": admit_gbs,
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
