@@ -474,10 +474,13 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
 // workgroups (32 rows each) merge the partial results (the kernel boundary makes them
 // visible on every XCD).
 __global__ __launch_bounds__(kAttnThreads) void attn_merge_kernel(AttnArgs a) {
-  const int unit = blockIdx.x / (BQ / kMergeRows), rb = blockIdx.x % (BQ / kMergeRows);
-  int q = 0;
-  while (q + 1 < a.n_queues && unit >= a.unit_base[q + 1]) ++q;
-  const int ui = unit - a.unit_base[q];
+  // Workgroup b merges for queue b % n_queues, like the forward workgroups that wrote
+  // the partials (a locality heuristic: the partials may still be in that XCD's L2).
+  const int q = (int)(blockIdx.x % (unsigned)a.n_queues);
+  const int j = (int)(blockIdx.x / (unsigned)a.n_queues);
+  const int ui = j / (BQ / kMergeRows), rb = j % (BQ / kMergeRows);
+  if (ui >= a.unit_base[q + 1] - a.unit_base[q]) return;
+  const int unit = a.unit_base[q] + ui;
   const int c_first = (int)(((int64_t)ui * a.U) / a.E);
   const int c_last = (int)(((int64_t)ui * a.U + a.T - 1) / a.E);
   if (c_first == c_last) return;  // written whole by its only chunk
@@ -494,7 +497,10 @@ hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t
   hipLaunchKernelGGL(attn_fwd_kernel, dim3(grid), dim3(kAttnThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !merge) return e;
-  hipLaunchKernelGGL(attn_merge_kernel, dim3(a.n_units * (BQ / kMergeRows)), dim3(kAttnThreads), 0, s, a);
+  int max_units = 0;
+  for (int q = 0; q < a.n_queues; ++q) max_units = max(max_units, a.unit_base[q + 1] - a.unit_base[q]);
+  hipLaunchKernelGGL(attn_merge_kernel, dim3(a.n_queues * max_units * (BQ / kMergeRows)), dim3(kAttnThreads), 0,
+                     s, a);
   return hipGetLastError();
 }
 
