@@ -8,8 +8,8 @@
 // Design (CDNA4):
 // * Work unit = (head, 128-query tile); 4 wave64s, 32 queries each.  Key/value tiles of
 //   64 rows go straight from global memory into LDS (global_load_lds_dwordx4), row-major
-//   with an XOR swizzle, double-buffered: the next tile streams in while the current
-//   one is computed.
+//   with an XOR swizzle, through a 4-stage ring whose stage offsets are compile-time
+//   constants: two tiles are computed per barrier while the next two stream in.
 // * Scores are formed transposed, S^T = K Q^T (v_mfma_f32_32x32x16_bf16), so each lane
 //   owns one query column: softmax max/sum are in-lane plus one exchange between the
 //   two 32-lane halves sharing a query.  The output is accumulated transposed too,
@@ -29,10 +29,12 @@
 //   U = k E >= T every unit is cut into k aligned pieces, so the workgroups holding the
 //   query tiles of one head walk the same key tiles at the same time and share them in
 //   L2.  A chunk that covers a whole unit writes its output directly; otherwise it
-//   writes a partial result (unnormalised O, reference m, row sum l) to its slot and a
-//   second launch merges each split unit's partials in chunk order (deterministic; the
-//   kernel boundary is the only synchronisation, so results do not depend on where
-//   the hardware places the workgroups).
+//   writes a partial result (its output normalised by its own row sum, in bf16, with
+//   its reference m and row sum l) to its slot and a second launch merges each split
+//   unit's partials in chunk order (deterministic; the kernel boundary is the only
+//   synchronisation, so results do not depend on where the hardware places the
+//   workgroups; the merge workgroups follow the queues' XCD mapping only so that the
+//   partials are likely still in that XCD's L2).
 #include "rv_internal.h"
 
 namespace rv {
