@@ -63,11 +63,20 @@ def admit_bytes(N, H, d, n_q, k):
             + k * H * 8)             # provenance
 
 
+def _code_only(text):
+    """Source text without comments and whitespace (so that editing a comment does not
+    mark recorded counters stale)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return re.sub(r"\s+", "", text)
+
+
 def kernel_source_hash(kernel):
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(CSRC, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(CSRC, f), encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
@@ -174,8 +183,9 @@ def summarize_pmc(fetch_dir, write_dir, workload):
             f"- hbm_bytes_per_launch: {total:.0f}",
             f"- source_hash: {kernel_source_hash(kernel)}",
             "",
-            "The source hash covers " + ", ".join(KERNEL_SOURCES[kernel]) + "; the benchmark",
-            "reports this traffic only while those files are unchanged.",
+            "The source hash covers the code (comments and whitespace removed) of "
+            + ", ".join(KERNEL_SOURCES[kernel]) + "; the benchmark",
+            "reports this traffic only while that code is unchanged.",
         ]
         path = traffic_path(kernel, workload)
         with open(path, "w") as fh:
