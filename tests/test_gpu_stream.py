@@ -146,6 +146,41 @@ def test_full_size_frame_sampled_rows(rv, name, layer, M):
     mem.close()
 
 
+def test_largest_frame_sampled_rows(rv):
+    """The largest frame the boundary accepts (16384 tokens, a 128 x 128 grid, 2 heads)
+    over a 3000-row memory: the 4096 sampled queries do not fit the saliency
+    workgroup's LDS (rows read from memory), the budget of 163 takes the radix
+    selection, and the key range spans 304 tiles.  Sampled rows against the oracle."""
+    import torch
+    H, N, M, k = 2, 16384, 3000, 163
+    print(f"largest frame N={N} H={H} M={M} budget={k}", flush=True)
+    qs = (128, 128, 0, 2)
+    qidx = oracle.qsub_index(*qs)
+    Q, K, V = (synth.normal_bf16(77, 0, 0, tag, (N, H, 64), 0.125) for tag in range(3))
+    memK = synth.normal_bf16(78, 1, 0, synth.TAG_MEMK, (H, M, 64), 0.125)
+    memV = synth.normal_bf16(78, 1, 0, synth.TAG_MEMV, (H, M, 64), 0.125)
+    mem = rv.Memory(H, reserve_tokens=M + k, max_tokens=M + k)
+    mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+    out, lse, sal, idx = gpu_frame_step(rv, mem, Q, K, V, qs, k, 3)
+
+    rng = np.random.default_rng(5)
+    extra = rng.choice(N, 48, replace=False)
+    edge = [0, 1, 63, 64, 127, 128, N - 65, N - 64, N - 2, N - 1]
+    rows = np.unique(np.concatenate([qidx, extra, np.array(edge)])).astype(np.int32)
+    out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M, rows=rows)
+    assert np.abs(out[rows] - out_o).max() <= OUT_ATOL
+    assert np.abs(lse[:, rows] - lse_o).max() <= LSE_ATOL
+    pos = np.searchsorted(rows, qidx)
+    sal_o = oracle.column_mass(Q, qidx, lse_o[:, pos], K, "frame")
+    assert (np.abs(sal - sal_o) <= SAL_RTOL * sal_o).all()
+    assert (idx == oracle.topk(sal, k)).all()
+    check_index_sets(idx, sal_o, k)
+    mk, mv, _ = (x.numpy().view(np.uint16) if x.dtype != torch.int32 else x.numpy() for x in mem.read())
+    for h in range(H):
+        assert (mk[h, M:] == K[idx[h], h]).all() and (mv[h, M:] == V[idx[h], h]).all()
+    mem.close()
+
+
 def test_layer_policy_stream(rv):
     """The paper's layer partition (Sec. 3.3 Eq. 4-5, Sec. 4.1): the first frame is kept
     whole in every layer (global anchor); afterwards only the regulated layers admit
