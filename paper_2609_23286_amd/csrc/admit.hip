@@ -37,7 +37,7 @@ constexpr int NT = kAdmitThreads;  // 256
 constexpr int NW = NT / 64;
 constexpr int kBlocksPerStep = 2;  // 32-key blocks a saliency wave holds at once
 constexpr int QS_STRIDE = D + 8;   // staged sampled-query rows, 144 bytes
-constexpr int kStageBatch = 12;    // 16-byte query-row loads in flight per thread
+constexpr int kStageBatch = 9;     // 16-byte query-row loads in flight per thread (one pass of 288 rows)
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kScaleLog2 = kLog2e * 0.125f;
 
@@ -45,7 +45,7 @@ static_assert(NT == 256, "the radix histogram has one bin per thread");
 
 // ---- saliency -----------------------------------------------------------------------
 
-__global__ __launch_bounds__(NT) void sal_kernel(AdmitArgs a) {
+__global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int H = a.n_heads, N = a.n_tokens, tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -63,15 +63,16 @@ __global__ __launch_bounds__(NT) void sal_kernel(AdmitArgs a) {
   uint16_t* s_q = a.stage_queries ? reinterpret_cast<uint16_t*>(smem + (size_t)nq_pad * 4) : nullptr;
 
   // LSE of the sampled queries in log2 units (padding rows: +inf -> weight 0) and, when
-  // they fit, the sampled query rows (padding rows zero).  Loads are issued in batches
-  // of kStageBatch per thread before any is stored, so a batch costs one round trip.
+  // they fit, the sampled query rows (padding rows zero), a pass of q_pass rows at a
+  // time.  Loads are issued in batches of kStageBatch per thread before any is stored,
+  // so a batch costs one round trip.
   auto q_token = [&](int i) {
     const int qi = i / a.q_cols;
     return a.q_base + qi * a.q_row_stride + (i - qi * a.q_cols) * a.q_col_stride;
   };
   // K rows (B operands, K^T) of a step's blocks: lane's key, dims ds*16 + half*8 ..;
-  // the first step's rows are requested before the staging, each next step's rows
-  // while the current step computes.
+  // a pass's first step's rows are requested before its staging, each next step's
+  // rows while the current step computes.
   auto load_k = [&](int bb, bf16x8 (&kf)[kBlocksPerStep][4]) {
 #pragma unroll
     for (int b = 0; b < kBlocksPerStep; ++b) {
@@ -82,8 +83,7 @@ __global__ __launch_bounds__(NT) void sal_kernel(AdmitArgs a) {
     }
   };
   bf16x8 kf[kBlocksPerStep][4], kn[kBlocksPerStep][4];
-  int bb = blk0 + wave * kBlocksPerStep;
-  if (bb < blk1) load_k(bb, kf);
+  if (blk0 + wave * kBlocksPerStep < blk1) load_k(blk0 + wave * kBlocksPerStep, kf);
 
   for (int i0 = 0; i0 < nq_pad; i0 += NT * 4) {
     float v[4];
@@ -98,23 +98,6 @@ __global__ __launch_bounds__(NT) void sal_kernel(AdmitArgs a) {
       if (i < nq_pad) s_lse2[i] = v[u] * kLog2e;
     }
   }
-  if (s_q) {
-    for (int c0 = 0; c0 < nq_pad * 8; c0 += NT * kStageBatch) {
-      uint4 v[kStageBatch];
-#pragma unroll
-      for (int u = 0; u < kStageBatch; ++u) {
-        const int c = c0 + u * NT + tid, i = c >> 3, ch = c & 7;
-        v[u] = uint4{0u, 0u, 0u, 0u};
-        if (i < a.n_q) v[u] = *reinterpret_cast<const uint4*>(L.Q + ((int64_t)q_token(i) * H + h) * D + ch * 8);
-      }
-#pragma unroll
-      for (int u = 0; u < kStageBatch; ++u) {
-        const int c = c0 + u * NT + tid, i = c >> 3, ch = c & 7;
-        if (i < nq_pad) *reinterpret_cast<uint4*>(&s_q[i * QS_STRIDE + ch * 8]) = v[u];
-      }
-    }
-  }
-  __syncthreads();
 
   // Query row of sampled query qa for the A operand when the rows are not staged.
   auto q_global = [&](int qa) -> const uint16_t* {
@@ -124,55 +107,89 @@ __global__ __launch_bounds__(NT) void sal_kernel(AdmitArgs a) {
     return L.Q + ((int64_t)tok * H + h) * D + half * 8;
   };
 
-  for (; bb < blk1; bb += NW * kBlocksPerStep) {
-    const int nb = min(kBlocksPerStep, blk1 - bb);
-    if (bb + NW * kBlocksPerStep < blk1) load_k(bb + NW * kBlocksPerStep, kn);
-    float acc[kBlocksPerStep] = {};
-    for (int qb = 0; qb < nq_pad; qb += 32) {
-      bf16x8 qf[4];
-      if (s_q) {
+  // Passes over the sampled queries; each key's sum is carried from pass to pass by the
+  // lane that owns it (fixed order).
+  const int q_pass = s_q ? a.q_pass : nq_pad;
+  for (int p0 = 0; p0 < nq_pad; p0 += q_pass) {
+    const int p1 = min(nq_pad, p0 + q_pass);
+    if (p0 > 0 && blk0 + wave * kBlocksPerStep < blk1) load_k(blk0 + wave * kBlocksPerStep, kf);
+    if (s_q) {
+      const int rows = p1 - p0;
+      for (int c0 = 0; c0 < rows * 8; c0 += NT * kStageBatch) {
+        uint4 v[kStageBatch];
 #pragma unroll
-        for (int ds = 0; ds < 4; ++ds)
-          qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[(qb + l32) * QS_STRIDE + ds * 16 + half * 8]);
-      } else {
-        const uint16_t* qp = q_global(qb + l32);
+        for (int u = 0; u < kStageBatch; ++u) {
+          const int c = c0 + u * NT + tid, i = p0 + (c >> 3), ch = c & 7;
+          v[u] = uint4{0u, 0u, 0u, 0u};
+          if (c < rows * 8 && i < a.n_q)
+            v[u] = *reinterpret_cast<const uint4*>(L.Q + ((int64_t)q_token(i) * H + h) * D + ch * 8);
+        }
 #pragma unroll
-        for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
+        for (int u = 0; u < kStageBatch; ++u) {
+          const int c = c0 + u * NT + tid, ch = c & 7;
+          if (c < rows * 8) *reinterpret_cast<uint4*>(&s_q[(c >> 3) * QS_STRIDE + ch * 8]) = v[u];
+        }
       }
-      // LSE of this lane's 16 accumulator rows: queries qb + 8*(r/4) + 4*half + r%4
-      float l2[16];
+    }
+    __syncthreads();
+
+    for (int bb = blk0 + wave * kBlocksPerStep; bb < blk1; bb += NW * kBlocksPerStep) {
+      const int nb = min(kBlocksPerStep, blk1 - bb);
+      if (bb + NW * kBlocksPerStep < blk1) load_k(bb + NW * kBlocksPerStep, kn);
+      float acc[kBlocksPerStep] = {};
+      for (int qb = p0; qb < p1; qb += 32) {
+        bf16x8 qf[4];
+        if (s_q) {
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const float4 v = *reinterpret_cast<const float4*>(&s_lse2[qb + 8 * r4 + 4 * half]);
-        l2[4 * r4] = v.x;
-        l2[4 * r4 + 1] = v.y;
-        l2[4 * r4 + 2] = v.z;
-        l2[4 * r4 + 3] = v.w;
+          for (int ds = 0; ds < 4; ++ds)
+            qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[(qb - p0 + l32) * QS_STRIDE + ds * 16 + half * 8]);
+        } else {
+          const uint16_t* qp = q_global(qb + l32);
+#pragma unroll
+          for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
+        }
+        // LSE of this lane's 16 accumulator rows: queries qb + 8*(r/4) + 4*half + r%4
+        float l2[16];
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const float4 v = *reinterpret_cast<const float4*>(&s_lse2[qb + 8 * r4 + 4 * half]);
+          l2[4 * r4] = v.x;
+          l2[4 * r4 + 1] = v.y;
+          l2[4 * r4 + 2] = v.z;
+          l2[4 * r4 + 3] = v.w;
+        }
+#pragma unroll
+        for (int b = 0; b < kBlocksPerStep; ++b) {
+          f32x16 z = {};
+#pragma unroll
+          for (int ds = 0; ds < 4; ++ds) z = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z, 0, 0, 0);
+          float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) {
+            s0 += __builtin_amdgcn_exp2f(fmaf(z[r], kScaleLog2, -l2[r]));
+            s1 += __builtin_amdgcn_exp2f(fmaf(z[r + 1], kScaleLog2, -l2[r + 1]));
+          }
+          acc[b] += s0 + s1;
+        }
       }
 #pragma unroll
       for (int b = 0; b < kBlocksPerStep; ++b) {
-        f32x16 z = {};
-#pragma unroll
-        for (int ds = 0; ds < 4; ++ds) z = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z, 0, 0, 0);
-        float s0 = 0.f, s1 = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-          s0 += __builtin_amdgcn_exp2f(fmaf(z[r], kScaleLog2, -l2[r]));
-          s1 += __builtin_amdgcn_exp2f(fmaf(z[r + 1], kScaleLog2, -l2[r + 1]));
+        const float tot = acc[b] + __shfl_xor(acc[b], 32);
+        const int j = (bb + b) * 32 + l32;
+        if (b < nb && half == 0 && j < N) {
+          float* sp = L.sal + (int64_t)h * N + j;
+          if (p0 == 0)  // uniform
+            *sp = tot;
+          else
+            *sp += tot;
         }
-        acc[b] += s0 + s1;
       }
+#pragma unroll
+      for (int b = 0; b < kBlocksPerStep; ++b)
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds) kf[b][ds] = kn[b][ds];
     }
-#pragma unroll
-    for (int b = 0; b < kBlocksPerStep; ++b) {
-      const float tot = acc[b] + __shfl_xor(acc[b], 32);
-      const int j = (bb + b) * 32 + l32;
-      if (b < nb && half == 0 && j < N) L.sal[(int64_t)h * N + j] = tot;
-    }
-#pragma unroll
-    for (int b = 0; b < kBlocksPerStep; ++b)
-#pragma unroll
-      for (int ds = 0; ds < 4; ++ds) kf[b][ds] = kn[b][ds];
+    if (p1 < nq_pad) __syncthreads();  // the staged rows are replaced by the next pass
   }
 }
 
@@ -368,15 +385,15 @@ __device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx
 
 // Head-specific retention (the paper's rule, Sec. 3.3): one workgroup per (layer, head)
 // ranks that head's saliency.  Shared selection (the arm without head-specific
-// retention in the ablation of Sec. 4.5, Table 4): one workgroup per layer ranks the
-// sum over heads of the saliencies (summed in head order; it orders tokens as the mean
-// does) and every head admits the same tokens.
+// retention in the ablation of Sec. 4.5, Table 4): every head's workgroup ranks the sum
+// over heads of the saliencies (summed in head order, so every workgroup of a layer
+// reaches the same selection; it orders tokens as the mean does) and appends those
+// tokens to its own head.
 __global__ __launch_bounds__(NT) void select_kernel(AdmitArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   __shared__ uint64_t s_cand[NW * kWaveTopK];
   const int H = a.n_heads, N = a.n_tokens, k = a.budget, tid = threadIdx.x;
-  const int per_layer = a.shared_select ? 1 : H;
-  const int layer = blockIdx.x / per_layer, h_own = blockIdx.x - layer * per_layer;
+  const int layer = blockIdx.x / H, h_own = blockIdx.x - layer * H;
   const AdmitLayer& L = a.layer[layer];
   float* s_sal = reinterpret_cast<float*>(smem);
   int32_t* s_idx = reinterpret_cast<int32_t*>(smem + (((size_t)N * 4 + 15) & ~(size_t)15));
@@ -401,8 +418,8 @@ __global__ __launch_bounds__(NT) void select_kernel(AdmitArgs a) {
     select_small(s_sal, N, k, s_idx, s_cand);
   else
     select_topk(s_sal, N, k, s_idx);
-  const int h0 = a.shared_select ? 0 : h_own, h1 = a.shared_select ? H : h_own + 1;
-  for (int h = h0; h < h1; ++h) {
+  {
+    const int h = h_own;
     if (L.idx)
       for (int r = tid; r < k; r += NT) L.idx[(int64_t)h * k + r] = s_idx[r];
     // 16-byte chunks: 8 per K row, 8 per V row.
@@ -450,7 +467,7 @@ __global__ __launch_bounds__(NT) void select_kernel(AdmitArgs a) {
 
 size_t sal_lds_bytes(const AdmitArgs& a) {
   const size_t nq_pad = (size_t)((a.n_q + 31) & ~31);
-  return nq_pad * 4 + (a.stage_queries ? nq_pad * QS_STRIDE * 2 : 0);
+  return nq_pad * 4 + (a.stage_queries ? (size_t)a.q_pass * QS_STRIDE * 2 : 0);
 }
 
 size_t select_lds_bytes(const AdmitArgs& a) {
@@ -482,7 +499,20 @@ void plan_saliency(AdmitArgs* a, int n_lh, int n_cus, int max_lds) {
   const int max_groups = n_blocks / NW > 1 ? n_blocks / NW : 1;
   int g = (3 * n_cus + n_lh - 1) / (n_lh > 0 ? n_lh : 1);
   a->sal_groups = g < 1 ? 1 : (g > max_groups ? max_groups : g);
-  a->stage_queries = 1;
+  // Sampled query rows are staged in passes of q_pass rows, sized so that three
+  // workgroups fit a CU's LDS; the pass size depends only on n_q and the device, so
+  // every launch of the same frame shape sums in the same order.
+  const int nq_pad = (a->n_q + 31) & ~31;
+  const long budget_lds = (long)max_lds / 3 - kAdmitStaticLdsMargin - (long)nq_pad * 4;
+  const int fit = budget_lds > 0 ? (int)(budget_lds / (QS_STRIDE * 2)) & ~31 : 0;
+  if (fit >= 32) {
+    const int passes = (nq_pad + fit - 1) / fit;
+    a->q_pass = ((nq_pad + passes - 1) / passes + 31) & ~31;
+    a->stage_queries = 1;
+  } else {
+    a->q_pass = nq_pad;
+    a->stage_queries = 0;
+  }
   if (sal_lds_bytes(*a) > (size_t)admit_max_dynamic_lds(max_lds)) a->stage_queries = 0;
 }
 
@@ -500,7 +530,7 @@ hipError_t launch_admit(const AdmitArgs& a, int max_lds, hipStream_t s) {
   if ((a.mode & kModeSelect) && a.budget > 0) {
     hipError_t e = set_lds_limit((const void*)select_kernel, &sel_attr, limit);
     if (e != hipSuccess) return e;
-    const unsigned grid = (unsigned)(a.n_layers * (a.shared_select ? 1 : a.n_heads));
+    const unsigned grid = (unsigned)(a.n_layers * a.n_heads);
     hipLaunchKernelGGL(select_kernel, dim3(grid), dim3(NT), select_lds_bytes(a), s, a);
     return hipGetLastError();
   }

@@ -88,6 +88,7 @@ struct AdmitArgs {
   int frame_id;
   int mode;
   int stage_queries;       // saliency: stage the sampled query rows in LDS
+  int q_pass;              // saliency: sampled query rows staged per pass (multiple of 32)
   int sal_groups;          // saliency: workgroups per (layer, head)
   int shared_select;       // selection: one top-k per layer on the head sum, shared by all heads
   int in_place;            // selection: K, V are the staged rows of the destination arena, so
