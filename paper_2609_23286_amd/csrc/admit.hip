@@ -45,22 +45,31 @@ static_assert(NT == 256, "the radix histogram has one bin per thread");
 
 // ---- saliency -----------------------------------------------------------------------
 
-__global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+// The two query-row sources are separate instantiations, so that neither path's
+// memory waits are merged into the other's loop.
+template <bool kStaged>
+__device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem) {
   const int H = a.n_heads, N = a.n_tokens, tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
   const int groups = a.sal_groups;
   const int lh = blockIdx.x / groups, g = blockIdx.x - lh * groups;
   const int layer = lh / H, h = lh - layer * H;
-  const AdmitLayer& L = a.layer[layer];
   const int n_blocks = (N + 31) / 32;
   const int per_group = (n_blocks + groups - 1) / groups;
   const int blk0 = g * per_group, blk1 = min(n_blocks, blk0 + per_group);
   if (blk0 >= blk1) return;  // uniform over the workgroup
+  // The layer's operands, read once: this head's frame keys, query rows, LSE and
+  // saliency row.
+  const AdmitLayer& L = a.layer[layer];
+  const int64_t kv_row = L.kv_row;
+  const uint16_t* Kh = L.K + (int64_t)h * L.kv_head;
+  const uint16_t* Qh = L.Q + (int64_t)h * D;
+  const float* lse_h = L.lse + (int64_t)h * N;
+  float* sal_h = L.sal + (int64_t)h * N;
   const int nq_pad = (a.n_q + 31) & ~31;
   float* s_lse2 = reinterpret_cast<float*>(smem);
-  uint16_t* s_q = a.stage_queries ? reinterpret_cast<uint16_t*>(smem + (size_t)nq_pad * 4) : nullptr;
+  uint16_t* s_q = reinterpret_cast<uint16_t*>(smem + (size_t)nq_pad * 4);
 
   // LSE of the sampled queries in log2 units (padding rows: +inf -> weight 0) and, when
   // they fit, the sampled query rows (padding rows zero), a pass of q_pass rows at a
@@ -77,7 +86,7 @@ __global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
 #pragma unroll
     for (int b = 0; b < kBlocksPerStep; ++b) {
       const int j = min((bb + b) * 32 + l32, N - 1);  // past the frame or the range: result unused
-      const uint16_t* kp = L.K + (int64_t)j * L.kv_row + (int64_t)h * L.kv_head + half * 8;
+      const uint16_t* kp = Kh + (int64_t)j * kv_row + half * 8;
 #pragma unroll
       for (int ds = 0; ds < 4; ++ds) kf[b][ds] = *reinterpret_cast<const bf16x8*>(kp + ds * 16);
     }
@@ -90,7 +99,7 @@ __global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int i = i0 + u * NT + tid;
-      v[u] = i < a.n_q ? L.lse[(int64_t)h * N + q_token(i)] : __builtin_inff();
+      v[u] = i < a.n_q ? lse_h[q_token(i)] : __builtin_inff();
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -99,21 +108,13 @@ __global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
     }
   }
 
-  // Query row of sampled query qa for the A operand when the rows are not staged.
-  auto q_global = [&](int qa) -> const uint16_t* {
-    const int i = min(qa, a.n_q - 1);
-    const int qi = i / a.q_cols;
-    const int tok = a.q_base + qi * a.q_row_stride + (i - qi * a.q_cols) * a.q_col_stride;
-    return L.Q + ((int64_t)tok * H + h) * D + half * 8;
-  };
-
   // Passes over the sampled queries; each key's sum is carried from pass to pass by the
   // lane that owns it (fixed order).
-  const int q_pass = s_q ? a.q_pass : nq_pad;
+  const int q_pass = kStaged ? a.q_pass : nq_pad;
   for (int p0 = 0; p0 < nq_pad; p0 += q_pass) {
     const int p1 = min(nq_pad, p0 + q_pass);
     if (p0 > 0 && blk0 + wave * kBlocksPerStep < blk1) load_k(blk0 + wave * kBlocksPerStep, kf);
-    if (s_q) {
+    if (kStaged) {
       const int rows = p1 - p0;
       for (int c0 = 0; c0 < rows * 8; c0 += NT * kStageBatch) {
         uint4 v[kStageBatch];
@@ -122,7 +123,7 @@ __global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
           const int c = c0 + u * NT + tid, i = p0 + (c >> 3), ch = c & 7;
           v[u] = uint4{0u, 0u, 0u, 0u};
           if (c < rows * 8 && i < a.n_q)
-            v[u] = *reinterpret_cast<const uint4*>(L.Q + ((int64_t)q_token(i) * H + h) * D + ch * 8);
+            v[u] = *reinterpret_cast<const uint4*>(Qh + (int64_t)q_token(i) * H * D + ch * 8);
         }
 #pragma unroll
         for (int u = 0; u < kStageBatch; ++u) {
@@ -139,12 +140,13 @@ __global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
       float acc[kBlocksPerStep] = {};
       for (int qb = p0; qb < p1; qb += 32) {
         bf16x8 qf[4];
-        if (s_q) {
+        if (kStaged) {
 #pragma unroll
           for (int ds = 0; ds < 4; ++ds)
             qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[(qb - p0 + l32) * QS_STRIDE + ds * 16 + half * 8]);
         } else {
-          const uint16_t* qp = q_global(qb + l32);
+          // Query row of sampled query qb + l32 for the A operand, read from memory.
+          const uint16_t* qp = Qh + (int64_t)q_token(min(qb + l32, a.n_q - 1)) * H * D + half * 8;
 #pragma unroll
           for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
         }
@@ -177,11 +179,10 @@ __global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
         const float tot = acc[b] + __shfl_xor(acc[b], 32);
         const int j = (bb + b) * 32 + l32;
         if (b < nb && half == 0 && j < N) {
-          float* sp = L.sal + (int64_t)h * N + j;
           if (p0 == 0)  // uniform
-            *sp = tot;
+            sal_h[j] = tot;
           else
-            *sp += tot;
+            sal_h[j] += tot;
         }
       }
 #pragma unroll
@@ -191,6 +192,14 @@ __global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
     }
     if (p1 < nq_pad) __syncthreads();  // the staged rows are replaced by the next pass
   }
+}
+
+__global__ __launch_bounds__(NT, 3) void sal_kernel(AdmitArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  if (a.stage_queries)
+    sal_body<true>(a, smem);
+  else
+    sal_body<false>(a, smem);
 }
 
 // ---- selection and append -----------------------------------------------------------
