@@ -24,6 +24,8 @@
 // finds the threshold value and how many of its ties to take, and block scans emit the
 // indices.  Either way the indices come out ascending and the chosen K/V rows are copied
 // to the memory arena at rows mem_len.. with their provenance.
+#include <type_traits>
+
 #include "rv_internal.h"
 
 namespace rv {
@@ -36,6 +38,7 @@ constexpr int D = kHeadDim;
 constexpr int NT = kAdmitThreads;  // 256
 constexpr int NW = NT / 64;
 constexpr int kBlocksPerStep = 2;  // 32-key blocks a saliency wave holds at once
+static_assert(kBlocksPerStep == 2, "a range's last step holds one block or two");
 constexpr int QS_STRIDE = D + 8;   // staged sampled-query rows, 144 bytes
 constexpr int kStageBatch = 9;     // 16-byte query-row loads in flight per thread (one pass of 288 rows)
 constexpr float kLog2e = 1.44269504088896341f;
@@ -135,56 +138,63 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
     __syncthreads();
 
     for (int bb = blk0 + wave * kBlocksPerStep; bb < blk1; bb += NW * kBlocksPerStep) {
-      const int nb = min(kBlocksPerStep, blk1 - bb);
       if (bb + NW * kBlocksPerStep < blk1) load_k(bb + NW * kBlocksPerStep, kn);
-      float acc[kBlocksPerStep] = {};
-      for (int qb = p0; qb < p1; qb += 32) {
-        bf16x8 qf[4];
-        if (kStaged) {
+      // NB blocks held (the range's last step may hold fewer than kBlocksPerStep).
+      auto sweep = [&](auto nb_c) {
+        constexpr int NB = decltype(nb_c)::value;
+        float acc[NB] = {};
+        for (int qb = p0; qb < p1; qb += 32) {
+          bf16x8 qf[4];
+          if (kStaged) {
 #pragma unroll
-          for (int ds = 0; ds < 4; ++ds)
-            qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[(qb - p0 + l32) * QS_STRIDE + ds * 16 + half * 8]);
-        } else {
-          // Query row of sampled query qb + l32 for the A operand, read from memory.
-          const uint16_t* qp = Qh + (int64_t)q_token(min(qb + l32, a.n_q - 1)) * H * D + half * 8;
+            for (int ds = 0; ds < 4; ++ds)
+              qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[(qb - p0 + l32) * QS_STRIDE + ds * 16 + half * 8]);
+          } else {
+            // Query row of sampled query qb + l32 for the A operand, read from memory.
+            const uint16_t* qp = Qh + (int64_t)q_token(min(qb + l32, a.n_q - 1)) * H * D + half * 8;
 #pragma unroll
-          for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
-        }
-        // LSE of this lane's 16 accumulator rows: queries qb + 8*(r/4) + 4*half + r%4
-        float l2[16];
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          const float4 v = *reinterpret_cast<const float4*>(&s_lse2[qb + 8 * r4 + 4 * half]);
-          l2[4 * r4] = v.x;
-          l2[4 * r4 + 1] = v.y;
-          l2[4 * r4 + 2] = v.z;
-          l2[4 * r4 + 3] = v.w;
-        }
-#pragma unroll
-        for (int b = 0; b < kBlocksPerStep; ++b) {
-          f32x16 z = {};
-#pragma unroll
-          for (int ds = 0; ds < 4; ++ds) z = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z, 0, 0, 0);
-          float s0 = 0.f, s1 = 0.f;
-#pragma unroll
-          for (int r = 0; r < 16; r += 2) {
-            s0 += __builtin_amdgcn_exp2f(fmaf(z[r], kScaleLog2, -l2[r]));
-            s1 += __builtin_amdgcn_exp2f(fmaf(z[r + 1], kScaleLog2, -l2[r + 1]));
+            for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
           }
-          acc[b] += s0 + s1;
-        }
-      }
+          // LSE of this lane's 16 accumulator rows: queries qb + 8*(r/4) + 4*half + r%4
+          float l2[16];
 #pragma unroll
-      for (int b = 0; b < kBlocksPerStep; ++b) {
-        const float tot = acc[b] + __shfl_xor(acc[b], 32);
-        const int j = (bb + b) * 32 + l32;
-        if (b < nb && half == 0 && j < N) {
-          if (p0 == 0)  // uniform
-            sal_h[j] = tot;
-          else
-            sal_h[j] += tot;
+          for (int r4 = 0; r4 < 4; ++r4) {
+            const float4 v = *reinterpret_cast<const float4*>(&s_lse2[qb + 8 * r4 + 4 * half]);
+            l2[4 * r4] = v.x;
+            l2[4 * r4 + 1] = v.y;
+            l2[4 * r4 + 2] = v.z;
+            l2[4 * r4 + 3] = v.w;
+          }
+#pragma unroll
+          for (int b = 0; b < NB; ++b) {
+            f32x16 z = {};
+#pragma unroll
+            for (int ds = 0; ds < 4; ++ds) z = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z, 0, 0, 0);
+            float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) {
+              s0 += __builtin_amdgcn_exp2f(fmaf(z[r], kScaleLog2, -l2[r]));
+              s1 += __builtin_amdgcn_exp2f(fmaf(z[r + 1], kScaleLog2, -l2[r + 1]));
+            }
+            acc[b] += s0 + s1;
+          }
         }
-      }
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const float tot = acc[b] + __shfl_xor(acc[b], 32);
+          const int j = (bb + b) * 32 + l32;
+          if (half == 0 && j < N) {
+            if (p0 == 0)  // uniform
+              sal_h[j] = tot;
+            else
+              sal_h[j] += tot;
+          }
+        }
+      };
+      if (bb + kBlocksPerStep <= blk1)  // uniform
+        sweep(std::integral_constant<int, kBlocksPerStep>{});
+      else
+        sweep(std::integral_constant<int, 1>{});
 #pragma unroll
       for (int b = 0; b < kBlocksPerStep; ++b)
 #pragma unroll
