@@ -328,20 +328,30 @@ __device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
 
 __device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 
-__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, l);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), l);
-  return ((uint64_t)hi << 32) | lo;
+// The larger key of the pair a v_permlane*_swap leaves in (lo, hi): the two lanes'
+// values, in some order on every lane.
+template <class Pair>
+__device__ __forceinline__ uint64_t pair_max_u64(const Pair& lo, const Pair& hi) {
+  const uint64_t x = ((uint64_t)hi[0] << 32) | lo[0];
+  const uint64_t y = ((uint64_t)hi[1] << 32) | lo[1];
+  return max_u64(x, y);
 }
 
-// Maximum over the wave's 64 lanes: DPP within each 16-lane row (quad swaps, half
-// mirror, mirror), then the four row results read out as scalars.
+// Maximum over the wave's 64 lanes, left on every lane: DPP within each 16-lane row
+// (quad swaps, half mirror, mirror), then rows paired by v_permlane16_swap and halves by
+// v_permlane32_swap.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
   x = max_u64(x, dpp_u64<0xB1>(x));   // quad_perm [1,0,3,2]
   x = max_u64(x, dpp_u64<0x4E>(x));   // quad_perm [2,3,0,1]
   x = max_u64(x, dpp_u64<0x141>(x));  // row_half_mirror
   x = max_u64(x, dpp_u64<0x140>(x));  // row_mirror
-  return max_u64(max_u64(readlane_u64(x, 0), readlane_u64(x, 16)), max_u64(readlane_u64(x, 32), readlane_u64(x, 48)));
+  uint32_t lo = (uint32_t)x, hi = (uint32_t)(x >> 32);
+  x = pair_max_u64(__builtin_amdgcn_permlane16_swap(lo, lo, false, false),
+                   __builtin_amdgcn_permlane16_swap(hi, hi, false, false));
+  lo = (uint32_t)x;
+  hi = (uint32_t)(x >> 32);
+  return pair_max_u64(__builtin_amdgcn_permlane32_swap(lo, lo, false, false),
+                      __builtin_amdgcn_permlane32_swap(hi, hi, false, false));
 }
 
 // Top-`budget` (budget <= kWaveTopK) of sal[0..N), ascending, into s_idx.  Wave w owns
@@ -350,6 +360,7 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
 // wave-wide maximum and its lane drops it.  The 4 x budget winners are then ranked
 // among themselves.
 constexpr int kWaveTopK = 32;
+static_assert(NW * kWaveTopK % 8 == 0, "candidates are ranked in groups of eight");
 constexpr int kLaneSlots = 8;  // tokens per lane: the wave path takes N <= 4 * 64 * 8
 
 __device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx, uint64_t* s_cand) {
@@ -382,13 +393,22 @@ __device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx
   }
   __syncthreads();
   // candidate c is chosen if fewer than `budget` candidates outrank it; its output slot
-  // is the number of chosen candidates with a lower token index
+  // is the number of chosen candidates with a lower token index.  The candidates are
+  // read eight at a time (broadcast LDS reads in flight together); s_cand and s_chosen
+  // hold NW * kWaveTopK entries, a multiple of eight, so a group never reads past them
+  // (entries from nc on are masked out).
   const int nc = NW * budget;
   __shared__ int s_chosen[NW * kWaveTopK];
   for (int c = tid; c < nc; c += NT) {
     const uint64_t kc = s_cand[c];
     int above = 0;
-    for (int u = 0; u < nc; ++u) above += s_cand[u] > kc;
+    for (int u0 = 0; u0 < nc; u0 += 8) {
+      uint64_t x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = s_cand[u0 + e];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) above += (u0 + e < nc) & (x[e] > kc);
+    }
     s_chosen[c] = kc != 0 && above < budget;
   }
   __syncthreads();
@@ -396,7 +416,17 @@ __device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx
     if (!s_chosen[c]) continue;
     const uint32_t jc = ~(uint32_t)s_cand[c];
     int pos = 0;
-    for (int u = 0; u < nc; ++u) pos += s_chosen[u] && ~(uint32_t)s_cand[u] < jc;
+    for (int u0 = 0; u0 < nc; u0 += 8) {
+      uint64_t x[8];
+      int ch[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        x[e] = s_cand[u0 + e];
+        ch[e] = s_chosen[u0 + e];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pos += (u0 + e < nc) & (ch[e] != 0) & (~(uint32_t)x[e] < jc);
+    }
     s_idx[pos] = (int32_t)jc;
   }
   __syncthreads();
