@@ -447,11 +447,20 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   }
 }
 
+// Requests a field from every 64-byte line of the argument block at once: the reads that
+// follow (some of them through indices that other arguments give) then hit the scalar
+// cache, instead of each line's first read costing a round trip of its own.
+__device__ __forceinline__ void touch_args(const AttnArgs& a) {
+  asm volatile("" ::"s"(a.Q), "s"(a.lse), "s"(a.n_queues), "s"(a.unit_base[kMaxQueues]),
+               "s"(a.n_chunks[kMaxQueues - 1]), "s"(a.chunk_base[0]), "s"(a.chunk_base[kMaxQueues - 1]));
+}
+
 __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[NSTAGE * STAGE];
   // Workgroup b serves queue b % n_queues, chunk b / n_queues.  Queues are per XCD (the
   // hardware deals workgroup ids round-robin over the XCDs), which keeps the query
   // tiles of a head under one L2; placement only affects speed, never results.
+  touch_args(a);
   const int q = (int)(blockIdx.x % (unsigned)a.n_queues);
   const int c = (int)(blockIdx.x / (unsigned)a.n_queues);
   if (c >= a.n_chunks[q]) return;
@@ -478,6 +487,7 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
 __global__ __launch_bounds__(kAttnThreads) void attn_merge_kernel(AttnArgs a) {
   // Workgroup b merges for queue b % n_queues, like the forward workgroups that wrote
   // the partials (a locality heuristic: the partials may still be in that XCD's L2).
+  touch_args(a);
   const int q = (int)(blockIdx.x % (unsigned)a.n_queues);
   const int j = (int)(blockIdx.x / (unsigned)a.n_queues);
   const int ui = j / (BQ / kMergeRows), rb = j % (BQ / kMergeRows);
