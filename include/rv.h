@@ -237,7 +237,7 @@ rv_status rv_admit_staged_layers(int n_layers, const void *const *Q, const float
 rv_status rv_device_status(void);
 
 /* Pre-allocates the current device's scratch workspace (split-KV partial results,
- * saliency staging, completion counters) for frames of up to n_tokens tokens with
+ * saliency staging) for frames of up to n_tokens tokens with
  * n_heads heads, and up to n_layers layers per rv_admit_layers call, so that later
  * calls within those sizes do not allocate. */
 rv_status rv_reserve_workspace(int n_tokens, int n_heads, int n_layers);
