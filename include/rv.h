@@ -30,6 +30,12 @@
  *   - Calls that share an rv_mem, or that run concurrently on one device, must be
  *     ordered on one stream: the library's scratch workspace is shared per device.
  *   - The library never aborts the process.
+ *   - Environment overrides of the attention work plan (tests and tuning only; results
+ *     are the same under every plan, to the stated tolerances): RV_ATTN_SPLIT (0:
+ *     stream-K chunks, k > 0: every unit cut into k aligned pieces), RV_ATTN_WG_PER_CU
+ *     (workgroups per CU the plan fills, default 2), RV_ATTN_MIN_CHUNK (smallest chunk
+ *     in 64-key tiles, default 2), RV_ATTN_SPLIT_SLACK (tiles by which the aligned split
+ *     may exceed stream-K before stream-K is taken, default 1).
  */
 #ifndef RV_H
 #define RV_H
