@@ -450,6 +450,8 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
 // Requests a field from every 64-byte line of the argument block at once: the reads that
 // follow (some of them through indices that other arguments give) then hit the scalar
 // cache, instead of each line's first read costing a round trip of its own.
+static_assert(sizeof(AttnArgs) <= 5 * 64 && offsetof(AttnArgs, chunk_base) + 4 * kMaxQueues > 4 * 64,
+              "touch_args names a field in each of the argument block's five lines");
 __device__ __forceinline__ void touch_args(const AttnArgs& a) {
   asm volatile("" ::"s"(a.Q), "s"(a.lse), "s"(a.n_queues), "s"(a.unit_base[kMaxQueues]),
                "s"(a.n_chunks[kMaxQueues - 1]), "s"(a.chunk_base[0]), "s"(a.chunk_base[kMaxQueues - 1]));
