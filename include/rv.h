@@ -35,7 +35,9 @@
  *     stream-K chunks, k > 0: every unit cut into k aligned pieces), RV_ATTN_WG_PER_CU
  *     (workgroups per CU the plan fills, default 2), RV_ATTN_MIN_CHUNK (smallest chunk
  *     in 64-key tiles, default 2), RV_ATTN_SPLIT_SLACK (tiles by which the aligned split
- *     may exceed stream-K before stream-K is taken, default 1).
+ *     may exceed stream-K before stream-K is taken, default 1), RV_ATTN_FIRST_PCT (tiles
+ *     of a stream-K chunk served by a workgroup dispatched first on its CU, in per cent
+ *     of the others', default 140).
  */
 #ifndef RV_H
 #define RV_H

@@ -271,10 +271,20 @@ constexpr int kSlotStatsFloat = BQ * D / 2;
 constexpr int kMergeRows = 32;   // output rows per merge workgroup (8 threads per row)
 constexpr int kMergeMax = 8;     // partials whose loads are in flight together
 
+// First iteration of chunk c of a queue: chunks 0 .. n_first-1 hold E tiles, the later
+// ones E1; and the chunk holding iteration `it`.
+__device__ __forceinline__ int64_t chunk_start(const AttnArgs& a, int c) {
+  return c < a.n_first ? (int64_t)c * a.E : (int64_t)a.n_first * a.E + (int64_t)(c - a.n_first) * a.E1;
+}
+__device__ __forceinline__ int chunk_of(const AttnArgs& a, int64_t it) {
+  const int64_t first = (int64_t)a.n_first * a.E;
+  return it < first ? (int)(it / a.E) : a.n_first + (int)((it - first) / a.E1);
+}
+
 // Partial slot of chunk c's segment of unit ui: slot 0 if the chunk starts inside the
 // unit, slot 1 if it began in an earlier unit.
 __device__ __forceinline__ const float* slot_ptr(const AttnArgs& a, int q, int c, int ui) {
-  const int slot = 2 * (a.chunk_base[q] + c) + ((int64_t)c * a.E >= (int64_t)ui * a.U ? 0 : 1);
+  const int slot = 2 * (a.chunk_base[q] + c) + (chunk_start(a, c) >= (int64_t)ui * a.U ? 0 : 1);
   return a.part + (int64_t)slot * kAttnSlotFloats;
 }
 
@@ -426,7 +436,7 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   }
 
   // Partial result: merged by the second launch.
-  const int seg = (int64_t)c * a.E >= (int64_t)ui * a.U ? 0 : 1;
+  const int seg = chunk_start(a, c) >= (int64_t)ui * a.U ? 0 : 1;
   float* ps = a.part + (int64_t)(2 * (a.chunk_base[q] + c) + seg) * kAttnSlotFloats;
   if (wave_active) {
     // normalised partial output in bf16 (the merge weights it by 2^(m - M) l), m and l in fp32
@@ -450,10 +460,13 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
 // Requests a field from every 64-byte line of the argument block at once: the reads that
 // follow (some of them through indices that other arguments give) then hit the scalar
 // cache, instead of each line's first read costing a round trip of its own.
-static_assert(sizeof(AttnArgs) <= 5 * 64 && offsetof(AttnArgs, chunk_base) + 4 * kMaxQueues > 4 * 64,
-              "touch_args names a field in each of the argument block's five lines");
+// (The scalars before the tables lie in the lines of Q and lse; each table spans at most
+// two lines, holding its first and last entries.)
+static_assert(offsetof(AttnArgs, lse) >= 64 && offsetof(AttnArgs, unit_base) <= 2 * 64 &&
+                  offsetof(AttnArgs, chunk_base) + 4 * kMaxQueues + 8 > sizeof(AttnArgs) && kMaxQueues <= 16,
+              "touch_args names a field in every line of the argument block");
 __device__ __forceinline__ void touch_args(const AttnArgs& a) {
-  asm volatile("" ::"s"(a.Q), "s"(a.lse), "s"(a.n_queues), "s"(a.unit_base[kMaxQueues]),
+  asm volatile("" ::"s"(a.Q), "s"(a.lse), "s"(a.unit_base[0]), "s"(a.unit_base[kMaxQueues]), "s"(a.n_chunks[0]),
                "s"(a.n_chunks[kMaxQueues - 1]), "s"(a.chunk_base[0]), "s"(a.chunk_base[kMaxQueues - 1]));
 }
 
@@ -468,8 +481,8 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
   if (c >= a.n_chunks[q]) return;
   const int ub = a.unit_base[q];
   const int total = (a.unit_base[q + 1] - ub) * a.U;
-  int it = c * a.E;
-  const int it_end = min(total, it + a.E);
+  int it = (int)chunk_start(a, c);
+  const int it_end = (int)min((int64_t)total, chunk_start(a, c + 1));
   while (it < it_end) {
     const int ui = it / a.U;
     const int t0 = it - ui * a.U;
@@ -495,8 +508,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_merge_kernel(AttnArgs a) {
   const int ui = j / (BQ / kMergeRows), rb = j % (BQ / kMergeRows);
   if (ui >= a.unit_base[q + 1] - a.unit_base[q]) return;
   const int unit = a.unit_base[q] + ui;
-  const int c_first = (int)(((int64_t)ui * a.U) / a.E);
-  const int c_last = (int)(((int64_t)ui * a.U + a.T - 1) / a.E);
+  const int c_first = chunk_of(a, (int64_t)ui * a.U);
+  const int c_last = chunk_of(a, (int64_t)ui * a.U + a.T - 1);
   if (c_first == c_last) return;  // written whole by its only chunk
   merge_rows(a, q, unit, ui, rb, c_first, c_last);
 }

@@ -157,7 +157,7 @@ rv_status check_qsub(const rv_qsub* qs, int n_tokens) {
 // tiles together.  Stream-K: U = T, chunks may straddle units.  RV_ATTN_SPLIT forces
 // one (0: stream-K, k > 0: k-way).
 struct AttnPlan {
-  int q_tiles, nt_mem, T, U, n_units, E, grid, total_chunks;
+  int q_tiles, nt_mem, T, U, n_units, E, E1, n_first, grid, total_chunks;
   int unit_base[rv::kMaxQueues + 1];
   int n_chunks[rv::kMaxQueues];
   int chunk_base[rv::kMaxQueues];
@@ -181,24 +181,42 @@ AttnPlan plan_attention(const Workspace& ws, int n_tokens, int n_fkeys, int64_t 
   // second pipeline start; the aligned split leaves some workgroup slots idle.  Take the
   // split while its chunks are at most kSplitSlackTiles longer than stream-K's.
   constexpr int kSplitSlackTiles = 1;
+  // Tiles of a first-dispatched stream-K chunk, in per cent of a later chunk's.
+  constexpr int kFirstChunkPct = 140;
   int k = env_int("RV_ATTN_SPLIT", -1);
   if (k < 0) {
     k = wg_per_queue / std::max(1, max_units);
     const int64_t e_sk = ceil_div((int64_t)max_units * p.T, wg_per_queue);
     if (k >= 1 && ceil_div(p.T, k) > e_sk + env_int("RV_ATTN_SPLIT_SLACK", kSplitSlackTiles)) k = 0;
   }
+  p.n_first = 0;
   if (k >= 1) {
     p.E = (int)std::max<int64_t>(e_min, ceil_div(p.T, k));
     k = (int)ceil_div(p.T, p.E);  // pieces that hold tiles
     p.U = k * p.E;
+    p.E1 = p.E;
   } else {
+    // Stream-K.  Workgroup ids are dealt round-robin over the XCDs and then over the
+    // CUs, so a queue's first n_cus / nq chunks go to the workgroups dispatched first
+    // on their CUs, which run measurably faster than the second ones: those chunks get
+    // kFirstChunkPct per cent of the later chunks' tiles (a speed heuristic only; any
+    // placement gives the same results).
     p.U = p.T;
-    p.E = (int)std::max<int64_t>(e_min, ceil_div((int64_t)max_units * p.T, wg_per_queue));
+    const int64_t work = (int64_t)max_units * p.T;
+    const int pct = std::max(100, env_int("RV_ATTN_FIRST_PCT", kFirstChunkPct));
+    const int n_first = std::min(wg_per_queue, std::max(0, ws.n_cus / nq));
+    const int n_rest = wg_per_queue - n_first;
+    p.E1 = (int)std::max<int64_t>(e_min, ceil_div(work * 100, (int64_t)n_first * pct + (int64_t)n_rest * 100));
+    p.E = (int)std::max<int64_t>(e_min, ceil_div((int64_t)p.E1 * pct, 100));
+    p.n_first = p.E == p.E1 ? 0 : n_first;
+    if (p.n_first == 0) p.E = p.E1;
   }
   p.total_chunks = 0;
   int max_chunks = 0;
   for (int q = 0; q < nq; ++q) {
-    p.n_chunks[q] = (int)ceil_div((int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.U, p.E);
+    const int64_t iters = (int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.U;
+    const int64_t first = (int64_t)p.n_first * p.E;
+    p.n_chunks[q] = iters <= first ? (int)ceil_div(iters, p.E) : p.n_first + (int)ceil_div(iters - first, p.E1);
     p.chunk_base[q] = p.total_chunks;
     p.total_chunks += p.n_chunks[q];
     max_chunks = std::max(max_chunks, p.n_chunks[q]);
@@ -559,13 +577,15 @@ rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens,
   a.n_units = p.n_units;
   a.n_queues = ws->n_queues;
   a.E = p.E;
+  a.E1 = p.E1;
+  a.n_first = p.n_first;
   for (int q = 0; q <= ws->n_queues; ++q) a.unit_base[q] = p.unit_base[q];
   for (int q = 0; q < ws->n_queues; ++q) {
     a.n_chunks[q] = p.n_chunks[q];
     a.chunk_base[q] = p.chunk_base[q];
   }
   // every unit whole in one chunk (no split) needs no merge launch
-  const bool split = (int64_t)p.E < p.T || p.U != p.T || (int64_t)p.T % p.E != 0;
+  const bool split = (int64_t)p.E < p.T || p.U != p.T || (int64_t)p.T % p.E != 0 || p.E1 != p.E;
   RV_HIP(rv::launch_attention(a, p.grid, split, s), "attention launch");
 
   if (saliency) {

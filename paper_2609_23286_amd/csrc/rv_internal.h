@@ -44,7 +44,9 @@ struct AttnArgs {
   int U;                   // iteration stride per unit: T (stream-K) or k * E >= T (k-way split)
   int n_units;             // n_heads * q_tiles
   int n_queues;
-  int E;                   // key tiles per chunk
+  int E;                   // key tiles per chunk (the first n_first chunks of a queue)
+  int E1;                  // key tiles per later chunk (E1 = E unless n_first > 0)
+  int n_first;             // chunks per queue of E tiles; the rest hold E1
   int unit_base[kMaxQueues + 1];
   int n_chunks[kMaxQueues];
   int chunk_base[kMaxQueues];

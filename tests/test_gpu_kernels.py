@@ -90,22 +90,27 @@ def test_attend_and_saliency_match_oracle(rv, N, H, M, sigma):
     assert (np.abs(sal - sal_o) <= SAL_RTOL * sal_o).all()
 
 
-PLANS = [  # (workgroups per CU, minimum chunk, split: -1 auto, 0 stream-K, k > 0 k-way)
-    ("1", "1", "0"), ("2", "2", "0"), ("4", "1", "0"), ("1", "100000", "0"),
-    ("2", "2", "-1"), ("1", "1", "1"), ("2", "1", "7"), ("2", "1", "64"), ("4", "3", "-1"),
+PLANS = [  # (workgroups per CU, minimum chunk, split: -1 auto, 0 stream-K, k > 0 k-way,
+           #  per cent of a later stream-K chunk's tiles given to a first-dispatched one)
+    ("1", "1", "0", "140"), ("2", "2", "0", "140"), ("4", "1", "0", "140"), ("1", "100000", "0", "140"),
+    ("2", "2", "-1", "140"), ("1", "1", "1", "140"), ("2", "1", "7", "140"), ("2", "1", "64", "140"),
+    ("4", "3", "-1", "140"), ("2", "1", "0", "100"), ("2", "1", "0", "101"), ("2", "2", "0", "400"),
+    ("4", "1", "0", "250"),
 ]
 
 
-@pytest.mark.parametrize("wg_per_cu,min_chunk,split", PLANS)
-def test_work_plans_agree_with_oracle(rv, wg_per_cu, min_chunk, split, monkeypatch):
-    """Work plans (stream-K chunks of one key tile, of a few, whole units; aligned k-way
-    splits with k = 1, several, more pieces than tiles) change only the rounding order
-    of the partial merges."""
+@pytest.mark.parametrize("wg_per_cu,min_chunk,split,first_pct", PLANS)
+def test_work_plans_agree_with_oracle(rv, wg_per_cu, min_chunk, split, first_pct, monkeypatch):
+    """Work plans (stream-K chunks of one key tile, of a few, whole units, with the
+    first-dispatched chunks as long as the others or longer; aligned k-way splits with
+    k = 1, several, more pieces than tiles) change only the rounding order of the
+    partial merges."""
     monkeypatch.setenv("RV_ATTN_WG_PER_CU", wg_per_cu)
     monkeypatch.setenv("RV_ATTN_MIN_CHUNK", min_chunk)
     monkeypatch.setenv("RV_ATTN_SPLIT", split)
+    monkeypatch.setenv("RV_ATTN_FIRST_PCT", first_pct)
     for N, H, M in ((333, 4, 1500), (1041, 16, 3000), (65, 1, 0)):
-        print(f"plan {wg_per_cu}/{min_chunk}/{split}: N={N} H={H} M={M}", flush=True)
+        print(f"plan {wg_per_cu}/{min_chunk}/{split}/{first_pct}: N={N} H={H} M={M}", flush=True)
         Q, K, V = frame(7 + N, N, H)
         memK, memV = memory_rows(8 + N, H, M)
         out, lse, _ = run_attend(rv, Q, K, V, memK, memV, qsub_for(N), with_saliency=False)
