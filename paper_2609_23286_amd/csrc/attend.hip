@@ -24,8 +24,10 @@
 // * Scheduling: 1041 queries x 16 heads is only 144 units, too few for 256 CUs, so each
 //   unit's key range is split.  Units are dealt to one queue per XCD (whole heads where
 //   possible); each queue's (unit, key tile) iterations, laid out with a stride of U
-//   tiles per unit, are cut into equal chunks of E tiles, one per workgroup.  With
-//   U = T (the unit's tile count) this is stream-K: chunks may straddle units.  With
+//   tiles per unit, are cut into chunks, one per workgroup.  With U = T (the unit's
+//   tile count) this is stream-K: chunks may straddle units, and the first n_first
+//   chunks of a queue (served by the workgroups dispatched first on their CUs, which
+//   run faster) hold E tiles against E1 for the rest.  With
 //   U = k E >= T every unit is cut into k aligned pieces, so the workgroups holding the
 //   query tiles of one head walk the same key tiles at the same time and share them in
 //   L2.  A chunk that covers a whole unit writes its output directly; otherwise it
