@@ -151,11 +151,12 @@ rv_status check_qsub(const rv_qsub* qs, int n_tokens) {
 
 // Work plan of one attention launch: units (head, 128-query tile) are dealt in
 // contiguous ranges to the per-XCD queues, and each queue's (unit, key tile) iterations
-// are cut into chunks of E tiles, one per workgroup, about kAttnWgPerCu per CU.
-// k-way split: each unit's key range is cut into k aligned pieces (iteration stride
-// U = k E per unit), so the workgroups on one head's query tiles stream the same key
-// tiles together.  Stream-K: U = T, chunks may straddle units.  RV_ATTN_SPLIT forces
-// one (0: stream-K, k > 0: k-way).
+// are cut into chunks, one per workgroup, about kAttnWgPerCu per CU: the first n_first
+// chunks of a queue hold E tiles, the others E1 (E1 = E and n_first = 0 unless
+// stream-K).  k-way split: each unit's key range is cut into k aligned pieces
+// (iteration stride U = k E per unit), so the workgroups on one head's query tiles
+// stream the same key tiles together.  Stream-K: U = T, chunks may straddle units.
+// RV_ATTN_SPLIT forces one (0: stream-K, k > 0: k-way).
 struct AttnPlan {
   int q_tiles, nt_mem, T, U, n_units, E, E1, n_first, grid, total_chunks;
   int unit_base[rv::kMaxQueues + 1];
@@ -209,7 +210,7 @@ AttnPlan plan_attention(const Workspace& ws, int n_tokens, int n_fkeys, int64_t 
     p.E1 = (int)std::max<int64_t>(e_min, ceil_div(work * 100, (int64_t)n_first * pct + (int64_t)n_rest * 100));
     p.E = (int)std::max<int64_t>(e_min, ceil_div((int64_t)p.E1 * pct, 100));
     p.n_first = p.E == p.E1 ? 0 : n_first;
-    if (p.n_first == 0) p.E = p.E1;
+    if (p.n_first == 0) p.E = p.E1;  // (no first workgroups to favour)
   }
   p.total_chunks = 0;
   int max_chunks = 0;
