@@ -244,6 +244,26 @@ rv_status rv_admit_staged_layers(int n_layers, const void *const *Q, const float
  * each step. */
 rv_status rv_device_status(void);
 
+/* Work plan the attention launch uses for one frame (introspection for tests and
+ * tuning; touches no device and allocates nothing).  n_cus and n_queues (XCDs, 1..16)
+ * describe the device; the library's own launches use the counts it reads at start-up,
+ * and the RV_ATTN_* overrides apply here as there.  Query tiles of 128 and key tiles of
+ * 64 make n_units = n_heads * q_tiles units of T key tiles each; queue q owns units
+ * unit_base[q] .. unit_base[q+1]-1, laid out as iterations i = u * U + t (t < U; tiles
+ * t >= T are padding).  Chunk c (0 <= c < n_chunks[q]) of queue q covers iterations
+ * [start(c), min(start(c+1), units_q * U)) with start(c) = c * E for c < n_first and
+ * n_first * E + (c - n_first) * E1 after; chunk_base[q] numbers the chunks of all
+ * queues consecutively, and grid = n_queues * max(n_chunks) workgroups are launched.
+ * RV_ERR_INVALID for out-of-range sizes or a NULL `out`. */
+typedef struct rv_attn_plan {
+    int n_units, q_tiles, T, U, E, E1, n_first, n_queues, grid, total_chunks;
+    int unit_base[17];
+    int n_chunks[16];
+    int chunk_base[16];
+} rv_attn_plan;
+rv_status rv_attention_plan(int n_tokens, int n_fkeys, int64_t mem_len, int n_heads, int n_cus,
+                            int n_queues, rv_attn_plan *out);
+
 /* Pre-allocates the current device's scratch workspace (split-KV partial results,
  * saliency staging) for frames of up to n_tokens tokens with
  * n_heads heads, and up to n_layers layers per rv_admit_layers call, so that later

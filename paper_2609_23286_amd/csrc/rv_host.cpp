@@ -205,7 +205,8 @@ AttnPlan plan_attention(const Workspace& ws, int n_tokens, int n_fkeys, int64_t 
     p.U = p.T;
     const int64_t work = (int64_t)max_units * p.T;
     const int pct = std::max(100, env_int("RV_ATTN_FIRST_PCT", kFirstChunkPct));
-    const int n_first = std::min(wg_per_queue, std::max(0, ws.n_cus / nq));
+    // (no second workgroup per CU to favour the first over: uniform chunks)
+    const int n_first = ws.n_cus / nq < wg_per_queue ? std::max(0, ws.n_cus / nq) : 0;
     const int n_rest = wg_per_queue - n_first;
     p.E1 = (int)std::max<int64_t>(e_min, ceil_div(work * 100, (int64_t)n_first * pct + (int64_t)n_rest * 100));
     p.E = (int)std::max<int64_t>(e_min, ceil_div((int64_t)p.E1 * pct, 100));
@@ -221,6 +222,10 @@ AttnPlan plan_attention(const Workspace& ws, int n_tokens, int n_fkeys, int64_t 
     p.chunk_base[q] = p.total_chunks;
     p.total_chunks += p.n_chunks[q];
     max_chunks = std::max(max_chunks, p.n_chunks[q]);
+  }
+  if (max_chunks <= p.n_first) {  // every chunk is a first one: say so plainly
+    p.n_first = 0;
+    p.E1 = p.E;
   }
   p.grid = nq * max_chunks;
   return p;
@@ -509,6 +514,36 @@ rv_status rv_mem_load(rv_mem m, const char* path) {
     if (e != hipSuccess) return hip_fail(e, "rv_mem_load copy");
   }
   m->len = len;
+  return RV_OK;
+}
+
+rv_status rv_attention_plan(int n_tokens, int n_fkeys, int64_t mem_len, int n_heads, int n_cus, int n_queues,
+                            rv_attn_plan* out) {
+  static_assert(rv::kMaxQueues == 16, "rv_attn_plan's tables hold kMaxQueues entries");
+  if (!out) return fail(RV_ERR_INVALID, "out is NULL");
+  if (n_tokens < 1 || n_tokens > rv::kMaxTokens || n_fkeys < 0 || n_fkeys > n_tokens || mem_len < 0 ||
+      n_heads < 1 || n_cus < 1 || n_queues < 1 || n_queues > rv::kMaxQueues)
+    return fail(RV_ERR_INVALID, "plan sizes out of range");
+  Workspace ws;
+  ws.n_cus = n_cus;
+  ws.n_queues = n_queues;
+  const AttnPlan p = plan_attention(ws, n_tokens, n_fkeys, mem_len, n_heads);
+  *out = rv_attn_plan{};
+  out->n_units = p.n_units;
+  out->q_tiles = p.q_tiles;
+  out->T = p.T;
+  out->U = p.U;
+  out->E = p.E;
+  out->E1 = p.E1;
+  out->n_first = p.n_first;
+  out->n_queues = n_queues;
+  out->grid = p.grid;
+  out->total_chunks = p.total_chunks;
+  for (int q = 0; q <= n_queues; ++q) out->unit_base[q] = p.unit_base[q];
+  for (int q = 0; q < n_queues; ++q) {
+    out->n_chunks[q] = p.n_chunks[q];
+    out->chunk_base[q] = p.chunk_base[q];
+  }
   return RV_OK;
 }
 

@@ -31,6 +31,12 @@ class rv_qsub(ctypes.Structure):
                 ("n_special", ctypes.c_int32), ("stride", ctypes.c_int32)]
 
 
+class rv_attn_plan(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("n_units", "q_tiles", "T", "U", "E", "E1", "n_first",
+                                               "n_queues", "grid", "total_chunks")] + [
+        ("unit_base", ctypes.c_int32 * 17), ("n_chunks", ctypes.c_int32 * 16), ("chunk_base", ctypes.c_int32 * 16)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
@@ -62,6 +68,7 @@ def _load():
         "rv_attend_staged": ([vp, i32, vp, P(rv_qsub), vp, vp, vp, vp], i32),
         "rv_admit_staged_layers": ([i32, P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp), vp], i32),
         "rv_reserve_workspace": ([i32, i32, i32], i32),
+        "rv_attention_plan": ([i32, i32, i64, i32, i32, i32, P(rv_attn_plan)], i32),
         "rv_device_status": ([], i32),
     }
     for name, (args, res) in sigs.items():
@@ -119,6 +126,14 @@ def qsub(grid_h, grid_w, n_special, stride):
 
 def reserve_workspace(n_tokens, n_heads, n_layers=1):
     _check(_lib.rv_reserve_workspace(n_tokens, n_heads, n_layers))
+
+
+def attention_plan(n_tokens, n_fkeys, mem_len, n_heads, n_cus, n_queues):
+    """The attention work plan for a frame on a device of n_cus CUs and n_queues XCDs
+    (rv_attention_plan; no device work), as an rv_attn_plan structure."""
+    out = rv_attn_plan()
+    _check(_lib.rv_attention_plan(n_tokens, n_fkeys, mem_len, n_heads, n_cus, n_queues, ctypes.byref(out)))
+    return out
 
 
 def device_status():
