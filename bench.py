@@ -2,19 +2,27 @@
 
 Workload: the 24-layer ViT-L-shaped stream (16 heads x 64, 1041 tokens per frame =
 28x37 patches + 5 special tokens, budget 10 tokens per head per frame, 2x2 query
-sampling), 1000 frames, memory starting empty and growing to 9,990 rows per
-(layer, head).  One step = one frame: for each of the 24 layers, attention of the
-frame over that layer's memory with per-query LSE (rv_attend_frame), then one deferred
-launch that computes every layer's LSE-saliency, selects each head's top 10 and appends
-them (rv_admit_layers).
+sampling) of 1000 frames, whose memory grows from empty to 9,990 rows per (layer, head)
+(Sec. 3.3 Eq. 6: 10 rows per frame).  One step = one frame: for each of the 24 layers,
+attention of the frame over that layer's memory with per-query LSE (rv_attend_frame),
+then one deferred launch that computes every layer's LSE-saliency, selects each head's
+top 10 and appends them (rv_admit_layers).
 
-Every frame's Q/K/V (distinct per layer and frame, seeded) is generated on the GPU and
-resident in HBM before timing starts (153 MB per frame).  The timed region covers the
-steps only, between device synchronisations.  HIP events on the compute stream
-bracket each frame's attention launches and its admission launch; they give the
-attention kernel's average duration, from which the roofline fraction is computed.
-The oracle is timed on the host on a bounded sample (one layer of the frame whose
-context equals the stream's mean context) and extrapolated to frames/s.
+--steps 1000 times the whole stream in order from an empty memory.  --steps K < 1000
+times a stratified sample of it: frame t_i = floor((i + 1/2) 1000 / K) for i < K, each
+attended and admitted at the memory length it has in the stream (t_i x 10 rows), so the
+mean context of the timed frames equals the stream's (about 6,036).  Each layer's memory
+is filled once with generator rows to the longest of those lengths, and the frames run
+back to back, longest memory first, each preceded by a host-side length change
+(rv_mem_truncate, no device work).
+
+Every timed frame's Q/K/V (distinct per layer and frame, seeded) is generated on the GPU
+and resident in HBM before timing starts (153 MB per frame).  The timed region covers the
+steps only, between device synchronisations.  HIP events on the compute stream bracket
+each frame's attention launches and its admission launch; they give the attention
+kernel's average duration, from which the roofline fraction is computed.  The oracle is
+timed on the host on a bounded sample (one layer of each of 24 stratified frames at its
+stream memory length) and extrapolated to frames/s.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -35,10 +43,11 @@ PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2609_23286_amd", "csrc")
 # Kernel -> the sources whose text decides its memory traffic; counters recorded for
 # other sources are stale and are not reported.
-KERNEL_SOURCES = {"attn_fwd_kernel": ("attend.hip", "rv_internal.h", "rv_host.cpp"),
-                  "attn_merge_kernel": ("attend.hip", "rv_internal.h", "rv_host.cpp"),
-                  "sal_kernel": ("admit.hip", "rv_internal.h", "rv_host.cpp"),
-                  "select_kernel": ("admit.hip", "rv_internal.h", "rv_host.cpp")}
+_HOST = ("rv_internal.h", "rv_plan.h", "rv_plan.cpp", "rv_host.cpp")
+KERNEL_SOURCES = {"attn_fwd_kernel": ("attend.hip",) + _HOST,
+                  "attn_merge_kernel": ("attend.hip",) + _HOST,
+                  "sal_kernel": ("admit.hip",) + _HOST,
+                  "select_kernel": ("admit.hip",) + _HOST}
 ADMISSION_KERNELS = ("sal_kernel", "select_kernel")  # one launch each per frame
 COPY_CALIBRATION_BYTES = 256 << 20   # read and written once by the calibration copy
 
@@ -124,6 +133,20 @@ def admission_traffic(workload):
     return None if any(p is None for p in parts) else sum(parts)
 
 
+def bench_args():
+    """This command's benchmark arguments, without the summary options."""
+    out, skip = [], 0
+    for a in sys.argv[1:]:
+        if skip:
+            skip -= 1
+            continue
+        if a in ("--pmc-summary", "--trace-summary"):
+            skip = 2
+            continue
+        out.append(a)
+    return " ".join(out)
+
+
 def summarize_pmc(fetch_dir, write_dir, workload):
     """Reduce two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; counter CSVs) of this
     benchmark started with --copy-calibration into per-launch HBM traffic.  The
@@ -167,10 +190,10 @@ def summarize_pmc(fetch_dir, write_dir, workload):
             "```",
             "cd /tmp && export TMPDIR=/tmp",
             "timeout -s KILL 600 rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/fetch -o fetch -- \\",
-            "    python /root/repo/bench.py --no-cpu-baseline --copy-calibration",
+            f"    python /root/repo/bench.py {bench_args()} --no-cpu-baseline --copy-calibration",
             "timeout -s KILL 600 rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/write -o write -- \\",
-            "    python /root/repo/bench.py --no-cpu-baseline --copy-calibration",
-            "python /root/repo/bench.py --pmc-summary <out>/fetch <out>/write",
+            f"    python /root/repo/bench.py {bench_args()} --no-cpu-baseline --copy-calibration",
+            f"python /root/repo/bench.py {bench_args()} --pmc-summary <out>/fetch <out>/write",
             "```",
             "",
             f"- dispatches: {len(fv)} (FETCH_SIZE pass), {len(wv)} (WRITE_SIZE pass)",
@@ -218,8 +241,8 @@ def summarize_trace(trace_dir, bench_json, workload):
              "Command (on the MI355X, from the repository root):", "", "```",
              "cd /tmp && export TMPDIR=/tmp",
              "rocprofv3 --kernel-trace --stats --output-format csv -d <out>/trace -o bench -- \\",
-             "    python /root/repo/bench.py --no-cpu-baseline > <out>/trace.json",
-             "python /root/repo/bench.py --trace-summary <out>/trace <out>/trace.json", "```", "",
+             f"    python /root/repo/bench.py {bench_args()} --no-cpu-baseline > <out>/trace.json",
+             f"python /root/repo/bench.py {bench_args()} --trace-summary <out>/trace <out>/trace.json", "```", "",
              "Kernel statistics (durations in ns; counts include the warm-up frames; the input",
              "generator kernels run before the timed region):", "",
              "| Kernel | Calls | Total ns | Average ns | % | Min ns | Max ns |", "|---|---|---|---|---|---|---|"]
@@ -244,36 +267,71 @@ def summarize_trace(trace_dir, bench_json, workload):
     print(f"wrote {path}")
 
 
-def cpu_baseline(cfg, mean_ctx, n_frames, budget, qs):
-    """Time the oracle on one layer of a frame whose context is the stream's mean."""
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, samples, budget, qs, mem_len, mean_ctx):
+    """Time the oracle as it stands on a bounded sample of the timed workload: for each
+    (layer, frame) in `samples`, one layer of that frame (all heads, all queries,
+    LSE-saliency, top-k, append) at the memory length that frame has in the stream.
+    Frames per second = 1 / (mean time per layer-frame x layers x (stream mean context /
+    sample mean context))."""
     import oracle
     from paper_2609_23286_amd import synth
     N, H = cfg.n_tokens, cfg.n_heads
-    M = max(0, int(round(mean_ctx - N)))
-    t_mid = M // max(budget, 1)
-    Q, K, V = synth.frame_qkv(cfg, 0, t_mid)
-    memK, memV = synth.memory_prefill(cfg, 0, M, M + budget)
     qidx = oracle.qsub_index(*qs)
-    omem = oracle.Memory(H, cfg.head_dim, M + budget)
+    rows = max(mem_len(l, t) for l, t in samples) + budget
+    memK, memV = synth.memory_prefill(cfg, 0, rows)   # memory rows; contents do not affect time
+    omem = oracle.Memory(H, cfg.head_dim, rows)
     omem.K[:], omem.V[:] = memK, memV
-    omem.len = M
-    t0 = time.perf_counter()
-    oracle.step(omem, Q, K, V, qidx, budget)
-    dt = time.perf_counter() - t0
-    per_frame = dt * cfg.n_layers * (mean_ctx / (M + N))
+    dt, ctx = 0.0, 0
+    for l, t in samples:
+        Q, K, V = synth.frame_qkv(cfg, l, t)
+        omem.len = mem_len(l, t)
+        ctx += omem.len + N
+        t0 = time.perf_counter()
+        oracle.step(omem, Q, K, V, qidx, budget)
+        dt += time.perf_counter() - t0
+    per_layer = dt / len(samples)
+    per_frame = per_layer * cfg.n_layers * (mean_ctx / (ctx / len(samples)))
     return {"value": 1.0 / per_frame, "unit": "frames/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": (f"one layer ({H} heads, all {N} queries, saliency, top-{budget}, append) at "
-                       f"context {M + N}, {dt:.2f} s, scaled x{cfg.n_layers} layers and to the "
-                       f"{n_frames}-frame mean context {mean_ctx:.0f}")}
+            "cpu_model": cpu_model(), "kind": "oracle",
+            "sample": (f"{len(samples)} layer-frames of the timed frames (one layer each: {H} heads, all {N} "
+                       f"queries, saliency, top-{budget}, append) at their stream memory lengths, mean "
+                       f"context {ctx / len(samples):.0f}, {dt:.1f} s in all; scaled x{cfg.n_layers} layers "
+                       f"and to the timed frames' mean context {mean_ctx:.0f}")}
+
+
+def stratified(n_stream, n):
+    """n frames of an n_stream-frame stream, one from the middle of each of n equal
+    stretches: t_i = floor((i + 1/2) n_stream / n)."""
+    return [int((i + 0.5) * n_stream / n) for i in range(n)]
+
+
+def workload_key(cfg, n_stream, steps, variant):
+    """Name under which counter profiles of this run are filed (None for variants)."""
+    if variant:
+        return None
+    return cfg.name if steps >= n_stream else f"{cfg.name}__{steps}of{n_stream}"
 
 
 def main():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=1000, help="frames timed (from an empty memory)")
+    p.add_argument("--steps", type=int, default=1000,
+                   help="frames timed; fewer than the stream's frames times a stratified sample of them "
+                        "(frame t_i = floor((i + 1/2) T / steps), each at the memory length it has in the stream)")
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--config", default="vitl_stack_1000")
+    p.add_argument("--stream-frames", type=int, default=None,
+                   help="length T of the stream the frames are drawn from (default: the configuration's)")
     p.add_argument("--policy", choices=("all", "paper"), default="all",
                    help="all: every layer regulated, no anchor (the configuration's setting); paper: "
                         "layers 11-17 regulated, first frame kept whole in every layer (Sec. 4.1)")
@@ -286,33 +344,54 @@ def main():
                         "own phase), attend over the contiguous arena (rv_attend_staged) and admit by "
                         "in-place compaction (rv_admit_staged_layers)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-samples", type=int, default=24, help="layer-frames the oracle is timed on")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run a 256 MiB device copy before the stream (HBM counter calibration)")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                   help="summarise two rocprofv3 --pmc runs into profiles/ and exit")
+                   help="summarise two rocprofv3 --pmc runs of this command into profiles/ and exit")
     p.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
-                   help="summarise a rocprofv3 --kernel-trace --stats run into profiles/ and exit")
+                   help="summarise a rocprofv3 --kernel-trace --stats run of this command into profiles/ "
+                        "and exit")
     args = p.parse_args()
-    if args.trace_summary:
-        summarize_trace(*args.trace_summary, args.config)
-        return
-    if args.pmc_summary:
-        summarize_pmc(*args.pmc_summary, args.config)
-        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this path has no multi-GPU mode "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
 
-    import torch
-    from paper_2609_23286_amd import rv, synth
-
+    from paper_2609_23286_amd import synth
     cfg = synth.CONFIGS[args.config]
     L, H, N, d, k = cfg.n_layers, cfg.n_heads, cfg.n_tokens, cfg.head_dim, cfg.budget
     if args.gamma is not None:
         k = int(args.gamma * N)
     stride = args.stride or cfg.stride
-    T, W = args.steps, args.warmup
+    n_stream = args.stream_frames or cfg.n_frames
+    K_steps, W = args.steps, args.warmup
+    if not 1 <= K_steps <= n_stream:
+        raise SystemExit(f"--steps must be in [1, {n_stream}] (the stream's length)")
+    full = K_steps == n_stream
+    variant = []
+    if args.policy == "paper":
+        variant.append("paper layer policy: layers 11-17 regulated, first frame kept whole in every layer")
+    if stride != cfg.stride:
+        variant.append(f"{stride}x{stride} query windows")
+    if args.gamma is not None:
+        variant.append(f"gamma {args.gamma}")
+    if args.shared:
+        variant.append("head-averaged selection")
+    if args.staged:
+        variant.append("frames staged in the arenas by a copy kernel (timed as staging_ms, inside the "
+                       "wall clock), attention over the contiguous arena, admission by in-place compaction")
+    wkey = workload_key(cfg, n_stream, K_steps, variant)
+    if args.trace_summary:
+        summarize_trace(*args.trace_summary, wkey or cfg.name)
+        return
+    if args.pmc_summary:
+        summarize_pmc(*args.pmc_summary, wkey or cfg.name)
+        return
+
+    import torch
+    from paper_2609_23286_amd import rv
+
     qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, stride)
     n_q = len(range(0, cfg.grid_h, stride)) * len(range(0, cfg.grid_w, stride))
     anchor = args.policy == "paper"
@@ -320,16 +399,41 @@ def main():
     admit_fn = "rv_admit_layers_shared" if args.shared else "rv_admit_layers"
     if args.staged and args.shared:
         raise SystemExit("--staged supports head-specific selection only")
+
+    def mem_len(l, t):
+        """Rows of layer l's memory when frame t of the stream is attended."""
+        n = cfg.prefill
+        if anchor and t > 0:
+            n += N
+        if l in regulated:
+            n += max(0, t - (1 if anchor else 0)) * k
+        return n
+
+    # Frames: the whole stream in order from its initial memory, or a stratified sample
+    # of it taken longest memory first, each layer's memory cut back (rv_mem_truncate,
+    # host-side only) to the length the frame has in the stream, so the timed frames run
+    # back to back.
+    if full:
+        timed = list(range(n_stream))
+        warm = list(range(min(W, n_stream)))
+    else:
+        timed = sorted(stratified(n_stream, K_steps), reverse=True)
+        warm = sorted(stratified(n_stream, W), reverse=True) if W > 0 else []
+    frame_ids = sorted(set(timed) | set(warm))
+
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
+    rv.init()
 
     frame_bytes = L * 3 * N * H * d * 2
     free, total = torch.cuda.mem_get_info()
-    log(f"{cfg.name}: L={L} H={H} N={N} k={k} frames={T}; inputs {T * frame_bytes / 1e9:.1f} GB, "
+    log(f"{cfg.name}: L={L} H={H} N={N} k={k}; {'whole' if full else 'stratified'} "
+        f"{K_steps} of {n_stream} frames; inputs {len(frame_ids) * frame_bytes / 1e9:.1f} GB, "
         f"device free {free / 1e9:.1f} of {total / 1e9:.1f} GB")
-    if T * frame_bytes > free - 8e9:
-        raise SystemExit("not enough device memory to keep every frame's inputs resident")
+    if len(frame_ids) * frame_bytes > free - 16e9:
+        raise SystemExit("not enough device memory to keep every timed frame's inputs resident "
+                         "(time fewer --steps: they are a stratified sample of the stream)")
 
     if args.copy_calibration:
         x = torch.ones(COPY_CALIBRATION_BYTES // 4, dtype=torch.float32, device=dev)
@@ -340,33 +444,35 @@ def main():
 
     # ---- inputs: every frame resident in HBM --------------------------------------
     t0 = time.perf_counter()
-    frames = []
-    for t in range(T):
+    frames = {}
+    for t in frame_ids:
         buf = torch.empty((L, 3, N, H, d), dtype=torch.int16, device=dev)
         rv.gpu_frame_qkv(cfg, t, buf)
-        frames.append(buf)
+        frames[t] = buf
     torch.cuda.synchronize()
-    log(f"generated {T} frames in {time.perf_counter() - t0:.1f} s")
+    log(f"generated {len(frame_ids)} frames in {time.perf_counter() - t0:.1f} s")
 
-    base = (N if anchor else 0) + cfg.prefill
-    cap = base + T * k + 64 + (N if args.staged else 0)
+    rows_max = [max(mem_len(l, t) for t in frame_ids) for l in range(L)]
+    cap = max(rows_max) + (N if anchor else k) + 64 + (N if args.staged else 0)
     mems = [rv.Memory(H, reserve_tokens=cap, max_tokens=cap) for _ in range(L)]
 
-    def prefill():
-        """Memory contents before frame 0: the configuration's prefilled rows, if any."""
-        for m in mems:
+    def fill_memories(rows_of):
+        """Each layer's memory gets rows_of(l) rows: near-Gaussian N(0, sigma^2) rows drawn
+        like the configuration's prefill (tags 4/5), standing in for prefilled and admitted
+        tokens (attention and admission time do not depend on the values)."""
+        for l, m in enumerate(mems):
             m.reset()
-        if cfg.prefill:
-            for l, m in enumerate(mems):
-                pk = torch.empty((H, cfg.prefill, d), dtype=torch.int16, device=dev)
+            n = rows_of(l)
+            if n:
+                pk = torch.empty((H, n, d), dtype=torch.int16, device=dev)
                 pv = torch.empty_like(pk)
                 rv.gpu_normal(cfg.seed, synth.PREFILL_FRAME, l, synth.TAG_MEMK, pk, cfg.sigma)
                 rv.gpu_normal(cfg.seed, synth.PREFILL_FRAME, l, synth.TAG_MEMV, pv, cfg.sigma)
                 m.write(pk, pv)
-            torch.cuda.synchronize()
+                del pk, pv
+        torch.cuda.synchronize()
 
-    prefill()
-    rv.reserve_workspace(N, H, L)
+    rv.reserve_workspace(N, H, max(rows_max), L)
     out = torch.empty((L, N, H, d), dtype=torch.int16, device=dev)
     lse = torch.empty((L, H, N), dtype=torch.float32, device=dev)
     sal = torch.empty((L, H, N), dtype=torch.float32, device=dev)
@@ -385,23 +491,28 @@ def main():
     lse_arr = arr(*[lse[l].data_ptr() for l in range(L)])
     mem_arr = arr(*[m.handle.value for m in mems])
     views = [m.view() for m in mems]  # capacity is reserved: arenas never move
-    frame_ptrs = []
-    for t in range(T):
+    frame_ptrs = {}
+    for t in frame_ids:
         fb = frames[t]
         qp = [fb[l, 0].data_ptr() for l in range(L)]
         kp = [fb[l, 1].data_ptr() for l in range(L)]
         vpp = [fb[l, 2].data_ptr() for l in range(L)]
-        frame_ptrs.append((qp, kp, vpp, arr(*qp), arr(*kp), arr(*vpp)))
+        frame_ptrs[t] = (qp, kp, vpp, arr(*qp), arr(*kp), arr(*vpp))
 
     reg_arr = lambda ptrs: (vp * len(regulated))(*[ptrs[l] for l in regulated])
     reg_sal = reg_arr([sal[l].data_ptr() for l in range(L)])
     reg_lse = reg_arr([lse[l].data_ptr() for l in range(L)])
     reg_mem = reg_arr([m.handle.value for m in mems])
-    reg_frames = [(reg_arr(f[0]), reg_arr(f[1]), reg_arr(f[2])) for f in frame_ptrs]
+    reg_frames = {t: (reg_arr(f[0]), reg_arr(f[1]), reg_arr(f[2])) for t, f in frame_ptrs.items()}
     admit = getattr(lib, admit_fn)
 
     def run_frame(t, ev=None):
         qp, kp, vpp, qa, ka, va = frame_ptrs[t]
+        if not full:
+            for l in range(L):
+                st = lib.rv_mem_truncate(mems[l].handle, mem_len(l, t))
+                if st:
+                    raise rv.RVError(st, lib.rv_last_error().decode())
         if args.staged:  # the producer's part: the frame's K/V into each arena's tail
             if ev is not None:
                 ev[3].record(stream)
@@ -442,90 +553,79 @@ def main():
         if ev is not None:
             ev[2].record(stream)
 
-    # ---- warmup on frames 0..W-1, then start the stream again from empty memory -----
-    for t in range(min(W, T)):
+    # ---- warm-up, then the timed frames --------------------------------------------
+    initial = (lambda l: mem_len(l, 0)) if full else (lambda l: rows_max[l])
+    fill_memories(initial)
+    for t in warm:
         run_frame(t)
     torch.cuda.synchronize()
-    prefill()
+    if full:
+        fill_memories(initial)  # the stream starts again from its initial memory
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(T)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in timed]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    for t in range(T):
-        run_frame(t, events[t])
-        if (t + 1) % 250 == 0:
-            log(f"enqueued {t + 1} frames")
+    for i, t in enumerate(timed):
+        run_frame(t, events[i])
+        if (i + 1) % 250 == 0:
+            log(f"enqueued {i + 1} frames")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     rv.device_status()
+    if full:
+        assert all(m.len == mem_len(l, n_stream) for l, m in enumerate(mems))
 
-    def mem_len(l, t):
-        """Rows of layer l's memory when frame t is attended."""
-        n = cfg.prefill
-        if anchor and t > 0:
-            n += N
-        if l in regulated:
-            n += max(0, t - (1 if anchor else 0)) * k
-        return n
-
-    assert all(m.len == mem_len(l, T) for l, m in enumerate(mems))
-
-    for f in sorted({0, T // 2, T - 1}):
-        log(f"frame {f}: attention {events[f][0].elapsed_time(events[f][1]) * 1e3 / L:.1f} us/launch "
-            f"(context {mem_len(regulated[0] if regulated else 0, f) + N}), "
-            f"admission {events[f][1].elapsed_time(events[f][2]) * 1e3:.1f} us")
+    for i in sorted({0, len(timed) // 2, len(timed) - 1}):
+        t = timed[i]
+        log(f"frame {t}: attention {events[i][0].elapsed_time(events[i][1]) * 1e3 / L:.1f} us/launch "
+            f"(context {mem_len(regulated[0] if regulated else 0, t) + N}), "
+            f"admission {events[i][1].elapsed_time(events[i][2]) * 1e3:.1f} us")
     attn_ms = sum(e[0].elapsed_time(e[1]) for e in events)
     admit_ms = sum(e[1].elapsed_time(e[2]) for e in events)
     stage_ms = sum(e[3].elapsed_time(e[0]) for e in events) if args.staged else None
-    flops = sum(attention_flops(N, H, d, mem_len(l, t) + N) for t in range(T) for l in range(L))
-    n_attn = T * L
+    n_timed = len(timed)
+    flops = sum(attention_flops(N, H, d, mem_len(l, t) + N) for t in timed for l in range(L))
+    n_attn = n_timed * L
     attn_avg_s = attn_ms / 1e3 / n_attn
     achieved_tf = flops / n_attn / attn_avg_s / 1e12
     bytes_admit = sum(admit_bytes(N, H, d, n_q, N) * L if (anchor and t == 0)
-                      else admit_bytes(N, H, d, n_q, k) * len(regulated) for t in range(T))
+                      else admit_bytes(N, H, d, n_q, k) * len(regulated) for t in timed)
     admit_gbs = bytes_admit / (admit_ms / 1e3) / 1e9
-    log(f"timed {T} frames in {elapsed:.3f} s: attention {attn_ms:.1f} ms "
+    log(f"timed {n_timed} frames in {elapsed:.3f} s: attention {attn_ms:.1f} ms "
         f"({attn_avg_s * 1e6:.1f} us/launch, {achieved_tf:.1f} TFLOP/s), admission {admit_ms:.1f} ms "
-        f"({admit_ms / T * 1e3:.1f} us/frame, {admit_gbs:.0f} GB/s)")
+        f"({admit_ms / n_timed * 1e3:.1f} us/frame, {admit_gbs:.0f} GB/s)")
 
-    mean_ctx = sum(mem_len(l, t) + N for t in range(T) for l in range(L)) / (T * L)
-    variant = []
-    if args.policy == "paper":
-        variant.append("paper layer policy: layers 11-17 regulated, first frame kept whole in every layer")
-    if stride != cfg.stride:
-        variant.append(f"{stride}x{stride} query windows")
-    if args.gamma is not None:
-        variant.append(f"gamma {args.gamma}")
-    if args.shared:
-        variant.append("head-averaged selection")
-    if args.staged:
-        variant.append("frames staged in the arenas by a copy kernel (timed as staging_ms, inside the "
-                       "wall clock), attention over the contiguous arena, admission by in-place compaction")
-    workload = (f"{cfg.name}: {L} layers x {H} heads x {d}, {N} tokens/frame ({cfg.grid_h}x{cfg.grid_w} "
-                f"patches + {cfg.n_special} special), budget {k}/head/frame, {stride}x{stride} query sampling, "
-                f"{T}-frame stream from " + (f"{cfg.prefill} prefilled memory rows" if cfg.prefill else "empty memory")
+    mean_ctx = sum(mem_len(l, t) + N for t in timed for l in range(L)) / n_attn
+    if full:
+        sampling = f"the whole {n_stream}-frame stream in order from "
+        sampling += f"{cfg.prefill} prefilled memory rows" if cfg.prefill else "empty memory"
+    else:
+        sampling = (f"{n_timed} of its {n_stream} frames, stratified (frame t_i = floor((i + 1/2) {n_stream} / "
+                    f"{n_timed})), each at the memory length it has in the stream ({cfg.prefill} prefilled + "
+                    f"{k} per frame), timed back to back longest first")
+    workload = (f"{cfg.name}: {n_stream}-frame stream, {L} layers x {H} heads x {d}, {N} tokens/frame "
+                f"({cfg.grid_h}x{cfg.grid_w} patches + {cfg.n_special} special), budget {k}/head/frame, "
+                f"{stride}x{stride} query sampling; {sampling}; mean context {mean_ctx:.0f}"
                 + "".join("; " + v for v in variant))
-    # counter profiles are recorded for the configurations' own settings only
-    wkey = cfg.name if not variant else None
     result = {
-        "metric": "frames/sec (attend+saliency+admit, 24 layers) at 1000-frame stream",
-        "value": T / elapsed,
+        "metric": f"frames/sec (attend+saliency+admit, {L} layers) at {n_stream}-frame stream; % MFMA/HBM peak",
+        "value": n_timed / elapsed,
         "unit": "frames/s",
         "n_gpus": 1,
-        "steps": T,
+        "steps": n_timed,
         "warmup": W,
-        "ms_per_step": elapsed / T * 1e3,
+        "ms_per_step": elapsed / n_timed * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded Philox streams of ViT-L token shape, 1% planted salient keys)",
         "config": {"workload": workload, "layers": L, "heads": H, "head_dim": d, "tokens_per_frame": N,
-                   "budget": k, "frames": T, "sampled_queries": n_q, "query_window": stride,
+                   "budget": k, "stream_frames": n_stream, "timed_frames": timed if not full else "all",
+                   "mean_context": mean_ctx, "sampled_queries": n_q, "query_window": stride,
                    "regulated_layers": len(regulated), "anchor": anchor,
                    "selection": "head-averaged" if args.shared else "head-specific",
-                   "staged_frames": bool(args.staged),
-                   "prefill_rows": cfg.prefill},
+                   "staged_frames": bool(args.staged), "prefill_rows": cfg.prefill},
         "roofline": {"kernel": "attn_fwd_kernel (+ attn_merge_kernel on split plans)", "bound": "mfma",
                      "achieved": achieved_tf,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved_tf / PEAK_BF16_TFLOPS,
@@ -538,13 +638,17 @@ def main():
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": admit_gbs / PEAK_HBM_GBS,
                                           "traffic": admission_traffic(wkey) if wkey else None,
-                                          "algorithmic_bytes_per_launch": bytes_admit / T}},
+                                          "algorithmic_bytes_per_launch": bytes_admit / n_timed}},
     }
-    if not args.no_cpu_baseline:
-        log("timing the oracle on a host sample ...")
-        result["cpu_baseline"] = cpu_baseline(cfg, mean_ctx, T, k, qs)
     for m in mems:
         m.close()
+    del frames
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a host sample ...")
+        ns = max(1, args.cpu_samples)
+        samples = [(i % L, t) for i, t in enumerate(stratified(n_stream, ns))]
+        samples = [(regulated[i % len(regulated)] if regulated else l, t) for i, (l, t) in enumerate(samples)]
+        result["cpu_baseline"] = cpu_baseline(cfg, samples, k, qs, mem_len, mean_ctx)
     print(json.dumps(result), flush=True)
 
 

@@ -23,6 +23,11 @@
  *   - head_dim must be 64 (the ViT-L aggregator's 1024 / 16).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream) and is
  *     asynchronous; nothing here synchronises the device except where stated.
+ *   - Set-up: rv_init (or rv_mem_create, or rv_reserve_workspace, which call it) must
+ *     have run on the current device before a compute call.  It records the device's
+ *     limits and allocates the scratch workspace, so that the compute calls
+ *     (rv_attend_frame, rv_attend_staged, rv_admit*) never allocate scratch memory or
+ *     synchronise; only the memory arenas grow, inside rv_admit* and rv_mem_* calls.
  *   - Every argument is checked before anything is enqueued.  On failure the call
  *     returns a non-zero rv_status, enqueues nothing, changes no state, and
  *     rv_last_error() describes the problem.  A fault in an earlier kernel surfaces as
@@ -81,6 +86,13 @@ const char *rv_last_error(void);
 /* Library version string. */
 const char *rv_version(void);
 
+/* Initialises librv on the current device (idempotent): reads its CU count and LDS
+ * limit, counts its XCDs with a probe launch, and allocates the split-KV workspace that
+ * every default attention work plan fits (about 18 MB on an MI355X; see
+ * rv_reserve_workspace for plans forced through the RV_ATTN_* overrides).  Synchronises
+ * the device.  Compute calls on a device where it has not run return RV_ERR_INVALID. */
+rv_status rv_init(void);
+
 /* ---- memory (Sec. 3.3 Eq. 4-6) ---------------------------------------------------- */
 
 /* Creates an empty memory on the current device with room for reserve_tokens rows per
@@ -109,6 +121,11 @@ rv_status rv_mem_reserve(rv_mem m, int64_t tokens, void *stream);
 
 /* Sets the length to 0 (arena contents are left as they are). */
 rv_status rv_mem_reset(rv_mem m);
+
+/* Drops the newest rows: sets the length to n_rows, 0 <= n_rows <= length (RV_ERR_INVALID
+ * otherwise), e.g. to roll a memory back to an earlier frame.  Rows past the new length
+ * keep their contents until overwritten.  Host-side only: no device work. */
+rv_status rv_mem_truncate(rv_mem m, int64_t n_rows);
 
 /* Overwrites rows 0..n_rows-1 of every head with K, V ([n_heads][n_rows][head_dim]
  * bf16, host or device memory) and sets the length to n_rows; provenance of these rows
@@ -148,10 +165,13 @@ rv_status rv_mem_load(rv_mem m, const char *path);
  * saliency: NULL, or [n_heads][n_tokens] fp32 that receives, for every frame key j,
  *   S_j = sum over sampled queries i (per *qs) of exp(z_ij - LSE_i)     (Sec. 3.3),
  * in which case qs must be given and describe n_tokens.
+ * (A subset with no window -- grid_h or grid_w 0 -- gives S_j = 0, the empty sum.)
  * Arithmetic: bf16 inputs, fp32 logits and softmax, probabilities rounded to bf16 for
  * the value product, fp32 accumulation, out rounded to bf16 (nearest-even).
- * n_tokens 0 is a no-op.  May allocate its split-KV workspace on first use (see
- * rv_reserve_workspace). */
+ * n_tokens 0 is a no-op.  Allocates nothing and does not synchronise: split-KV partial
+ * results go to the workspace rv_init allocated (RV_ERR_INVALID if rv_init has not run
+ * on this device; RV_ERR_CAPACITY if an RV_ATTN_* override forces a plan with more
+ * partial slots than rv_reserve_workspace provided). */
 rv_status rv_attend_frame(const void *Q, const void *K, const void *V, int n_tokens,
                           const void *memK, const void *memV, int64_t mem_len,
                           int64_t head_stride_tokens, int n_heads, int head_dim,
@@ -178,7 +198,9 @@ rv_status rv_admit(const float *saliency, int budget, const void *K, const void 
  * the next frame on).  Q, K, V, lse, mems: host arrays of n_layers device pointers /
  * handles.  saliency_out, idx_out: NULL, or host arrays of n_layers device pointers
  * ([n_heads][n_tokens] fp32, [n_heads][budget] int32), each of which may be NULL.
- * All layers share n_heads, n_tokens, qs, budget.  1 <= n_layers <= 4096. */
+ * All layers share n_heads, n_tokens, qs, budget.  1 <= n_layers <= 4096.  Without a
+ * saliency output for every layer the workspace's saliency staging is used: it must hold
+ * min(n_layers, 24) layers' values (rv_reserve_workspace), else RV_ERR_CAPACITY. */
 rv_status rv_admit_layers(int n_layers, const void *const *Q, const void *const *K,
                           const void *const *V, const float *const *lse, int n_tokens,
                           const rv_qsub *qs, int budget, const rv_mem *mems, int frame_id,
@@ -264,11 +286,14 @@ typedef struct rv_attn_plan {
 rv_status rv_attention_plan(int n_tokens, int n_fkeys, int64_t mem_len, int n_heads, int n_cus,
                             int n_queues, rv_attn_plan *out);
 
-/* Pre-allocates the current device's scratch workspace (split-KV partial results,
- * saliency staging) for frames of up to n_tokens tokens with
- * n_heads heads, and up to n_layers layers per rv_admit_layers call, so that later
- * calls within those sizes do not allocate. */
-rv_status rv_reserve_workspace(int n_tokens, int n_heads, int n_layers);
+/* Grows the current device's scratch workspace (calling rv_init first if needed): the
+ * split-KV partial slots of the work plan for frames of n_tokens tokens and n_heads heads
+ * over memories of up to max_mem_len rows -- the default plans fit the workspace rv_init
+ * allocates; plans forced through RV_ATTN_SPLIT may need more -- and the saliency
+ * staging that rv_admit_layers* use when the caller passes no saliency output, for up to
+ * n_layers layers per call.  The workspace never shrinks.  Synchronises the device when
+ * it replaces a buffer. */
+rv_status rv_reserve_workspace(int n_tokens, int n_heads, int64_t max_mem_len, int n_layers);
 
 #ifdef __cplusplus
 }

@@ -28,7 +28,7 @@ def _hipcc(out, sources, verbose, extra=()):
 
 
 def build(verbose: bool = False):
-    _hipcc(LIB, [os.path.join(CSRC, f) for f in ("rv_host.cpp", "attend.hip", "admit.hip")], verbose,
+    _hipcc(LIB, [os.path.join(CSRC, f) for f in ("rv_host.cpp", "rv_plan.cpp", "attend.hip", "admit.hip")], verbose,
            KERNEL_FLAGS)
     _hipcc(SYNTH_LIB, [os.path.join(CSRC, "synth_gpu.hip")], verbose)
     return LIB, SYNTH_LIB

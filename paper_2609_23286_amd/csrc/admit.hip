@@ -39,7 +39,7 @@ constexpr int NT = kAdmitThreads;  // 256
 constexpr int NW = NT / 64;
 constexpr int kBlocksPerStep = 2;  // 32-key blocks a saliency wave holds at once
 static_assert(kBlocksPerStep == 2, "a range's last step holds one block or two");
-constexpr int QS_STRIDE = D + 8;   // staged sampled-query rows, 144 bytes
+constexpr int QS_STRIDE = kSalQStride;  // staged sampled-query rows, 144 bytes
 constexpr int kStageBatch = 9;     // 16-byte query-row loads in flight per thread (one pass of 288 rows)
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kScaleLog2 = kLog2e * 0.125f;
@@ -71,6 +71,10 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
   const float* lse_h = L.lse + (int64_t)h * N;
   float* sal_h = L.sal + (int64_t)h * N;
   const int nq_pad = (a.n_q + 31) & ~31;
+  if (nq_pad == 0) {  // no sampled queries: every key's saliency is the empty sum
+    for (int j = blk0 * 32 + tid; j < min(N, blk1 * 32); j += NT) sal_h[j] = 0.f;
+    return;
+  }
   float* s_lse2 = reinterpret_cast<float*>(smem);
   uint16_t* s_q = reinterpret_cast<uint16_t*>(smem + (size_t)nq_pad * 4);
 
@@ -514,15 +518,6 @@ __global__ __launch_bounds__(NT) void select_kernel(AdmitArgs a) {
   }
 }
 
-size_t sal_lds_bytes(const AdmitArgs& a) {
-  const size_t nq_pad = (size_t)((a.n_q + 31) & ~31);
-  return nq_pad * 4 + (a.stage_queries ? (size_t)a.q_pass * QS_STRIDE * 2 : 0);
-}
-
-size_t select_lds_bytes(const AdmitArgs& a) {
-  return (((size_t)a.n_tokens * 4 + 15) & ~(size_t)15) + (size_t)a.budget * 4;
-}
-
 hipError_t set_lds_limit(const void* kernel, int* cached, int limit) {
   if (*cached == limit) return hipSuccess;
   const hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, limit);
@@ -531,39 +526,6 @@ hipError_t set_lds_limit(const void* kernel, int* cached, int limit) {
 }
 
 }  // namespace
-
-size_t admit_lds_bytes(const AdmitArgs& a) {
-  size_t need = 0;
-  if (a.mode & kModeSaliency) need = sal_lds_bytes(a);
-  if ((a.mode & kModeSelect) && select_lds_bytes(a) > need) need = select_lds_bytes(a);
-  return need;
-}
-
-int admit_max_dynamic_lds(int max_lds) { return max_lds - kAdmitStaticLdsMargin; }
-
-void plan_saliency(AdmitArgs* a, int n_lh, int n_cus, int max_lds) {
-  // About three 4-wave workgroups per CU over the launch, and at least one 32-key
-  // block per wave.
-  const int n_blocks = (a->n_tokens + 31) / 32;
-  const int max_groups = n_blocks / NW > 1 ? n_blocks / NW : 1;
-  int g = (3 * n_cus + n_lh - 1) / (n_lh > 0 ? n_lh : 1);
-  a->sal_groups = g < 1 ? 1 : (g > max_groups ? max_groups : g);
-  // Sampled query rows are staged in passes of q_pass rows, sized so that three
-  // workgroups fit a CU's LDS; the pass size depends only on n_q and the device, so
-  // every launch of the same frame shape sums in the same order.
-  const int nq_pad = (a->n_q + 31) & ~31;
-  const long budget_lds = (long)max_lds / 3 - kAdmitStaticLdsMargin - (long)nq_pad * 4;
-  const int fit = budget_lds > 0 ? (int)(budget_lds / (QS_STRIDE * 2)) & ~31 : 0;
-  if (fit >= 32) {
-    const int passes = (nq_pad + fit - 1) / fit;
-    a->q_pass = ((nq_pad + passes - 1) / passes + 31) & ~31;
-    a->stage_queries = 1;
-  } else {
-    a->q_pass = nq_pad;
-    a->stage_queries = 0;
-  }
-  if (sal_lds_bytes(*a) > (size_t)admit_max_dynamic_lds(max_lds)) a->stage_queries = 0;
-}
 
 hipError_t launch_admit(const AdmitArgs& a, int max_lds, hipStream_t s) {
   static int sal_attr = 0, sel_attr = 0;

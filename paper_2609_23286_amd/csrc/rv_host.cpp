@@ -41,22 +41,21 @@ rv_status hip_fail(hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail(e_, what); \
   } while (0)
 
-int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
-
-int env_int(const char* name, int dflt) {
-  const char* v = std::getenv(name);
-  if (!v || !*v) return dflt;
-  return std::atoi(v);
-}
 
 // ---- per-device context: placement calibration, limits, scratch workspace --------
+//
+// Every compute call plans and launches with what rv_init recorded for the current
+// device and writes its split-KV partials into the workspace allocated there, so that
+// no compute call allocates device memory or synchronises.  rv_reserve_workspace is the
+// other call that may allocate (a larger workspace for forced work plans, the saliency
+// staging of rv_admit_layers*).
 struct Workspace {
   bool ready = false;
   int n_cus = 0;
   int max_lds = 0;
   int n_queues = 1;          // attention work queues: one per XCD
-  float* part = nullptr;     // attention partial slots
-  size_t part_floats = 0;
+  float* part = nullptr;     // attention partial slots, kAttnSlotFloats floats each
+  int64_t part_slots = 0;
   float* sal = nullptr;      // saliency staging when the caller passes none
   size_t sal_floats = 0;
 };
@@ -64,22 +63,14 @@ struct Workspace {
 std::mutex g_ws_mu;
 std::map<int, Workspace> g_ws;
 
-template <class T>
-rv_status grow(T** p, size_t* have, size_t need, bool zero, const char* what) {
+// Replaces *p by a buffer of `need` floats if it holds fewer.  Earlier launches may still
+// use the old buffer, so the device is synchronised before it is freed.
+rv_status grow_floats(float** p, size_t* have, size_t need, const char* what) {
   if (*have >= need) return RV_OK;
-  size_t n = std::max(need, *have * 2);
-  T* q = nullptr;
-  hipError_t e = hipMalloc(&q, n * sizeof(T));
+  float* q = nullptr;
+  hipError_t e = hipMalloc(&q, need * sizeof(float));
   if (e != hipSuccess) return hip_fail(e, what);
-  if (zero) {
-    e = hipMemset(q, 0, n * sizeof(T));
-    if (e != hipSuccess) {
-      (void)hipFree(q);
-      return hip_fail(e, what);
-    }
-  }
   if (*p) {
-    // earlier launches may still use the old buffer
     e = hipDeviceSynchronize();
     if (e != hipSuccess) {
       (void)hipFree(q);
@@ -88,14 +79,22 @@ rv_status grow(T** p, size_t* have, size_t need, bool zero, const char* what) {
     (void)hipFree(*p);
   }
   *p = q;
-  *have = n;
+  *have = need;
   return RV_OK;
 }
 
-// Reads the CU count and the LDS limit, and counts the XCDs (distinct XCC ids seen by
-// a probe launch): the attention kernel keeps one work queue per XCD so that the query
-// tiles of a head share an L2.  Placement only steers locality; results never depend
-// on it.
+rv_status reserve_partials(Workspace* ws, int64_t slots) {
+  if (slots <= ws->part_slots) return RV_OK;
+  size_t have = (size_t)ws->part_slots * rv::kAttnSlotFloats;
+  rv_status st = grow_floats(&ws->part, &have, (size_t)slots * rv::kAttnSlotFloats, "attention workspace");
+  if (st == RV_OK) ws->part_slots = slots;
+  return st;
+}
+
+// Reads the CU count and the LDS limit, counts the XCDs (distinct XCC ids seen by a
+// probe launch: the attention kernel keeps one work queue per XCD so that the query
+// tiles of a head share an L2; placement only steers locality, results never depend on
+// it), and allocates the partial slots of every default work plan.  Synchronous.
 rv_status init_device(Workspace* ws, int dev) {
   if (ws->ready) return RV_OK;
   RV_HIP(hipDeviceGetAttribute(&ws->n_cus, hipDeviceAttributeMultiprocessorCount, dev), "CU count");
@@ -112,11 +111,14 @@ rv_status init_device(Workspace* ws, int dev) {
   for (int id : ids)
     if (std::find(distinct.begin(), distinct.end(), id) == distinct.end()) distinct.push_back(id);
   ws->n_queues = std::max(1, std::min((int)distinct.size(), rv::kMaxQueues));
+  rv_status st = reserve_partials(ws, rv::default_partial_slots(ws->n_cus, ws->n_queues));
+  if (st != RV_OK) return st;
   ws->ready = true;
   return RV_OK;
 }
 
-rv_status current_ws(Workspace** out) {
+// The current device's context, initialised if need be (set-up calls only).
+rv_status setup_ws(Workspace** out) {
   int dev = 0;
   RV_HIP(hipGetDevice(&dev), "hipGetDevice");
   Workspace* ws = &g_ws[dev];
@@ -126,114 +128,21 @@ rv_status current_ws(Workspace** out) {
   return RV_OK;
 }
 
-// Sampled queries (Sec. 3.3, head-specific retention): query i of the subset is frame
-// token q_base + (i / q_cols) * q_row_stride + (i % q_cols) * q_col_stride, the
-// top-left patch of the i-th stride x stride window in row-major window order.
-void set_qsub(rv::AdmitArgs* b, const rv_qsub& q) {
-  const int rows = (q.grid_h + q.stride - 1) / q.stride;
-  const int cols = (q.grid_w + q.stride - 1) / q.stride;
-  b->n_q = rows * cols;
-  b->q_cols = cols > 0 ? cols : 1;
-  b->q_base = q.n_special;
-  b->q_row_stride = q.stride * q.grid_w;
-  b->q_col_stride = q.stride;
-}
-
-rv_status check_qsub(const rv_qsub* qs, int n_tokens) {
-  if (!qs) return fail(RV_ERR_INVALID, "query subset descriptor is NULL");
-  if (qs->grid_h < 0 || qs->grid_w < 0 || qs->n_special < 0 || qs->stride < 1)
-    return fail(RV_ERR_INVALID, "query subset has negative sizes or stride < 1");
-  if ((int64_t)qs->grid_h * qs->grid_w + qs->n_special != n_tokens)
-    return fail(RV_ERR_INVALID, "query subset %dx%d+%d does not describe %d tokens", qs->grid_h,
-                qs->grid_w, qs->n_special, n_tokens);
+// The current device's context for a compute call: it must have been initialised.
+rv_status ready_ws(Workspace** out) {
+  int dev = 0;
+  RV_HIP(hipGetDevice(&dev), "hipGetDevice");
+  auto it = g_ws.find(dev);
+  if (it == g_ws.end() || !it->second.ready)
+    return fail(RV_ERR_INVALID, "librv is not initialised on device %d: call rv_init() first", dev);
+  *out = &it->second;
   return RV_OK;
 }
 
-// Work plan of one attention launch: units (head, 128-query tile) are dealt in
-// contiguous ranges to the per-XCD queues, and each queue's (unit, key tile) iterations
-// are cut into chunks, one per workgroup, about kAttnWgPerCu per CU: the first n_first
-// chunks of a queue hold E tiles, the others E1 (E1 = E and n_first = 0 unless
-// stream-K).  k-way split: each unit's key range is cut into k aligned pieces
-// (iteration stride U = k E per unit), so the workgroups on one head's query tiles
-// stream the same key tiles together.  Stream-K: U = T, chunks may straddle units.
-// RV_ATTN_SPLIT forces one (0: stream-K, k > 0: k-way).
-struct AttnPlan {
-  int q_tiles, nt_mem, T, U, n_units, E, E1, n_first, grid, total_chunks;
-  int unit_base[rv::kMaxQueues + 1];
-  int n_chunks[rv::kMaxQueues];
-  int chunk_base[rv::kMaxQueues];
-};
-
-// n_tokens queries; keys: mem_len memory rows, then n_fkeys frame rows.
-AttnPlan plan_attention(const Workspace& ws, int n_tokens, int n_fkeys, int64_t mem_len, int n_heads) {
-  AttnPlan p{};
-  p.q_tiles = (int)ceil_div(n_tokens, rv::kAttnBQ);
-  p.nt_mem = (int)ceil_div(mem_len, rv::kAttnBK);
-  p.T = p.nt_mem + (int)ceil_div(n_fkeys, rv::kAttnBK);
-  p.n_units = p.q_tiles * n_heads;
-  const int nq = ws.n_queues;
-  const int wg_per_queue =
-      std::max(1, env_int("RV_ATTN_WG_PER_CU", rv::kAttnWgPerCu) * ws.n_cus / nq);
-  int max_units = 0;
-  for (int q = 0; q <= nq; ++q) p.unit_base[q] = (int)((int64_t)q * p.n_units / nq);
-  for (int q = 0; q < nq; ++q) max_units = std::max(max_units, p.unit_base[q + 1] - p.unit_base[q]);
-  const int e_min = std::max(1, env_int("RV_ATTN_MIN_CHUNK", 2));
-  // Stream-K balances the tiles exactly but pays, per chunk that straddles two units, a
-  // second pipeline start; the aligned split leaves some workgroup slots idle.  Take the
-  // split while its chunks are at most kSplitSlackTiles longer than stream-K's.
-  constexpr int kSplitSlackTiles = 1;
-  // Tiles of a first-dispatched stream-K chunk, in per cent of a later chunk's.
-  constexpr int kFirstChunkPct = 140;
-  int k = env_int("RV_ATTN_SPLIT", -1);
-  if (k < 0) {
-    k = wg_per_queue / std::max(1, max_units);
-    const int64_t e_sk = ceil_div((int64_t)max_units * p.T, wg_per_queue);
-    if (k >= 1 && ceil_div(p.T, k) > e_sk + env_int("RV_ATTN_SPLIT_SLACK", kSplitSlackTiles)) k = 0;
-  }
-  p.n_first = 0;
-  if (k >= 1) {
-    p.E = (int)std::max<int64_t>(e_min, ceil_div(p.T, k));
-    k = (int)ceil_div(p.T, p.E);  // pieces that hold tiles
-    p.U = k * p.E;
-    p.E1 = p.E;
-  } else {
-    // Stream-K.  Workgroup ids are dealt round-robin over the XCDs and then over the
-    // CUs, so a queue's first n_cus / nq chunks go to the workgroups dispatched first
-    // on their CUs, which run measurably faster than the second ones: those chunks get
-    // kFirstChunkPct per cent of the later chunks' tiles (a speed heuristic only; any
-    // placement gives the same results).
-    p.U = p.T;
-    const int64_t work = (int64_t)max_units * p.T;
-    const int pct = std::max(100, env_int("RV_ATTN_FIRST_PCT", kFirstChunkPct));
-    // (no second workgroup per CU to favour the first over: uniform chunks)
-    const int n_first = ws.n_cus / nq < wg_per_queue ? std::max(0, ws.n_cus / nq) : 0;
-    const int n_rest = wg_per_queue - n_first;
-    p.E1 = (int)std::max<int64_t>(e_min, ceil_div(work * 100, (int64_t)n_first * pct + (int64_t)n_rest * 100));
-    p.E = (int)std::max<int64_t>(e_min, ceil_div((int64_t)p.E1 * pct, 100));
-    p.n_first = p.E == p.E1 ? 0 : n_first;
-    if (p.n_first == 0) p.E = p.E1;  // (no first workgroups to favour)
-  }
-  p.total_chunks = 0;
-  int max_chunks = 0;
-  for (int q = 0; q < nq; ++q) {
-    const int64_t iters = (int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.U;
-    const int64_t first = (int64_t)p.n_first * p.E;
-    p.n_chunks[q] = iters <= first ? (int)ceil_div(iters, p.E) : p.n_first + (int)ceil_div(iters - first, p.E1);
-    p.chunk_base[q] = p.total_chunks;
-    p.total_chunks += p.n_chunks[q];
-    max_chunks = std::max(max_chunks, p.n_chunks[q]);
-  }
-  if (max_chunks <= p.n_first) {  // every chunk is a first one: say so plainly
-    p.n_first = 0;
-    p.E1 = p.E;
-  }
-  p.grid = nq * max_chunks;
-  return p;
-}
-
-rv_status reserve_attention(Workspace* ws, const AttnPlan& p) {
-  return grow(&ws->part, &ws->part_floats, (size_t)2 * p.total_chunks * rv::kAttnSlotFloats, false,
-              "attention workspace");
+rv_status check_qsub(const rv_qsub* qs, int n_tokens) {
+  const char* why = rv::qsub_problem(qs, n_tokens);
+  if (why) return fail(RV_ERR_INVALID, "%s", why);
+  return RV_OK;
 }
 
 }  // namespace
@@ -333,6 +242,12 @@ rv_status rv_mem_create(int n_heads, int head_dim, int64_t reserve_tokens, int64
   if (head_dim != rv::kHeadDim) return fail(RV_ERR_INVALID, "head_dim must be 64 (got %d)", head_dim);
   if (reserve_tokens < 0 || max_tokens < 0 || reserve_tokens > max_tokens)
     return fail(RV_ERR_INVALID, "need 0 <= reserve_tokens <= max_tokens");
+  {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    Workspace* ws;
+    rv_status st = setup_ws(&ws);
+    if (st != RV_OK) return st;
+  }
   rv_mem m = new (std::nothrow) rv_mem_s;
   if (!m) return fail(RV_ERR_OOM, "host allocation failed");
   hipError_t e = hipGetDevice(&m->device);
@@ -389,6 +304,15 @@ rv_status rv_mem_reserve(rv_mem m, int64_t tokens, void* stream) {
 rv_status rv_mem_reset(rv_mem m) {
   if (!m) return fail(RV_ERR_INVALID, "memory is NULL");
   m->len = 0;
+  return RV_OK;
+}
+
+rv_status rv_mem_truncate(rv_mem m, int64_t n_rows) {
+  if (!m) return fail(RV_ERR_INVALID, "memory is NULL");
+  if (n_rows < 0 || n_rows > m->len)
+    return fail(RV_ERR_INVALID, "n_rows must be in [0, length %lld] (got %lld)", (long long)m->len,
+                (long long)n_rows);
+  m->len = n_rows;
   return RV_OK;
 }
 
@@ -524,10 +448,7 @@ rv_status rv_attention_plan(int n_tokens, int n_fkeys, int64_t mem_len, int n_he
   if (n_tokens < 1 || n_tokens > rv::kMaxTokens || n_fkeys < 0 || n_fkeys > n_tokens || mem_len < 0 ||
       n_heads < 1 || n_cus < 1 || n_queues < 1 || n_queues > rv::kMaxQueues)
     return fail(RV_ERR_INVALID, "plan sizes out of range");
-  Workspace ws;
-  ws.n_cus = n_cus;
-  ws.n_queues = n_queues;
-  const AttnPlan p = plan_attention(ws, n_tokens, n_fkeys, mem_len, n_heads);
+  const rv::AttnPlan p = rv::plan_attention(n_cus, n_queues, n_tokens, n_fkeys, mem_len, n_heads);
   *out = rv_attn_plan{};
   out->n_units = p.n_units;
   out->q_tiles = p.q_tiles;
@@ -547,26 +468,28 @@ rv_status rv_attention_plan(int n_tokens, int n_fkeys, int64_t mem_len, int n_he
   return RV_OK;
 }
 
-rv_status rv_reserve_workspace(int n_tokens, int n_heads, int n_layers) {
-  if (n_tokens < 1 || n_tokens > rv::kMaxTokens || n_heads < 1 || n_layers < 1)
+rv_status rv_init(void) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace* ws;
+  return setup_ws(&ws);
+}
+
+rv_status rv_reserve_workspace(int n_tokens, int n_heads, int64_t max_mem_len, int n_layers) {
+  if (n_tokens < 1 || n_tokens > rv::kMaxTokens || n_heads < 1 || n_layers < 1 || max_mem_len < 0)
     return fail(RV_ERR_INVALID, "bad workspace sizes");
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace* ws;
-  rv_status st = current_ws(&ws);
+  rv_status st = setup_ws(&ws);
   if (st != RV_OK) return st;
-  // the chunk count of a plan does not grow with the context: plan a long one
-  const AttnPlan p = plan_attention(*ws, n_tokens, n_tokens, (int64_t)1 << 20, n_heads);
-  st = reserve_attention(ws, p);
+  // the chunk count of a forced plan may grow with the context; a default plan's never does
+  const rv::AttnPlan p = rv::plan_attention(ws->n_cus, ws->n_queues, n_tokens, n_tokens, max_mem_len, n_heads);
+  st = reserve_partials(ws, rv::plan_partial_slots(p));
   if (st != RV_OK) return st;
-  return grow(&ws->sal, &ws->sal_floats,
-              (size_t)std::min(n_layers, rv::kMaxLayersPerLaunch) * n_heads * n_tokens, false, "saliency workspace");
+  return grow_floats(&ws->sal, &ws->sal_floats,
+                     (size_t)std::min(n_layers, rv::kMaxLayersPerLaunch) * n_heads * n_tokens, "saliency workspace");
 }
 
 rv_status rv_device_status(void) {
-  std::lock_guard<std::mutex> lk(g_ws_mu);
-  Workspace* ws;
-  rv_status st = current_ws(&ws);
-  if (st != RV_OK) return st;
   RV_HIP(hipDeviceSynchronize(), "device synchronisation");
   RV_HIP(hipGetLastError(), "device status");
   return RV_OK;
@@ -585,12 +508,15 @@ rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens,
                       int64_t s_head, hipStream_t s) {
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace* ws;
-  rv_status st = current_ws(&ws);
+  rv_status st = ready_ws(&ws);
   if (st != RV_OK) return st;
 
-  const AttnPlan p = plan_attention(*ws, n_tokens, n_fkeys, mem_len, n_heads);
-  st = reserve_attention(ws, p);
-  if (st != RV_OK) return st;
+  const rv::AttnPlan p = rv::plan_attention(ws->n_cus, ws->n_queues, n_tokens, n_fkeys, mem_len, n_heads);
+  if (rv::plan_partial_slots(p) > ws->part_slots)
+    return fail(RV_ERR_CAPACITY,
+                "the work plan needs %lld attention partial slots, the workspace holds %lld "
+                "(a forced plan: call rv_reserve_workspace with this frame's sizes)",
+                (long long)rv::plan_partial_slots(p), (long long)ws->part_slots);
 
   rv::AttnArgs a{};
   a.Q = (const uint16_t*)Q;
@@ -621,8 +547,7 @@ rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens,
     a.chunk_base[q] = p.chunk_base[q];
   }
   // every unit whole in one chunk (no split) needs no merge launch
-  const bool split = (int64_t)p.E < p.T || p.U != p.T || (int64_t)p.T % p.E != 0 || p.E1 != p.E;
-  RV_HIP(rv::launch_attention(a, p.grid, split, s), "attention launch");
+  RV_HIP(rv::launch_attention(a, p.grid, rv::plan_splits_units(p), s), "attention launch");
 
   if (saliency) {
     rv::AdmitArgs b{};
@@ -632,7 +557,7 @@ rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens,
     b.layer[0].kv_head = s_head;
     b.layer[0].lse = lse;
     b.layer[0].sal = saliency;
-    set_qsub(&b, *qs);
+    rv::set_qsub(&b, *qs);
     b.n_tokens = n_tokens;
     b.n_heads = n_heads;
     b.n_layers = 1;
@@ -733,7 +658,7 @@ rv_status rv_admit(const float* saliency, int budget, const void* K, const void*
   hipStream_t s = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace* ws;
-  st = current_ws(&ws);
+  st = ready_ws(&ws);
   if (st != RV_OK) return st;
   st = arena_reserve(m, m->len + budget, s);
   if (st != RV_OK) return st;
@@ -796,10 +721,10 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
   hipStream_t s = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace* ws;
-  st = current_ws(&ws);
+  st = ready_ws(&ws);
   if (st != RV_OK) return st;
   rv::AdmitArgs probe{};
-  set_qsub(&probe, *qs);
+  rv::set_qsub(&probe, *qs);
   probe.n_tokens = n_tokens;
   probe.budget = budget;
   probe.mode = rv::kModeBoth;
@@ -812,10 +737,11 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
   const int chunk_layers = std::min(n_layers, rv::kMaxLayersPerLaunch);
   bool need_ws_sal = !saliency_out;
   for (int l = 0; saliency_out && l < n_layers; ++l) need_ws_sal |= !saliency_out[l];
-  if (need_ws_sal) {
-    st = grow(&ws->sal, &ws->sal_floats, (size_t)chunk_layers * H * n_tokens, false, "saliency workspace");
-    if (st != RV_OK) return st;
-  }
+  if (need_ws_sal && ws->sal_floats < (size_t)chunk_layers * H * n_tokens)
+    return fail(RV_ERR_CAPACITY,
+                "no saliency output given and the saliency workspace holds %zu values, %zu needed "
+                "(call rv_reserve_workspace with n_layers >= %d)",
+                ws->sal_floats, (size_t)chunk_layers * H * n_tokens, chunk_layers);
   // growth for every layer before anything is enqueued (a staged memory has its room)
   for (int l = 0; !staged && l < n_layers; ++l) {
     st = arena_reserve(mems[l], mems[l]->len + budget, s);

@@ -1,0 +1,158 @@
+// rv_plan.h -- librv's kernel argument blocks and the host-side work planning that fills
+// them (not installed).  Plain C++ with no HIP dependency, so the planning logic also
+// builds with a host compiler alone (the sanitizer build of the tests does that).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/rv.h"
+
+namespace rv {
+
+constexpr int kHeadDim = 64;     // head dimension supported by every kernel
+constexpr int kAttnBQ = 128;     // queries per attention workgroup (4 waves x 32)
+constexpr int kAttnBK = 64;      // keys per staged K/V tile
+constexpr int kAttnThreads = 256;
+constexpr int kAdmitThreads = 256;  // saliency and selection workgroups
+constexpr int kMaxTokens = 16384;  // frame size limit (LDS-resident sampled queries and selected indices)
+constexpr int kMaxLayersPerLaunch = 24;
+
+constexpr int kMaxQueues = 16;     // work queues (one per XCD) in the attention kernel
+constexpr int kAttnWgPerCu = 2;    // attention workgroups resident per CU
+
+// Attention forward with per-query LSE over [memory ; frame], XCD-local stream-K.
+//
+// A unit is (head, 128-query tile); its context is T key tiles of 64 keys.  Units are
+// dealt to per-XCD queues (contiguous unit ranges); each queue's (unit, key tile)
+// iteration space is cut into chunks of E tiles, chunk c of queue q going to workgroup
+// c * n_queues + q, which the hardware places on queue q's XCD.
+struct AttnArgs {
+  const uint16_t* Q;       // [N][H][64]
+  const uint16_t* K;
+  const uint16_t* V;
+  const uint16_t* memK;    // [H][head_stride][64]
+  const uint16_t* memV;
+  int64_t mem_len;
+  int64_t head_stride;
+  uint16_t* out;           // [N][H][64]
+  float* lse;              // [H][N]
+  float* part;             // partial slots, kAttnSlotFloats each
+  int n_tokens;            // queries (and, unless staged, the frame's keys)
+  int n_fkeys;             // keys of the frame segment: n_tokens, or 0 when the frame's
+                           // keys are staged in the arena and counted in mem_len
+  int n_heads;
+  int q_tiles;
+  int nt_mem;              // key tiles of the memory segment
+  int T;                   // key tiles per unit (memory + frame)
+  int U;                   // iteration stride per unit: T (stream-K) or k * E >= T (k-way split)
+  int n_units;             // n_heads * q_tiles
+  int n_queues;
+  int E;                   // key tiles per chunk (the first n_first chunks of a queue)
+  int E1;                  // key tiles per later chunk (E1 = E unless n_first > 0)
+  int n_first;             // chunks per queue of E tiles; the rest hold E1
+  int unit_base[kMaxQueues + 1];
+  int n_chunks[kMaxQueues];
+  int chunk_base[kMaxQueues];
+};
+// A partial slot: 128 output rows of 64 bf16, then the reference m[128] and sum l[128].
+constexpr int kAttnSlotFloats = kAttnBQ * kHeadDim / 2 + 2 * kAttnBQ;
+constexpr size_t kAttnSlotBytes = (size_t)kAttnSlotFloats * 4;
+
+// One layer's share of the saliency / selection / append kernel.
+struct AdmitLayer {
+  const uint16_t* Q;       // [N][H][64]   (saliency)
+  const uint16_t* K;       // frame keys: row j of head h at K + j * kv_row + h * kv_head
+  const uint16_t* V;       //   (saliency, append); V likewise (append)
+  int64_t kv_row;          // elements between a head's consecutive frame rows
+  int64_t kv_head;         // elements between heads' rows of one token
+  const float* lse;        // [H][N]       (saliency)
+  float* sal;              // [H][N]       written by saliency, read by selection
+  int32_t* idx;            // [H][budget]  optional output
+  uint16_t* memK;          // [H][head_stride][64]
+  uint16_t* memV;
+  int32_t* prov;           // [H][head_stride][2]
+  int64_t mem_len;
+  int64_t head_stride;
+};
+
+enum AdmitMode : int {
+  kModeSaliency = 1,       // saliency only
+  kModeSelect = 2,         // selection + append from a given saliency
+  kModeBoth = 3,           // saliency, then selection + append (two launches)
+};
+
+struct AdmitArgs {
+  AdmitLayer layer[kMaxLayersPerLaunch];
+  int n_q;                 // sampled queries: token q_base + (i / q_cols) * q_row_stride
+  int q_cols;              //   + (i % q_cols) * q_col_stride for i < n_q
+  int q_base;
+  int q_row_stride;
+  int q_col_stride;
+  int n_tokens;
+  int n_heads;
+  int n_layers;
+  int budget;
+  int frame_id;
+  int mode;
+  int stage_queries;       // saliency: stage the sampled query rows in LDS
+  int q_pass;              // saliency: sampled query rows staged per pass (multiple of 32)
+  int sal_groups;          // saliency: workgroups per (layer, head)
+  int shared_select;       // selection: one top-k per layer on the head sum, shared by all heads
+  int in_place;            // selection: K, V are the staged rows of the destination arena, so
+                           //   the append is an in-place compaction (read before write)
+};
+
+constexpr int kSalQStride = kHeadDim + 8;  // staged sampled-query rows: 72 elements (144 bytes)
+constexpr int kAdmitStaticLdsMargin = 4096;  // LDS left for the admission kernels' static arrays
+
+// ---- attention work plan ------------------------------------------------------------
+
+// Work plan of one attention launch: units (head, 128-query tile) are dealt in
+// contiguous ranges to the per-XCD queues, and each queue's (unit, key tile) iterations
+// are cut into chunks, one per workgroup, about kAttnWgPerCu per CU.
+struct AttnPlan {
+  int q_tiles, nt_mem, T, U, n_units, E, E1, n_first, grid, total_chunks;
+  int unit_base[kMaxQueues + 1];
+  int n_chunks[kMaxQueues];
+  int chunk_base[kMaxQueues];
+};
+
+// Plan for n_tokens queries over mem_len memory keys then n_fkeys frame keys, on a
+// device of n_cus CUs and n_queues XCDs (1..kMaxQueues).  Reads the RV_ATTN_* overrides.
+AttnPlan plan_attention(int n_cus, int n_queues, int n_tokens, int n_fkeys, int64_t mem_len, int n_heads);
+
+// Whether some unit's key range is split over several chunks (then a merge launch runs).
+bool plan_splits_units(const AttnPlan& p);
+
+// Partial slots a plan writes into: two per chunk (a chunk's segment of the unit it starts
+// in, and of the unit it ends in).
+inline int64_t plan_partial_slots(const AttnPlan& p) { return 2 * (int64_t)p.total_chunks; }
+
+// Upper bound on plan_partial_slots of every plan on this device unless RV_ATTN_SPLIT forces
+// a split (a chunk count set by the workgroup slots, whatever the sizes).
+int64_t default_partial_slots(int n_cus, int n_queues);
+
+// ---- query subset and admission launch shape -------------------------------------------
+
+// NULL if qs describes a frame of n_tokens tokens, else a description of the problem.
+const char* qsub_problem(const rv_qsub* qs, int n_tokens);
+
+// Sampled queries (Sec. 3.3, head-specific retention): query i of the subset is frame
+// token q_base + (i / q_cols) * q_row_stride + (i % q_cols) * q_col_stride, the
+// top-left patch of the i-th stride x stride window in row-major window order.
+void set_qsub(AdmitArgs* b, const rv_qsub& q);
+
+// Dynamic LDS bytes the saliency and selection launches take, the larger of the two for
+// the launches a.mode asks for, and the most they may use on a device whose per-workgroup
+// LDS limit is max_lds.
+size_t sal_lds_bytes(const AdmitArgs& a);
+size_t select_lds_bytes(const AdmitArgs& a);
+size_t admit_lds_bytes(const AdmitArgs& a);
+int admit_max_dynamic_lds(int max_lds);
+
+// Saliency launch shape for n_lh (layer, head) pairs on a device with n_cus CUs: sets
+// a->sal_groups, a->q_pass and a->stage_queries (rows staged when they fit max_lds).
+void plan_saliency(AdmitArgs* a, int n_lh, int n_cus, int max_lds);
+
+}  // namespace rv

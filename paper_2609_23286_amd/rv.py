@@ -47,6 +47,7 @@ def _load():
     sigs = {
         "rv_last_error": ([], ctypes.c_char_p),
         "rv_version": ([], ctypes.c_char_p),
+        "rv_init": ([], i32),
         "rv_mem_create": ([i32, i32, i64, i64, P(vp)], i32),
         "rv_mem_destroy": ([vp], i32),
         "rv_mem_len": ([vp], i64),
@@ -54,6 +55,7 @@ def _load():
         "rv_mem_view": ([vp, P(vp), P(vp), P(i64)], i32),
         "rv_mem_reserve": ([vp, i64, vp], i32),
         "rv_mem_reset": ([vp], i32),
+        "rv_mem_truncate": ([vp, i64], i32),
         "rv_mem_write": ([vp, vp, vp, i64, i32, vp], i32),
         "rv_mem_read": ([vp, vp, vp, vp, vp], i32),
         "rv_mem_save": ([vp, ctypes.c_char_p], i32),
@@ -67,7 +69,7 @@ def _load():
         "rv_mem_stage_frame": ([vp, vp, vp, i32, vp], i32),
         "rv_attend_staged": ([vp, i32, vp, P(rv_qsub), vp, vp, vp, vp], i32),
         "rv_admit_staged_layers": ([i32, P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp), vp], i32),
-        "rv_reserve_workspace": ([i32, i32, i32], i32),
+        "rv_reserve_workspace": ([i32, i32, i64, i32], i32),
         "rv_attention_plan": ([i32, i32, i64, i32, i32, i32, P(rv_attn_plan)], i32),
         "rv_device_status": ([], i32),
     }
@@ -124,8 +126,15 @@ def qsub(grid_h, grid_w, n_special, stride):
     return rv_qsub(grid_h, grid_w, n_special, stride)
 
 
-def reserve_workspace(n_tokens, n_heads, n_layers=1):
-    _check(_lib.rv_reserve_workspace(n_tokens, n_heads, n_layers))
+def init():
+    """rv_init: set up librv on the current device (limits, XCD count, workspace)."""
+    _check(_lib.rv_init())
+
+
+def reserve_workspace(n_tokens, n_heads, max_mem_len=0, n_layers=1):
+    """rv_reserve_workspace: partial slots for forced work plans up to max_mem_len memory
+    rows, saliency staging for n_layers layers."""
+    _check(_lib.rv_reserve_workspace(n_tokens, n_heads, max_mem_len, n_layers))
 
 
 def attention_plan(n_tokens, n_fkeys, mem_len, n_heads, n_cus, n_queues):
@@ -180,6 +189,10 @@ class Memory:
 
     def reset(self):
         _check(_lib.rv_mem_reset(self.handle))
+
+    def truncate(self, n_rows):
+        """rv_mem_truncate: drop the newest rows (host-side length change only)."""
+        _check(_lib.rv_mem_truncate(self.handle, n_rows))
 
     def write(self, K, V, frame_id=-1, stream=None):
         """Overwrite rows 0..n-1 with K, V ([H, n, 64], 2-byte elements, host or device)."""

@@ -1,0 +1,142 @@
+// host_logic_check.cpp -- drives librv's host-only planning code (rv_plan.cpp) over many
+// shapes, devices and work-plan overrides.  Built with AddressSanitizer and
+// UndefinedBehaviorSanitizer by tests/test_sanitizers.py, so any out-of-bounds table
+// access, signed overflow or division by zero in the planning aborts the run; the
+// checks below add the invariants the kernels rely on.  Prints "host logic OK".
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <initializer_list>
+
+#include "../../paper_2609_23286_amd/csrc/rv_plan.h"
+
+static int g_fail = 0;
+#define CHECK(c, ...)                                    \
+  do {                                                   \
+    if (!(c)) {                                          \
+      std::fprintf(stderr, "FAIL %s:%d: ", __FILE__, __LINE__); \
+      std::fprintf(stderr, __VA_ARGS__);                 \
+      std::fprintf(stderr, "\n");                        \
+      ++g_fail;                                          \
+    }                                                    \
+  } while (0)
+
+static int64_t chunk_start(const rv::AttnPlan& p, int c) {
+  return c < p.n_first ? (int64_t)c * p.E : (int64_t)p.n_first * p.E + (int64_t)(c - p.n_first) * p.E1;
+}
+
+// Every queue's iterations are covered exactly once by its chunks, in order.
+static void check_attention(int n_tokens, int n_fkeys, int64_t mem_len, int n_heads, int n_cus, int n_queues,
+                            bool forced_split) {
+  const rv::AttnPlan p = rv::plan_attention(n_cus, n_queues, n_tokens, n_fkeys, mem_len, n_heads);
+  const int q_tiles = (n_tokens + 127) / 128;
+  const int64_t T = (mem_len + 63) / 64 + (n_fkeys + 63) / 64;
+  CHECK(p.q_tiles == q_tiles && p.T == T && p.n_units == q_tiles * n_heads, "plan sizes");
+  CHECK(p.U >= p.T && p.E >= 1 && p.E1 >= 1 && p.E >= p.E1, "chunk sizes E=%d E1=%d U=%d T=%d", p.E, p.E1,
+        p.U, p.T);
+  CHECK(p.unit_base[0] == 0 && p.unit_base[n_queues] == p.n_units, "unit ranges");
+  CHECK(p.grid % n_queues == 0, "grid");
+  int total = 0;
+  for (int q = 0; q < n_queues; ++q) {
+    CHECK(p.unit_base[q] <= p.unit_base[q + 1], "unit ranges ordered");
+    const int64_t iters = (int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.U;
+    const int n = p.n_chunks[q];
+    CHECK(p.chunk_base[q] == total && n >= 0 && n <= p.grid / n_queues, "chunk table");
+    total += n;
+    if (iters == 0) {
+      CHECK(n == 0, "empty queue has chunks");
+      continue;
+    }
+    for (int c = 0; c < n; ++c) CHECK(chunk_start(p, c) < chunk_start(p, c + 1), "chunk order");
+    CHECK(chunk_start(p, n - 1) < iters && iters <= chunk_start(p, n), "chunks cover the queue");
+  }
+  CHECK(total == p.total_chunks, "total chunks");
+  // the workspace rv_init allocates holds every plan that RV_ATTN_SPLIT does not force
+  if (!forced_split)
+    CHECK(rv::plan_partial_slots(p) <= rv::default_partial_slots(n_cus, n_queues),
+          "plan needs %lld partial slots, default workspace %lld (N=%d M=%lld H=%d cus=%d q=%d)",
+          (long long)rv::plan_partial_slots(p), (long long)rv::default_partial_slots(n_cus, n_queues), n_tokens,
+          (long long)mem_len, n_heads, n_cus, n_queues);
+}
+
+static void check_saliency(int grid_h, int grid_w, int n_special, int stride, int n_lh, int n_cus, int max_lds) {
+  const int n_tokens = grid_h * grid_w + n_special;
+  rv_qsub qs{grid_h, grid_w, n_special, stride};
+  CHECK(rv::qsub_problem(&qs, n_tokens) == nullptr, "valid descriptor rejected");
+  CHECK(rv::qsub_problem(&qs, n_tokens + 1) != nullptr, "wrong token count accepted");
+  rv::AdmitArgs a{};
+  rv::set_qsub(&a, qs);
+  const int rows = (grid_h + stride - 1) / stride, cols = (grid_w + stride - 1) / stride;
+  CHECK(a.n_q == rows * cols, "sampled query count");
+  for (int i = 0; i < a.n_q; ++i) {  // every sampled token lies on the grid
+    const int qi = i / a.q_cols;
+    const int tok = a.q_base + qi * a.q_row_stride + (i - qi * a.q_cols) * a.q_col_stride;
+    CHECK(tok >= n_special && tok < n_tokens, "sampled token %d outside the grid", tok);
+  }
+  a.n_tokens = n_tokens;
+  a.budget = n_tokens < 10 ? n_tokens : 10;
+  a.mode = rv::kModeBoth;
+  rv::plan_saliency(&a, n_lh, n_cus, max_lds);
+  const int nq_pad = (a.n_q + 31) & ~31;
+  CHECK(a.sal_groups >= 1, "saliency groups");
+  if (a.stage_queries) {
+    CHECK(a.q_pass >= 32 && a.q_pass % 32 == 0, "pass size %d", a.q_pass);
+    CHECK(rv::sal_lds_bytes(a) <= (size_t)rv::admit_max_dynamic_lds(max_lds), "staged rows exceed LDS");
+  } else {
+    CHECK(a.q_pass == nq_pad, "unstaged pass covers every sampled query");
+  }
+}
+
+int main() {
+  static const int shapes[][4] = {  // n_tokens, n_fkeys, mem_len, n_heads
+      {1041, 1041, 0, 16},   {1041, 1041, 1000, 16}, {1041, 1041, 5000, 16}, {1041, 1041, 9990, 16},
+      {1041, 1041, 52000, 16}, {1041, 0, 11031, 16}, {1374, 1374, 26000, 16}, {16384, 16384, 3000, 2},
+      {65, 65, 0, 1},        {333, 333, 1500, 4},    {1, 1, 0, 1},           {1, 1, 63, 3},
+      {128, 128, 64, 1},     {1041, 1041, 250, 16},  {2000, 2000, 100000, 16}};
+  static const int devices[][2] = {{256, 8}, {304, 8}, {80, 2}, {32, 1}, {120, 3}, {1, 1}, {512, 16}};
+  struct Env {
+    const char *split, *pct, *wg, *min_chunk;
+  };
+  static const Env envs[] = {{nullptr, nullptr, nullptr, nullptr}, {"0", nullptr, nullptr, nullptr},
+                             {"3", nullptr, nullptr, nullptr},       {"1", nullptr, nullptr, nullptr},
+                             {"0", "100", nullptr, nullptr},         {"0", "101", nullptr, nullptr},
+                             {"0", "400", nullptr, nullptr},         {nullptr, nullptr, "1", nullptr},
+                             {nullptr, nullptr, "4", "1"},           {nullptr, "250", "3", "1"},
+                             {nullptr, nullptr, nullptr, "100000"}};
+  for (const Env& e : envs) {
+    auto set = [](const char* k, const char* v) {
+      if (v)
+        setenv(k, v, 1);
+      else
+        unsetenv(k);
+    };
+    set("RV_ATTN_SPLIT", e.split);
+    set("RV_ATTN_FIRST_PCT", e.pct);
+    set("RV_ATTN_WG_PER_CU", e.wg);
+    set("RV_ATTN_MIN_CHUNK", e.min_chunk);
+    for (const auto& d : devices)
+      for (const auto& s : shapes)
+        check_attention(s[0], s[1], s[2], s[3], d[0], d[1], e.split && std::atoi(e.split) > 0);
+  }
+  // a stream-K split (RV_ATTN_SPLIT=0) is not a forced k-way split: the bound holds
+  static const int grids[][4] = {  // grid_h, grid_w, n_special, stride
+      {28, 37, 5, 2}, {37, 37, 5, 2}, {8, 8, 0, 2}, {8, 8, 0, 1}, {28, 37, 5, 1}, {28, 37, 5, 3},
+      {28, 37, 5, 4}, {128, 128, 0, 2}, {1, 1041, 0, 2}, {0, 5, 7, 2}, {5, 0, 7, 2}, {0, 0, 1, 1},
+      {3, 3, 0, 5}, {1, 1, 0, 1}};
+  static const int lds_limits[] = {65536, 163840, 16384, 4096};
+  for (const auto& g : grids)
+    for (int n_lh : {1, 16, 384})
+      for (int n_cus : {1, 80, 256})
+        for (int lds : lds_limits) check_saliency(g[0], g[1], g[2], g[3], n_lh, n_cus, lds);
+  rv_qsub bad{-1, 2, 0, 2};
+  CHECK(rv::qsub_problem(&bad, 0) != nullptr, "negative grid accepted");
+  bad = rv_qsub{2, 2, 0, 0};
+  CHECK(rv::qsub_problem(&bad, 4) != nullptr, "stride 0 accepted");
+  CHECK(rv::qsub_problem(nullptr, 4) != nullptr, "NULL descriptor accepted");
+  if (g_fail) {
+    std::fprintf(stderr, "%d checks failed\n", g_fail);
+    return 1;
+  }
+  std::printf("host logic OK\n");
+  return 0;
+}

@@ -84,3 +84,27 @@ def test_invalid_arguments_are_rejected_before_any_device_work():
     # n_tokens == 0 is a no-op that succeeds without touching the device
     assert L.rv_attend_frame(None, None, None, 0, None, None, 0, 0, 16, 64, None, None, None,
                              None, None) == rv.RV_OK
+
+
+def test_empty_query_subset_is_accepted_and_returns_a_status():
+    """A subset with no window ({0, w, N, 2}: every token special) passes the argument
+    checks -- its saliency is the empty sum -- and the call returns a status instead of
+    aborting: with no GPU here, the status says the device is unavailable or the library
+    is not initialised on it."""
+    from paper_2609_23286_amd import rv
+    L = rv.lib()
+    vp = ctypes.c_void_p
+    N = 1041
+    empty = rv.rv_qsub(0, 37, N, 2)
+    st = L.rv_attend_frame(vp(1), vp(1), vp(1), N, None, None, 0, 0, 16, 64, ctypes.byref(empty), vp(1),
+                           vp(1), vp(1), None)
+    assert st in (rv.RV_ERR_INVALID, rv.RV_ERR_HIP) and L.rv_last_error()
+    assert b"query subset" not in L.rv_last_error()
+
+
+def test_truncate_checks_its_arguments():
+    from paper_2609_23286_amd import rv
+    L = rv.lib()
+    assert L.rv_mem_truncate(None, 0) == rv.RV_ERR_INVALID
+    assert L.rv_reserve_workspace(0, 16, 0, 1) == rv.RV_ERR_INVALID
+    assert L.rv_reserve_workspace(1041, 16, -1, 1) == rv.RV_ERR_INVALID

@@ -17,6 +17,7 @@ pytestmark = pytest.mark.gpu
 @pytest.fixture(scope="module")
 def rv():
     from paper_2609_23286_amd import rv as _rv
+    _rv.init()
     return _rv
 
 
@@ -111,12 +112,96 @@ def test_work_plans_agree_with_oracle(rv, wg_per_cu, min_chunk, split, first_pct
     monkeypatch.setenv("RV_ATTN_FIRST_PCT", first_pct)
     for N, H, M in ((333, 4, 1500), (1041, 16, 3000), (65, 1, 0)):
         print(f"plan {wg_per_cu}/{min_chunk}/{split}/{first_pct}: N={N} H={H} M={M}", flush=True)
+        rv.reserve_workspace(N, H, M)   # a forced plan may need more partial slots than the default
         Q, K, V = frame(7 + N, N, H)
         memK, memV = memory_rows(8 + N, H, M)
         out, lse, _ = run_attend(rv, Q, K, V, memK, memV, qsub_for(N), with_saliency=False)
         out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M)
         assert np.abs(out - out_o).max() <= OUT_ATOL
         assert np.abs(lse - lse_o).max() <= LSE_ATOL
+
+
+def test_empty_query_subset_gives_zero_saliency(rv):
+    """A query-subset descriptor with no window (grid_h = 0: every token is a special
+    token) is valid: every saliency is the empty sum 0 (as the oracle's definition
+    gives), so the selection takes the lowest indices.  Through rv_attend_frame and
+    through the deferred rv_admit_layers."""
+    import torch
+    N, H, M, budget = 1041, 16, 300, 10
+    qs = (0, 37, N, 2)
+    qidx = oracle.qsub_index(*qs)
+    assert len(qidx) == 0
+    Q, K, V = frame(21, N, H)
+    memK, memV = memory_rows(22, H, M)
+    out, lse, sal = run_attend(rv, Q, K, V, memK, memV, qs)
+    out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M)
+    sal_o = oracle.saliency(Q, K, lse_o, qidx)
+    assert (sal_o == 0).all() and (sal == 0).all()
+    assert np.abs(out - out_o).max() <= OUT_ATOL and np.abs(lse - lse_o).max() <= LSE_ATOL
+    mem = rv.Memory(H, reserve_tokens=M, max_tokens=M + budget)
+    mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+    sal_d = torch.full((H, N), -1.0, dtype=torch.float32, device="cuda")
+    idx = torch.full((H, budget), -1, dtype=torch.int32, device="cuda")
+    rv.admit_layers([to_dev(Q)], [to_dev(K)], [to_dev(V)], [to_dev(lse.astype(np.float32))], qs, budget,
+                    [mem], 4, [sal_d], [idx])
+    rv.device_status()
+    assert (sal_d.cpu().numpy() == 0).all()
+    assert (idx.cpu().numpy() == oracle.topk(sal_o, budget)).all()
+    assert (idx.cpu().numpy() == np.arange(budget)).all()
+    mem.close()
+
+
+def test_attend_frame_neither_allocates_nor_synchronises(rv, monkeypatch):
+    """rv_attend_frame returns while earlier work on its stream is still running (no
+    implicit device synchronisation), and a work plan that needs more partial slots than
+    the workspace holds is refused with RV_ERR_CAPACITY -- nothing enqueued, outputs
+    untouched -- instead of allocating; after rv_reserve_workspace the same call runs."""
+    import torch
+    N, H, M = 1041, 16, 2000
+    Q, K, V = frame(31, N, H)
+    memK, memV = memory_rows(32, H, M)
+    mem = rv.Memory(H, reserve_tokens=M, max_tokens=M)
+    mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+    Qd, Kd, Vd = to_dev(Q), to_dev(K), to_dev(V)
+    out = torch.full((N, H, 64), 7, dtype=torch.int16, device="cuda")
+    lse = torch.full((H, N), 5.0, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    if hasattr(torch.cuda, "_sleep"):          # keeps the stream busy for a bounded while
+        torch.cuda._sleep(200_000_000)
+    else:
+        a = torch.full((4096, 4096), 1e-3, device="cuda")
+        for _ in range(40):
+            a = a @ a
+    busy = torch.cuda.Event()
+    busy.record()
+    rv.attend_frame(Qd, Kd, Vd, mem, out, lse)
+    returned_early = not busy.query()
+    torch.cuda.synchronize()
+    assert returned_early, "rv_attend_frame waited for earlier work on the device"
+    out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M, rows=np.arange(0, N, 97, dtype=np.int32))
+    assert np.abs(bf16_to_f64(to_host_u16(out))[::97] - out_o).max() <= OUT_ATOL
+    # every tile its own chunk, at a memory length no other test reserves for
+    monkeypatch.setenv("RV_ATTN_SPLIT", "100000")
+    monkeypatch.setenv("RV_ATTN_MIN_CHUNK", "1")
+    big = 40000
+    memK2 = np.zeros((H, big, 64), dtype=np.uint16)
+    mem2 = rv.Memory(H, reserve_tokens=big, max_tokens=big)
+    mem2.write(torch.from_numpy(memK2.view(np.int16)), torch.from_numpy(memK2.view(np.int16)))
+    out.fill_(7)
+    lse.fill_(5.0)
+    torch.cuda.synchronize()
+    with pytest.raises(rv.RVError) as e:
+        rv.attend_frame(Qd, Kd, Vd, mem2, out, lse)
+    assert e.value.status == rv.RV_ERR_CAPACITY
+    torch.cuda.synchronize()
+    assert (out == 7).all() and (lse == 5.0).all()
+    monkeypatch.setenv("RV_ATTN_SPLIT", "40")
+    rv.reserve_workspace(N, H, M)
+    rv.attend_frame(Qd, Kd, Vd, mem, out, lse)
+    rv.device_status()
+    assert np.abs(bf16_to_f64(to_host_u16(out))[::97] - out_o).max() <= OUT_ATOL
+    mem.close()
+    mem2.close()
 
 
 def test_saliency_is_bit_reproducible(rv):

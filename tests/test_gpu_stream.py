@@ -24,6 +24,7 @@ pytestmark = pytest.mark.gpu
 @pytest.fixture(scope="module")
 def rv():
     from paper_2609_23286_amd import rv as _rv
+    _rv.init()
     return _rv
 
 
@@ -42,21 +43,37 @@ def gpu_frame_step(rv, mem, Q, K, V, qs, budget, frame_id):
             sal.cpu().numpy().astype(np.float64), idx.cpu().numpy())
 
 
-def run_free_stream(rv, cfg, n_frames, anchor=False):
+def run_free_stream(rv, cfg, n_frames, anchor=False, row_sample=None):
+    """Free-running stream: the GPU and the oracle each keep their own memory.  With
+    row_sample, the oracle computes only the sampled queries (all of them, for the
+    saliency) and the given output rows -- the rest of the attention is not needed for
+    the admission -- and outputs are compared on those rows."""
     import torch
     H, N, k = cfg.n_heads, cfg.n_tokens, cfg.budget
     qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
     qidx = oracle.qsub_index(*qs)
+    rows = None
+    if row_sample is not None:
+        rows = np.unique(np.concatenate([qidx, np.asarray(row_sample, dtype=np.int32)])).astype(np.int32)
+        pos = np.searchsorted(rows, qidx)
     cap = (N if anchor else 0) + n_frames * k + 8
     mem = rv.Memory(H, reserve_tokens=cap, max_tokens=cap)
     omem = oracle.Memory(H, cfg.head_dim, cap)
     resyncs = 0
     for t in range(n_frames):
-        print(f"{cfg.name} frame {t}", flush=True)
+        print(f"{cfg.name} frame {t} (memory {mem.len})", flush=True)
         Q, K, V = synth.frame_qkv(cfg, 0, t)
         budget = N if (anchor and t == 0) else k
         out, lse, sal, idx = gpu_frame_step(rv, mem, Q, K, V, qs, budget, t)
-        ref = oracle.step(omem, Q, K, V, qidx, budget)
+        if rows is None:
+            ref = oracle.step(omem, Q, K, V, qidx, budget)
+        else:
+            out_o, lse_o = oracle.attend(Q, K, V, omem.K, omem.V, omem.len, rows=rows)
+            sal_o = oracle.column_mass(Q, qidx, lse_o[:, pos], K, "frame")
+            idx_o = oracle.topk(sal_o, budget)
+            omem.append(K, V, idx_o)
+            ref = {"out": out_o, "lse": lse_o, "sal": sal_o, "idx": idx_o}
+            out, lse = out[rows], lse[:, rows]
         assert np.abs(out - ref["out"]).max() <= OUT_ATOL
         assert np.abs(lse - ref["lse"]).max() <= LSE_ATOL
         assert (np.abs(sal - ref["sal"]) <= SAL_RTOL * ref["sal"]).all()
@@ -87,8 +104,44 @@ def test_tiny_stream_with_anchor_frame(rv):
     assert run_free_stream(rv, synth.CONFIGS["tiny"], 8, anchor=True) == 0
 
 
-def test_vitl_layer_stream_first_frames(rv):
-    assert run_free_stream(rv, synth.CONFIGS["vitl_layer"], 6) == 0
+def test_vitl_layer_stream_free_running(rv):
+    """The whole 100-frame single-layer ViT-L stream, free-running from an empty memory
+    to 1,000 rows: every frame's saliency, admitted set and memory bytes against the
+    oracle's own stream, outputs and LSE on every sampled query plus tile-edge and
+    scattered rows."""
+    cfg = synth.CONFIGS["vitl_layer"]
+    N = cfg.n_tokens
+    sample = np.array([0, 1, 4, 5, 31, 32, 63, 64, 127, 128, 129, 511, 512, N - 2, N - 1], dtype=np.int32)
+    sample = np.concatenate([sample, np.arange(3, N, 53, dtype=np.int32)])
+    assert run_free_stream(rv, cfg, cfg.n_frames, row_sample=sample) == 0
+
+
+def test_stream_continues_bit_identically_after_restore(rv, tmp_path):
+    """Checkpoint / resume: a memory saved after frame t and loaded into a fresh memory
+    continues the stream exactly as the uninterrupted one -- outputs, LSE, saliency,
+    admitted indices and memory bytes equal bit for bit for the frames that follow."""
+    cfg = synth.CONFIGS["vitl_layer"]
+    H, k = cfg.n_heads, cfg.budget
+    qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
+    cap = 12 * k
+    mem = rv.Memory(H, reserve_tokens=cap, max_tokens=cap)
+    for t in range(6):
+        gpu_frame_step(rv, mem, *synth.frame_qkv(cfg, 0, t), qs, k, t)
+    path = tmp_path / "layer0.rvm"
+    mem.save(path)
+    restored = rv.Memory(H, reserve_tokens=0, max_tokens=cap)
+    restored.load(path)
+    for t in range(6, 12):
+        frame = synth.frame_qkv(cfg, 0, t)
+        a = gpu_frame_step(rv, mem, *frame, qs, k, t)
+        b = gpu_frame_step(rv, restored, *frame, qs, k, t)
+        for x, y in zip(a, b):
+            assert (x == y).all(), f"frame {t} differs after the restore"
+    assert mem.len == restored.len == 12 * k
+    for x, y in zip(mem.read(), restored.read()):
+        assert (x.numpy() == y.numpy()).all()
+    mem.close()
+    restored.close()
 
 
 def test_stream_is_deterministic(rv):
