@@ -140,8 +140,8 @@ def bench_args():
         if skip:
             skip -= 1
             continue
-        if a in ("--pmc-summary", "--trace-summary"):
-            skip = 2
+        if a in ("--pmc-summary", "--trace-summary", "--mfma-summary"):
+            skip = 3 if a == "--mfma-summary" else 2
             continue
         out.append(a)
     return " ".join(out)
@@ -215,6 +215,89 @@ def summarize_pmc(fetch_dir, write_dir, workload):
             fh.write("\n".join(lines) + "\n")
         print(f"{kernel}: {f_kib:.1f} KiB fetched, {w_kib:.1f} KiB written per dispatch -> "
               f"{total / 1e6:.2f} MB per launch ({path})")
+
+
+MFMA_PASSES = (("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_COEXEC_CYCLES",
+                "SQ_INSTS_MFMA", "GRBM_GUI_ACTIVE"),
+               ("SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_BUSY_CYCLES",
+                "GRBM_GUI_ACTIVE"))
+MI355X_XCDS, MI355X_SIMDS = 8, 1024    # 8 XCDs x 32 CUs x 4 SIMDs
+
+
+def mfma_path(workload):
+    return os.path.join(PROFILES, f"attn_fwd_kernel__{workload}__mfma.md")
+
+
+def summarize_mfma(dir_a, dir_b, bench_json, workload):
+    """Reduce two rocprofv3 --pmc runs of this benchmark (the counters of MFMA_PASSES) into
+    per-dispatch matrix-core and vector-ALU activity of each kernel, and tie the attention
+    kernel's to the benchmark line of the same command (bench_json)."""
+    import csv
+
+    def per_kernel(d):
+        out = {}
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                name = r["Kernel_Name"].split("(")[0].replace("rv::(anonymous namespace)::", "")
+                out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+        return out
+
+    a, b = per_kernel(dir_a), per_kernel(dir_b)
+    bench = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    mean = lambda v: sum(v) / len(v)
+    lines = [f"# Matrix-core and vector-ALU activity per dispatch, {workload}", "",
+             "Two counter passes over the benchmark command (one run each, the program after `--`):", "",
+             "```", "cd /tmp && export TMPDIR=/tmp"]
+    for i, cs in enumerate(MFMA_PASSES):
+        lines.append(f"timeout -s KILL 600 rocprofv3 --pmc {' '.join(cs)} --output-format csv -d <out>/m{i} "
+                     f"-o m{i} -- python /root/repo/bench.py {bench_args()} --no-cpu-baseline")
+    lines += [f"python /root/repo/bench.py {bench_args()} --mfma-summary <out>/m0 <out>/m1 <bench json>", "```",
+              "", "Counters are summed over the chip (GRBM_GUI_ACTIVE over its 8 XCDs).  Per dispatch:",
+              "`busy` = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024 SIMDs), the fraction of SIMD",
+              "cycles the matrix core is busy (rocprofv3's MfmaUtil); `coexec` = SQ_VALU_MFMA_COEXEC_CYCLES /",
+              "SQ_VALU_MFMA_BUSY_CYCLES, the share of those cycles in which a vector instruction was also",
+              "issued; `valu` = 4 x SQ_ACTIVE_INST_VALU / (GRBM_GUI_ACTIVE / 8 x 1024), vector-ALU cycles per",
+              "SIMD cycle (quad-cycle units); `bf16 flops` = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16.", "",
+              "| Kernel | dispatches | GUI cycles / XCD | busy | coexec | valu | MFMA instrs | bf16 flops | "
+              "VALU instrs | exp/log (f32 trans) instrs |", "|---|---|---|---|---|---|---|---|---|---|"]
+    rows = {}
+    for name in sorted(set(a) | set(b)):
+        if name not in KERNEL_SOURCES:
+            continue
+        ca, cb = a.get(name, {}), b.get(name, {})
+        try:
+            gui = mean(ca["GRBM_GUI_ACTIVE"]) / MI355X_XCDS
+            busy = mean(ca["SQ_VALU_MFMA_BUSY_CYCLES"])
+            r = {"n": len(ca["GRBM_GUI_ACTIVE"]), "gui": gui, "busy": busy / (gui * MI355X_SIMDS),
+                 "coexec": mean(ca["SQ_VALU_MFMA_COEXEC_CYCLES"]) / max(busy, 1.0),
+                 "mfma": mean(ca["SQ_INSTS_MFMA"]), "flops": 512.0 * mean(ca["SQ_INSTS_VALU_MFMA_MOPS_BF16"]),
+                 "valu": 4.0 * mean(cb["SQ_ACTIVE_INST_VALU"]) / (mean(cb["GRBM_GUI_ACTIVE"]) / MI355X_XCDS
+                                                                 * MI355X_SIMDS),
+                 "vinst": mean(cb["SQ_INSTS_VALU"]), "trans": mean(cb["SQ_INSTS_VALU_TRANS_F32"])}
+        except KeyError as e:
+            raise SystemExit(f"{name}: counter {e} missing from the CSVs")
+        rows[name] = r
+        lines.append(f"| `{name}` | {r['n']} | {r['gui']:.0f} | {100 * r['busy']:.1f} % | {100 * r['coexec']:.1f} % | "
+                     f"{100 * r['valu']:.1f} % | {r['mfma']:.0f} | {r['flops']:.3e} | {r['vinst']:.0f} | "
+                     f"{r['trans']:.0f} |")
+    f = rows.get("attn_fwd_kernel")
+    if f:
+        alg = bench["roofline"]["algorithmic_flops_per_launch"]
+        lines += ["", "The attention forward kernel against the benchmark line of the same command:", "",
+                  f"- algorithmic flops per launch (4 x 64 per query-key pair): {alg:.4e}; bf16 MFMA flops "
+                  f"executed per dispatch: {f['flops']:.4e} (x{f['flops'] / alg:.3f}: query tiles padded to 128 "
+                  "rows and key tiles to 64)",
+                  f"- matrix core busy {100 * f['busy']:.1f} % of SIMD cycles; a vector instruction issued in "
+                  f"{100 * f['coexec']:.1f} % of those; vector ALU active {100 * f['valu']:.1f} % of SIMD cycles",
+                  f"- benchmark line: {bench['roofline']['achieved']:.1f} TFLOP/s = "
+                  f"{100 * bench['roofline']['frac']:.1f} % of {bench['roofline']['peak']} TFLOP/s for the "
+                  f"attention step (forward + merge launches, {bench['roofline']['avg_launch_us']:.1f} us per "
+                  "layer by HIP events)",
+                  f"- source_hash: {kernel_source_hash('attn_fwd_kernel')}"]
+    path = mfma_path(workload)
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(f"wrote {path}")
 
 
 def summarize_trace(trace_dir, bench_json, workload):
@@ -349,6 +432,9 @@ def main():
                    help="run a 256 MiB device copy before the stream (HBM counter calibration)")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="summarise two rocprofv3 --pmc runs of this command into profiles/ and exit")
+    p.add_argument("--mfma-summary", nargs=3, metavar=("PASS0_DIR", "PASS1_DIR", "BENCH_JSON"),
+                   help="summarise the two rocprofv3 --pmc passes of MFMA_PASSES over this command into "
+                        "profiles/ and exit")
     p.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
                    help="summarise a rocprofv3 --kernel-trace --stats run of this command into profiles/ "
                         "and exit")
@@ -387,6 +473,9 @@ def main():
         return
     if args.pmc_summary:
         summarize_pmc(*args.pmc_summary, wkey or cfg.name)
+        return
+    if args.mfma_summary:
+        summarize_mfma(*args.mfma_summary, wkey or cfg.name)
         return
 
     import torch
@@ -559,8 +648,9 @@ def main():
     for t in warm:
         run_frame(t)
     torch.cuda.synchronize()
-    if full:
-        fill_memories(initial)  # the stream starts again from its initial memory
+    # the stream starts again from its initial memory (a stratified run's warm-up frames
+    # cut the memories back, and cutting back is the only length change between frames)
+    fill_memories(initial)
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in timed]
     torch.cuda.synchronize()
