@@ -178,6 +178,23 @@ rv_status rv_attend_frame(const void *Q, const void *K, const void *V, int n_tok
                           const rv_qsub *qs, void *out, float *lse, float *saliency,
                           void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): rv_attend_frame with the same
+ * arguments, results and errors, except that its split-KV partial results live in a
+ * static array the library holds on every GPU it runs on (1,152 slots of 17,408 bytes,
+ * 20.1 MB, kept until the process ends) instead of the rv_init workspace.  It calls no
+ * allocating routine; rv_init must have run on the device (it records the array's
+ * address there).  A work plan that needs more than 1,152 partial slots (only forced
+ * RV_ATTN_* plans can) is refused with RV_ERR_CAPACITY before anything is enqueued.
+ * Nothing in the array needs clearing between calls (each call writes every slot it
+ * reads), but all calls on one GPU share it: calls that overlap on one GPU (on
+ * different streams) race and must be ordered by the caller. */
+rv_status rv_attend_frame_noalloc(const void *Q, const void *K, const void *V, int n_tokens,
+                                  const void *memK, const void *memV, int64_t mem_len,
+                                  int64_t head_stride_tokens, int n_heads, int head_dim,
+                                  const rv_qsub *qs, void *out, float *lse, float *saliency,
+                                  void *stream);
+
 /* Admission from a given saliency (Sec. 3.3 Eq. 6): per head, selects the `budget`
  * tokens of largest saliency -- equal saliencies ordered by lower token index -- and
  * appends their K and V rows (exact copies) to m in ascending token order; the length

@@ -520,7 +520,17 @@ __global__ void xcc_probe_kernel(int* ids) {
   if (threadIdx.x == 0) ids[blockIdx.x] = hw_xcc_id();
 }
 
+// Split-KV partial slots of the allocation-free entry point: every GPU the library runs
+// on holds one copy, from the library's load until the process ends.
+static __device__ __align__(256) float scratch[(size_t)kStaticScratchSlots * kAttnSlotFloats];
+
 }  // namespace
+
+hipError_t static_scratch_address(float** ptr) {
+  // host code may not use `scratch` itself as a device address: take the current
+  // device's copy of the array through the runtime
+  return hipGetSymbolAddress(reinterpret_cast<void**>(ptr), HIP_SYMBOL(scratch));
+}
 
 hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t s) {
   hipLaunchKernelGGL(attn_fwd_kernel, dim3(grid), dim3(kAttnThreads), 0, s, a);

@@ -58,6 +58,7 @@ struct Workspace {
   int64_t part_slots = 0;
   float* sal = nullptr;      // saliency staging when the caller passes none
   size_t sal_floats = 0;
+  float* static_part = nullptr;  // this device's copy of the static partial-slot array
 };
 
 std::mutex g_ws_mu;
@@ -111,6 +112,7 @@ rv_status init_device(Workspace* ws, int dev) {
   for (int id : ids)
     if (std::find(distinct.begin(), distinct.end(), id) == distinct.end()) distinct.push_back(id);
   ws->n_queues = std::max(1, std::min((int)distinct.size(), rv::kMaxQueues));
+  RV_HIP(rv::static_scratch_address(&ws->static_part), "static scratch address");
   rv_status st = reserve_partials(ws, rv::default_partial_slots(ws->n_cus, ws->n_queues));
   if (st != RV_OK) return st;
   ws->ready = true;
@@ -502,21 +504,29 @@ namespace {
 // Attention (+ saliency) launch shared by the frame and staged entry points.  Keys: the
 // mem_len rows of memK/memV, then n_fkeys frame rows of K/V ([n][H][64]).  The saliency's
 // keys are the frame's rows j at sK + j * s_row + h * s_head.  Arguments are checked.
+// use_static: the partial slots are the static array's (the allocation-free entry point).
 rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens, int n_fkeys, const void* memK,
                       const void* memV, int64_t mem_len, int64_t head_stride_tokens, int n_heads,
                       const rv_qsub* qs, void* out, float* lse, float* saliency, const void* sK, int64_t s_row,
-                      int64_t s_head, hipStream_t s) {
+                      int64_t s_head, hipStream_t s, bool use_static = false) {
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace* ws;
   rv_status st = ready_ws(&ws);
   if (st != RV_OK) return st;
 
   const rv::AttnPlan p = rv::plan_attention(ws->n_cus, ws->n_queues, n_tokens, n_fkeys, mem_len, n_heads);
-  if (rv::plan_partial_slots(p) > ws->part_slots)
+  if (use_static) {
+    if (rv::plan_partial_slots(p) > rv::kStaticScratchSlots)
+      return fail(RV_ERR_CAPACITY,
+                  "the work plan needs %lld attention partial slots, the static scratch array holds %d "
+                  "(%zu bytes)", (long long)rv::plan_partial_slots(p), rv::kStaticScratchSlots,
+                  (size_t)rv::kStaticScratchSlots * rv::kAttnSlotBytes);
+  } else if (rv::plan_partial_slots(p) > ws->part_slots) {
     return fail(RV_ERR_CAPACITY,
                 "the work plan needs %lld attention partial slots, the workspace holds %lld "
                 "(a forced plan: call rv_reserve_workspace with this frame's sizes)",
                 (long long)rv::plan_partial_slots(p), (long long)ws->part_slots);
+  }
 
   rv::AttnArgs a{};
   a.Q = (const uint16_t*)Q;
@@ -528,7 +538,7 @@ rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens,
   a.head_stride = head_stride_tokens;
   a.out = (uint16_t*)out;
   a.lse = lse;
-  a.part = ws->part;
+  a.part = use_static ? ws->static_part : ws->part;
   a.n_tokens = n_tokens;
   a.n_fkeys = n_fkeys;
   a.n_heads = n_heads;
@@ -593,6 +603,29 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   }
   return attend_impl(Q, K, V, n_tokens, n_tokens, memK, memV, mem_len, head_stride_tokens, n_heads, qs, out, lse,
                      saliency, K, (int64_t)n_heads * rv::kHeadDim, rv::kHeadDim, (hipStream_t)stream);
+}
+
+rv_status rv_attend_frame_noalloc(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
+                                  const void* memV, int64_t mem_len, int64_t head_stride_tokens, int n_heads,
+                                  int head_dim, const rv_qsub* qs, void* out, float* lse, float* saliency,
+                                  void* stream) {
+  if (n_tokens < 0 || n_tokens > rv::kMaxTokens)
+    return fail(RV_ERR_INVALID, "n_tokens must be in [0, %d] (got %d)", rv::kMaxTokens, n_tokens);
+  if (n_heads < 1) return fail(RV_ERR_INVALID, "n_heads must be >= 1");
+  if (head_dim != rv::kHeadDim) return fail(RV_ERR_INVALID, "head_dim must be 64 (got %d)", head_dim);
+  if (mem_len < 0) return fail(RV_ERR_INVALID, "mem_len must be >= 0");
+  if (mem_len > 0 && (!memK || !memV)) return fail(RV_ERR_INVALID, "memK/memV NULL with mem_len > 0");
+  if (mem_len > 0 && head_stride_tokens < mem_len)
+    return fail(RV_ERR_INVALID, "head_stride_tokens (%lld) < mem_len (%lld)", (long long)head_stride_tokens,
+                (long long)mem_len);
+  if (n_tokens == 0) return RV_OK;
+  if (!Q || !K || !V || !out || !lse) return fail(RV_ERR_INVALID, "Q, K, V, out and lse are required");
+  if (saliency) {
+    rv_status st = check_qsub(qs, n_tokens);
+    if (st != RV_OK) return st;
+  }
+  return attend_impl(Q, K, V, n_tokens, n_tokens, memK, memV, mem_len, head_stride_tokens, n_heads, qs, out, lse,
+                     saliency, K, (int64_t)n_heads * rv::kHeadDim, rv::kHeadDim, (hipStream_t)stream, true);
 }
 
 rv_status rv_mem_stage(rv_mem m, int n_tokens, void** K_tail, void** V_tail, int64_t* head_stride_tokens,

@@ -10,6 +10,9 @@
 namespace rv {
 
 hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t s);
+// Device address, on the current device, of the library's static partial-slot array
+// (kStaticScratchSlots slots of kAttnSlotFloats floats).
+hipError_t static_scratch_address(float** ptr);
 // Copies a frame's K, V ([n][H][64] bf16) to staged arena rows: row j of head h goes to
 // dK / dV + (h * head_stride + j) * 64.
 hipError_t launch_stage(uint16_t* dK, uint16_t* dV, int64_t head_stride, const uint16_t* K, const uint16_t* V,

@@ -58,6 +58,9 @@ struct AttnArgs {
 // A partial slot: 128 output rows of 64 bf16, then the reference m[128] and sum l[128].
 constexpr int kAttnSlotFloats = kAttnBQ * kHeadDim / 2 + 2 * kAttnBQ;
 constexpr size_t kAttnSlotBytes = (size_t)kAttnSlotFloats * 4;
+// Partial slots of the allocation-free attention entry point's static array (20.1 MB):
+// more than the 1,040 the default plans on an MI355X (256 CUs, 8 XCDs) can take.
+constexpr int kStaticScratchSlots = 1152;
 
 // One layer's share of the saliency / selection / append kernel.
 struct AdmitLayer {

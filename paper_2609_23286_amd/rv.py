@@ -61,6 +61,8 @@ def _load():
         "rv_mem_save": ([vp, ctypes.c_char_p], i32),
         "rv_mem_load": ([vp, ctypes.c_char_p], i32),
         "rv_attend_frame": ([vp, vp, vp, i32, vp, vp, i64, i64, i32, i32, P(rv_qsub), vp, vp, vp, vp], i32),
+        "rv_attend_frame_noalloc": ([vp, vp, vp, i32, vp, vp, i64, i64, i32, i32, P(rv_qsub), vp, vp, vp, vp],
+                                    i32),
         "rv_admit": ([vp, i32, vp, vp, i32, vp, i32, vp, vp], i32),
         "rv_admit_layers": ([i32, P(vp), P(vp), P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp), vp], i32),
         "rv_admit_layers_shared": ([i32, P(vp), P(vp), P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp),
