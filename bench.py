@@ -238,7 +238,7 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
         out = {}
         for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             for r in csv.DictReader(open(f)):
-                name = r["Kernel_Name"].split("(")[0].replace("rv::(anonymous namespace)::", "")
+                name = r["Kernel_Name"].replace("rv::(anonymous namespace)::", "").split("(")[0]
                 out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
         return out
 
@@ -426,6 +426,9 @@ def main():
                    help="stage each frame's K/V in the memory arenas (rv_mem_stage_frame, timed as its "
                         "own phase), attend over the contiguous arena (rv_attend_staged) and admit by "
                         "in-place compaction (rv_admit_staged_layers)")
+    p.add_argument("--fused", action="store_true",
+                   help="saliency in the attention epilogue (rv_attend_frame_fused, per 128-query block) "
+                        "and admission from those rows (rv_admit_layers_tiled)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-samples", type=int, default=24, help="layer-frames the oracle is timed on")
     p.add_argument("--copy-calibration", action="store_true",
@@ -467,6 +470,8 @@ def main():
     if args.staged:
         variant.append("frames staged in the arenas by a copy kernel (timed as staging_ms, inside the "
                        "wall clock), attention over the contiguous arena, admission by in-place compaction")
+    if args.fused:
+        variant.append("saliency in the attention epilogue (per 128-query block), admission from those rows")
     wkey = workload_key(cfg, n_stream, K_steps, variant)
     if args.trace_summary:
         summarize_trace(*args.trace_summary, wkey or cfg.name)
@@ -488,6 +493,8 @@ def main():
     admit_fn = "rv_admit_layers_shared" if args.shared else "rv_admit_layers"
     if args.staged and args.shared:
         raise SystemExit("--staged supports head-specific selection only")
+    if args.fused and (args.staged or args.shared or args.policy == "paper"):
+        raise SystemExit("--fused runs the configuration's own policy with head-specific selection only")
 
     def mem_len(l, t):
         """Rows of layer l's memory when frame t of the stream is attended."""
@@ -565,6 +572,8 @@ def main():
     out = torch.empty((L, N, H, d), dtype=torch.int16, device=dev)
     lse = torch.empty((L, H, N), dtype=torch.float32, device=dev)
     sal = torch.empty((L, H, N), dtype=torch.float32, device=dev)
+    n_qb = -(-N // 128)
+    tiles = torch.empty((L, H, n_qb, N), dtype=torch.float32, device=dev) if args.fused else None
 
     # Raw C calls with pre-marshalled arguments keep the host ahead of the GPU.
     import ctypes
@@ -588,11 +597,14 @@ def main():
         vpp = [fb[l, 2].data_ptr() for l in range(L)]
         frame_ptrs[t] = (qp, kp, vpp, arr(*qp), arr(*kp), arr(*vpp))
 
+    tiles_p = [vp(tiles[l].data_ptr()) for l in range(L)] if args.fused else None
+    qsub_c = rv.rv_qsub(*qs)
     reg_arr = lambda ptrs: (vp * len(regulated))(*[ptrs[l] for l in regulated])
     reg_sal = reg_arr([sal[l].data_ptr() for l in range(L)])
     reg_lse = reg_arr([lse[l].data_ptr() for l in range(L)])
     reg_mem = reg_arr([m.handle.value for m in mems])
     reg_frames = {t: (reg_arr(f[0]), reg_arr(f[1]), reg_arr(f[2])) for t, f in frame_ptrs.items()}
+    reg_tiles = reg_arr([tiles[l].data_ptr() for l in range(L)]) if args.fused else None
     admit = getattr(lib, admit_fn)
 
     def run_frame(t, ev=None):
@@ -614,6 +626,11 @@ def main():
         for l in range(L):
             if args.staged:
                 st = lib.rv_attend_staged(vp(qp[l]), N, mems[l].handle, None, out_p[l], lse_p[l], None, s_h)
+            elif args.fused and l in regulated:
+                mk, mv, hs = views[l]
+                st = lib.rv_attend_frame_fused(vp(qp[l]), vp(kp[l]), vp(vpp[l]), N, vp(mk), vp(mv),
+                                               lib.rv_mem_len(mems[l].handle), hs, H, d, ctypes.byref(qsub_c),
+                                               out_p[l], lse_p[l], tiles_p[l], s_h)
             else:
                 mk, mv, hs = views[l]
                 st = lib.rv_attend_frame(vp(qp[l]), vp(kp[l]), vp(vpp[l]), N, vp(mk), vp(mv),
@@ -633,6 +650,9 @@ def main():
             if args.staged:
                 st = lib.rv_admit_staged_layers(len(regulated), rq, reg_lse, N, qref, k, reg_mem, t, reg_sal,
                                                 None, s_h)
+            elif args.fused:
+                st = lib.rv_admit_layers_tiled(len(regulated), reg_tiles, N, k, rk, rvv, reg_mem, t, reg_sal, None,
+                                               s_h)
             else:
                 st = admit(len(regulated), rq, rk, rvv, reg_lse, N, qref, k, reg_mem, t, reg_sal, None, s_h)
         else:

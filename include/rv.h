@@ -195,6 +195,39 @@ rv_status rv_attend_frame_noalloc(const void *Q, const void *K, const void *V, i
                                   const rv_qsub *qs, void *out, float *lse, float *saliency,
                                   void *stream);
 
+/* ---- saliency in the attention epilogue ------------------------------------------------
+ *
+ * The saliency needs each sampled query's final LSE, which exists only once the key range
+ * of the query's 128-query block has been merged; these two calls form it there, right
+ * after the attention, from the frame's keys the attention has just read, and leave the
+ * top-k to a later launch that needs no keys.  The saliency of key j is split by query
+ * block: S_j = sum over b of S_j^(b), with
+ *   S_j^(b) = sum over sampled queries i in [RV_QUERY_BLOCK b, RV_QUERY_BLOCK (b + 1))
+ *             of exp(z_ij - LSE_i)                                      (Sec. 3.3). */
+#define RV_QUERY_BLOCK 128
+
+/* rv_attend_frame (same arguments, layouts, arithmetic and errors; qs required) that also
+ * writes, per head h and query block b < ceil(n_tokens / RV_QUERY_BLOCK), the row
+ * sal_tiles[h][b][0 .. n_tokens-1] = S_j^(b) (fp32, summed in a fixed order: the same
+ * inputs give the same bits).  sal_tiles: [n_heads][ceil(n_tokens / 128)][n_tokens] fp32,
+ * device memory, every entry written. */
+rv_status rv_attend_frame_fused(const void *Q, const void *K, const void *V, int n_tokens,
+                                const void *memK, const void *memV, int64_t mem_len,
+                                int64_t head_stride_tokens, int n_heads, int head_dim,
+                                const rv_qsub *qs, void *out, float *lse, float *sal_tiles, void *stream);
+
+/* Admission (Sec. 3.3 Eq. 6) of n_layers layers in one launch from the per-block saliency
+ * rv_attend_frame_fused wrote: per layer and head, S_j is the sum of the rows b = 0, 1, ...
+ * in that order; then the selection and the append of rv_admit_layers.  sal_tiles: host
+ * array of n_layers device pointers ([n_heads][ceil(n_tokens / 128)][n_tokens] fp32).
+ * saliency_out, idx_out: NULL, or host arrays of n_layers device pointers (each may be
+ * NULL) receiving S ([n_heads][n_tokens] fp32) and the selection ([n_heads][budget]).
+ * Otherwise as rv_admit_layers (K, V, mems, frame_id, budget, growth and errors). */
+rv_status rv_admit_layers_tiled(int n_layers, const float *const *sal_tiles, int n_tokens, int budget,
+                                const void *const *K, const void *const *V, const rv_mem *mems,
+                                int frame_id, float *const *saliency_out, int32_t *const *idx_out,
+                                void *stream);
+
 /* Admission from a given saliency (Sec. 3.3 Eq. 6): per head, selects the `budget`
  * tokens of largest saliency -- equal saliencies ordered by lower token index -- and
  * appends their K and V rows (exact copies) to m in ascending token order; the length

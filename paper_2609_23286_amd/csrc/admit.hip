@@ -457,6 +457,25 @@ __global__ __launch_bounds__(NT) void select_kernel(AdmitArgs a) {
       for (int h = 0; h < H; ++h) acc += L.sal[(int64_t)h * N + j];
       s_sal[j] = acc;
     }
+  } else if (a.sal_tiles > 0) {
+    // per-block saliency rows of this head (computed in the attention epilogue), summed
+    // in block order; the sum is the saliency, written out when asked for
+    // (eight rows' loads in flight per step)
+    const int T = a.sal_tiles;
+    const float* gs = L.sal + (int64_t)h_own * T * N;
+    for (int j = tid; j < N; j += NT) {
+      float acc = 0.f;
+      for (int t0 = 0; t0 < T; t0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = t0 + u < T ? gs[(int64_t)(t0 + u) * N + j] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (t0 + u < T) acc = (t0 + u == 0) ? v[u] : acc + v[u];
+      }
+      s_sal[j] = acc;
+      if (L.sal_out) L.sal_out[(int64_t)h_own * N + j] = acc;
+    }
   } else {
     const float* gs = L.sal + (int64_t)h_own * N;
     if ((N & 3) == 0) {

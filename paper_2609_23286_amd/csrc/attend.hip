@@ -54,6 +54,7 @@ constexpr int TILE = BK * D;                    // one K or V tile: 64 rows x 12
 constexpr int STAGE = 2 * TILE;                 // K tile then V tile
 constexpr int NSTAGE = 4;                       // LDS ring: two tiles computed, two in flight
 constexpr float kLn2 = 0.69314718055994531f;
+constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kScaleLog2 = 1.44269504088896341f * 0.125f;  // log2(e) / sqrt(64)
 constexpr float kOverflowGuard = 18446744073709551616.0f;  // 2^64
 constexpr float kNegBig = -1.0e30f;
@@ -516,6 +517,148 @@ __global__ __launch_bounds__(kAttnThreads) void attn_merge_kernel(AttnArgs a) {
   merge_rows(a, q, unit, ui, rb, c_first, c_last);
 }
 
+// Merge launch with the saliency in its epilogue (Sec. 3.3: the saliency reuses the LSE,
+// so it can only start once a query's LSE is final).  kEpiGroups workgroups per unit
+// (head h, 128-query block qt); workgroup g
+// * merges output rows 32 g .. 32 g + 31 of a split unit exactly as the merge launch does
+//   (a unit whose key range one chunk covered was written by the forward launch);
+// * forms the final LSE (log2 units) of all 128 rows -- from the partials' m and l with
+//   merge_rows' arithmetic, or read back for a whole unit -- and lists the block's sampled
+//   queries (the window rule of SalEpi) in row order, staging their rows in LDS;
+// * sums, for the keys of its quarter of the frame's 32-key blocks, exp2(z log2(e) / 8 -
+//   LSE log2(e)) over the sampled queries with v_mfma_f32_32x32x16_bf16 (Z = Q~ K^T, one
+//   lane per key), in a fixed order -- in-lane over the accumulator rows, over 32-query
+//   blocks, then across the lane halves -- into tiles[h][qt][j].
+constexpr int kEpiGroups = 4;
+constexpr int kEpiQStride = kHeadDim + 8;   // staged query rows, 144 bytes
+constexpr int kEpiKeyBatch = 4;             // 32-key blocks whose K rows a wave loads together
+
+// Final LSE (log2 units) of row `row` of a split unit, with merge_rows' arithmetic.
+__device__ float merged_lse2(const AttnArgs& a, int q, int ui, int row, int c_first, int c_last) {
+  float mmax = kNegBig, L = 0.f;
+  for (int c0 = c_first; c0 <= c_last; c0 += kMergeMax) {
+    const int n = min(kMergeMax, c_last - c0 + 1);
+    float mv[kMergeMax], lv[kMergeMax];
+#pragma unroll
+    for (int j = 0; j < kMergeMax; ++j) {
+      const float* ps = slot_ptr(a, q, min(c0 + j, c_last), ui);
+      mv[j] = ps[kSlotStatsFloat + row];
+      lv[j] = ps[kSlotStatsFloat + BQ + row];
+    }
+    float m_new = mmax;
+#pragma unroll
+    for (int j = 0; j < kMergeMax; ++j) m_new = fmaxf(m_new, mv[j]);
+    L *= __builtin_amdgcn_exp2f(mmax - m_new);
+    mmax = m_new;
+#pragma unroll
+    for (int j = 0; j < kMergeMax; ++j) L += j < n ? __builtin_amdgcn_exp2f(mv[j] - mmax) * lv[j] : 0.f;
+  }
+  return mmax + __log2f(L);
+}
+
+__global__ __launch_bounds__(kAttnThreads) void attn_merge_sal_kernel(AttnArgs a, SalEpi e) {
+  __shared__ float s_lse2[BQ];                        // by row
+  __shared__ float s_lsec[BQ];                        // by sampled position (padding: +inf)
+  __shared__ int s_list[BQ];
+  __shared__ int s_count[2];
+  __shared__ __attribute__((aligned(16))) uint16_t s_q[BQ * kEpiQStride];
+  touch_args(a);
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int q = (int)(blockIdx.x % (unsigned)a.n_queues);
+  const int jg = (int)(blockIdx.x / (unsigned)a.n_queues);
+  const int ui = jg / kEpiGroups, g = jg % kEpiGroups;
+  if (ui >= a.unit_base[q + 1] - a.unit_base[q]) return;  // uniform
+  const int unit = a.unit_base[q] + ui;
+  const int h = unit / a.q_tiles, qt = unit % a.q_tiles;
+  const int N = a.n_tokens;
+  const int c_first = chunk_of(a, (int64_t)ui * a.U);
+  const int c_last = chunk_of(a, (int64_t)ui * a.U + a.T - 1);
+
+  // ---- this group's output rows, and the LSE of all the block's rows ----
+  if (c_first != c_last) merge_rows(a, q, unit, ui, g, c_first, c_last);
+  if (tid < BQ) {
+    const int qi = qt * BQ + tid;
+    float l2 = 0.f;
+    if (qi < N) l2 = c_first == c_last ? a.lse[(int64_t)h * N + qi] * kLog2e : merged_lse2(a, q, ui, tid, c_first, c_last);
+    s_lse2[tid] = l2;
+  }
+
+  // ---- the block's sampled queries, in row order (waves 0 and 1 hold rows 0 .. 127) ----
+  const int srow = wave * 64 + lane;
+  bool sampled = false;
+  int before = 0;
+  if (wave < 2) {
+    const int r = qt * BQ + srow - e.q_base;
+    sampled = r >= 0 && r < e.grid_cells && (r / e.grid_w) % e.stride == 0 && (r % e.grid_w) % e.stride == 0;
+    const uint64_t bal = __ballot(sampled);
+    before = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) s_count[wave] = __builtin_popcountll(bal);
+  }
+  __syncthreads();
+  if (sampled) s_list[(wave == 1 ? s_count[0] : 0) + before] = srow;
+  __syncthreads();
+  const int n_s = s_count[0] + s_count[1];
+  const int ns_pad = (n_s + 31) & ~31;
+  const uint16_t* Kh = e.K + (int64_t)h * e.kv_head;
+  float* tile_h = e.tiles + ((int64_t)h * a.q_tiles + qt) * N;
+  const int n_blocks = (N + 31) / 32;
+  const int per_group = (n_blocks + kEpiGroups - 1) / kEpiGroups;
+  const int blk0 = g * per_group, blk1 = min(n_blocks, blk0 + per_group);
+  if (n_s == 0) {  // no sampled query in this block: its saliency row is the empty sum
+    for (int j = blk0 * 32 + tid; j < min(N, blk1 * 32); j += kAttnThreads) tile_h[j] = 0.f;
+    return;
+  }
+  // sampled query rows and their LSE (padding rows: zero rows, +inf -> weight 0)
+  for (int x = tid; x < ns_pad * 8; x += kAttnThreads) {
+    const int s = x >> 3, ch = x & 7;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (s < n_s) v = *reinterpret_cast<const uint4*>(a.Q + ((int64_t)(qt * BQ + s_list[s]) * a.n_heads + h) * D + ch * 8);
+    *reinterpret_cast<uint4*>(&s_q[s * kEpiQStride + ch * 8]) = v;
+  }
+  for (int s = tid; s < ns_pad; s += kAttnThreads) s_lsec[s] = s < n_s ? s_lse2[s_list[s]] : __builtin_inff();
+  __syncthreads();
+
+  // ---- this group's key blocks, kEpiKeyBatch per wave at a time ----
+  const int l32 = lane & 31, half = lane >> 5;
+  for (int kb0 = blk0 + wave; kb0 < blk1; kb0 += kEpiKeyBatch * (kAttnThreads / 64)) {
+    bf16x8 kf[kEpiKeyBatch][4];
+#pragma unroll
+    for (int bb = 0; bb < kEpiKeyBatch; ++bb) {
+      const int j = min((kb0 + bb * (kAttnThreads / 64)) * 32 + l32, N - 1);  // past the range: result unused
+      const uint16_t* kp = Kh + (int64_t)j * e.kv_row + half * 8;
+#pragma unroll
+      for (int ds = 0; ds < 4; ++ds) kf[bb][ds] = *reinterpret_cast<const bf16x8*>(kp + ds * 16);
+    }
+#pragma unroll
+    for (int bb = 0; bb < kEpiKeyBatch; ++bb) {
+      const int kb = kb0 + bb * (kAttnThreads / 64);
+      if (kb >= blk1) break;  // uniform
+      float acc = 0.f;
+      for (int qb = 0; qb < ns_pad; qb += 32) {
+        bf16x8 qf[4];
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds)
+          qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[(qb + l32) * kEpiQStride + ds * 16 + half * 8]);
+        f32x16 z = {};
+#pragma unroll
+        for (int ds = 0; ds < 4; ++ds) z = mfma32(qf[ds], kf[bb][ds], z);
+        // accumulator entry r: sampled query qb + 8 (r / 4) + 4 half + r % 4, key kb * 32 + l32
+        float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          const int i0 = qb + 8 * (r >> 2) + 4 * half + (r & 3);
+          s0 += __builtin_amdgcn_exp2f(fmaf(z[r], kScaleLog2, -s_lsec[i0]));
+          s1 += __builtin_amdgcn_exp2f(fmaf(z[r + 1], kScaleLog2, -s_lsec[i0 + 1]));
+        }
+        acc += s0 + s1;
+      }
+      const float tot = acc + __shfl_xor(acc, 32);
+      const int j = kb * 32 + l32;
+      if (half == 0 && j < N) tile_h[j] = tot;
+    }
+  }
+}
+
 __global__ void xcc_probe_kernel(int* ids) {
   if (threadIdx.x == 0) ids[blockIdx.x] = hw_xcc_id();
 }
@@ -540,6 +683,17 @@ hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t
   for (int q = 0; q < a.n_queues; ++q) max_units = max(max_units, a.unit_base[q + 1] - a.unit_base[q]);
   hipLaunchKernelGGL(attn_merge_kernel, dim3(a.n_queues * max_units * (BQ / kMergeRows)), dim3(kAttnThreads), 0,
                      s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_saliency(const AttnArgs& a, const SalEpi& e, int grid, hipStream_t s) {
+  hipLaunchKernelGGL(attn_fwd_kernel, dim3(grid), dim3(kAttnThreads), 0, s, a);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  int max_units = 0;
+  for (int q = 0; q < a.n_queues; ++q) max_units = max(max_units, a.unit_base[q + 1] - a.unit_base[q]);
+  hipLaunchKernelGGL(attn_merge_sal_kernel, dim3(a.n_queues * max_units * kEpiGroups), dim3(kAttnThreads), 0, s,
+                     a, e);
   return hipGetLastError();
 }
 

@@ -505,10 +505,12 @@ namespace {
 // mem_len rows of memK/memV, then n_fkeys frame rows of K/V ([n][H][64]).  The saliency's
 // keys are the frame's rows j at sK + j * s_row + h * s_head.  Arguments are checked.
 // use_static: the partial slots are the static array's (the allocation-free entry point).
+// sal_tiles: the saliency is formed in the attention epilogue, per 128-query block, into
+// sal_tiles ([H][q_tiles][N]) instead of by a separate launch into `saliency`.
 rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens, int n_fkeys, const void* memK,
                       const void* memV, int64_t mem_len, int64_t head_stride_tokens, int n_heads,
                       const rv_qsub* qs, void* out, float* lse, float* saliency, const void* sK, int64_t s_row,
-                      int64_t s_head, hipStream_t s, bool use_static = false) {
+                      int64_t s_head, hipStream_t s, bool use_static = false, float* sal_tiles = nullptr) {
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace* ws;
   rv_status st = ready_ws(&ws);
@@ -555,6 +557,19 @@ rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens,
   for (int q = 0; q < ws->n_queues; ++q) {
     a.n_chunks[q] = p.n_chunks[q];
     a.chunk_base[q] = p.chunk_base[q];
+  }
+  if (sal_tiles) {
+    rv::SalEpi e{};
+    e.tiles = sal_tiles;
+    e.K = (const uint16_t*)sK;
+    e.kv_row = s_row;
+    e.kv_head = s_head;
+    e.q_base = qs->n_special;
+    e.grid_w = qs->grid_w > 0 ? qs->grid_w : 1;
+    e.grid_cells = qs->grid_h * qs->grid_w;
+    e.stride = qs->stride;
+    RV_HIP(rv::launch_attention_saliency(a, e, p.grid, s), "attention launch");
+    return RV_OK;
   }
   // every unit whole in one chunk (no split) needs no merge launch
   RV_HIP(rv::launch_attention(a, p.grid, rv::plan_splits_units(p), s), "attention launch");
@@ -603,6 +618,29 @@ rv_status rv_attend_frame(const void* Q, const void* K, const void* V, int n_tok
   }
   return attend_impl(Q, K, V, n_tokens, n_tokens, memK, memV, mem_len, head_stride_tokens, n_heads, qs, out, lse,
                      saliency, K, (int64_t)n_heads * rv::kHeadDim, rv::kHeadDim, (hipStream_t)stream);
+}
+
+rv_status rv_attend_frame_fused(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
+                                const void* memV, int64_t mem_len, int64_t head_stride_tokens, int n_heads,
+                                int head_dim, const rv_qsub* qs, void* out, float* lse, float* sal_tiles,
+                                void* stream) {
+  if (n_tokens < 0 || n_tokens > rv::kMaxTokens)
+    return fail(RV_ERR_INVALID, "n_tokens must be in [0, %d] (got %d)", rv::kMaxTokens, n_tokens);
+  if (n_heads < 1) return fail(RV_ERR_INVALID, "n_heads must be >= 1");
+  if (head_dim != rv::kHeadDim) return fail(RV_ERR_INVALID, "head_dim must be 64 (got %d)", head_dim);
+  if (mem_len < 0) return fail(RV_ERR_INVALID, "mem_len must be >= 0");
+  if (mem_len > 0 && (!memK || !memV)) return fail(RV_ERR_INVALID, "memK/memV NULL with mem_len > 0");
+  if (mem_len > 0 && head_stride_tokens < mem_len)
+    return fail(RV_ERR_INVALID, "head_stride_tokens (%lld) < mem_len (%lld)", (long long)head_stride_tokens,
+                (long long)mem_len);
+  if (n_tokens == 0) return RV_OK;
+  if (!Q || !K || !V || !out || !lse || !sal_tiles)
+    return fail(RV_ERR_INVALID, "Q, K, V, out, lse and sal_tiles are required");
+  rv_status st = check_qsub(qs, n_tokens);
+  if (st != RV_OK) return st;
+  return attend_impl(Q, K, V, n_tokens, n_tokens, memK, memV, mem_len, head_stride_tokens, n_heads, qs, out, lse,
+                     nullptr, K, (int64_t)n_heads * rv::kHeadDim, rv::kHeadDim, (hipStream_t)stream, false,
+                     sal_tiles);
 }
 
 rv_status rv_attend_frame_noalloc(const void* Q, const void* K, const void* V, int n_tokens, const void* memK,
@@ -727,21 +765,23 @@ namespace {
 
 // staged: the frame's K, V are the rows each memory staged past its length (K, V
 // unused); the selected rows are compacted in place.
+// tiles: per-block saliency rows from rv_attend_frame_fused (then Q, lse and qs are unused).
 rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K, const void* const* V,
                        const float* const* lse, int n_tokens, const rv_qsub* qs, int budget, const rv_mem* mems,
                        int frame_id, float* const* saliency_out, int32_t* const* idx_out, void* stream,
-                       bool shared, bool staged) {
+                       bool shared, bool staged, const float* const* tiles = nullptr) {
   if (n_layers < 1 || n_layers > 4096) return fail(RV_ERR_INVALID, "n_layers must be in [1, 4096]");
-  if (!Q || (!staged && (!K || !V)) || !lse || !mems) return fail(RV_ERR_INVALID, "NULL pointer array");
+  if ((!tiles && (!Q || !lse)) || (!staged && (!K || !V)) || !mems)
+    return fail(RV_ERR_INVALID, "NULL pointer array");
   if (n_tokens < 1 || n_tokens > rv::kMaxTokens)
     return fail(RV_ERR_INVALID, "n_tokens must be in [1, %d] (got %d)", rv::kMaxTokens, n_tokens);
   if (budget < 0 || budget > n_tokens)
     return fail(RV_ERR_INVALID, "budget must be in [0, n_tokens] (got %d)", budget);
-  rv_status st = check_qsub(qs, n_tokens);
+  rv_status st = tiles ? RV_OK : check_qsub(qs, n_tokens);
   if (st != RV_OK) return st;
   const int H = mems[0] ? mems[0]->n_heads : 0;
   for (int l = 0; l < n_layers; ++l) {
-    if (!Q[l] || (!staged && (!K[l] || !V[l])) || !lse[l] || !mems[l])
+    if ((tiles ? !tiles[l] : (!Q[l] || !lse[l])) || (!staged && (!K[l] || !V[l])) || !mems[l])
       return fail(RV_ERR_INVALID, "layer %d: NULL tensor or memory", l);
     if (mems[l]->n_heads != H) return fail(RV_ERR_INVALID, "layer %d: head count differs", l);
     st = check_device(mems[l]);
@@ -757,19 +797,24 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
   st = ready_ws(&ws);
   if (st != RV_OK) return st;
   rv::AdmitArgs probe{};
-  rv::set_qsub(&probe, *qs);
   probe.n_tokens = n_tokens;
   probe.budget = budget;
-  probe.mode = rv::kModeBoth;
   probe.n_heads = H;
   probe.shared_select = shared ? 1 : 0;
-  rv::plan_saliency(&probe, std::min(n_layers, rv::kMaxLayersPerLaunch) * H, ws->n_cus, ws->max_lds);
+  if (tiles) {
+    probe.mode = rv::kModeSelect;
+    probe.sal_tiles = (n_tokens + rv::kAttnBQ - 1) / rv::kAttnBQ;
+  } else {
+    rv::set_qsub(&probe, *qs);
+    probe.mode = rv::kModeBoth;
+    rv::plan_saliency(&probe, std::min(n_layers, rv::kMaxLayersPerLaunch) * H, ws->n_cus, ws->max_lds);
+  }
   const size_t lds_cap = (size_t)rv::admit_max_dynamic_lds(ws->max_lds);
   if (rv::admit_lds_bytes(probe) > lds_cap)
     return fail(RV_ERR_INVALID, "frame too large for the admission workgroup's LDS");
   const int chunk_layers = std::min(n_layers, rv::kMaxLayersPerLaunch);
-  bool need_ws_sal = !saliency_out;
-  for (int l = 0; saliency_out && l < n_layers; ++l) need_ws_sal |= !saliency_out[l];
+  bool need_ws_sal = !tiles && !saliency_out;
+  for (int l = 0; !tiles && saliency_out && l < n_layers; ++l) need_ws_sal |= !saliency_out[l];
   if (need_ws_sal && ws->sal_floats < (size_t)chunk_layers * H * n_tokens)
     return fail(RV_ERR_CAPACITY,
                 "no saliency output given and the saliency workspace holds %zu values, %zu needed "
@@ -787,7 +832,7 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
     for (int i = 0; i < nl; ++i) {
       const int l = l0 + i;
       rv::AdmitLayer& L = b.layer[i];
-      L.Q = (const uint16_t*)Q[l];
+      L.Q = tiles ? nullptr : (const uint16_t*)Q[l];
       if (staged) {
         L.K = mems[l]->K + mems[l]->len * rv::kHeadDim;
         L.V = mems[l]->V + mems[l]->len * rv::kHeadDim;
@@ -799,8 +844,13 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
         L.kv_row = (int64_t)H * rv::kHeadDim;
         L.kv_head = rv::kHeadDim;
       }
-      L.lse = lse[l];
-      L.sal = (saliency_out && saliency_out[l]) ? saliency_out[l] : ws->sal + (size_t)i * H * n_tokens;
+      if (tiles) {
+        L.sal = const_cast<float*>(tiles[l]);
+        L.sal_out = saliency_out ? saliency_out[l] : nullptr;
+      } else {
+        L.lse = lse[l];
+        L.sal = (saliency_out && saliency_out[l]) ? saliency_out[l] : ws->sal + (size_t)i * H * n_tokens;
+      }
       L.idx = idx_out ? idx_out[l] : nullptr;
       L.memK = mems[l]->K;
       L.memV = mems[l]->V;
@@ -836,6 +886,14 @@ rv_status rv_admit_layers_shared(int n_layers, const void* const* Q, const void*
                                  int32_t* const* idx_out, void* stream) {
   return admit_layers(n_layers, Q, K, V, lse, n_tokens, qs, budget, mems, frame_id, saliency_out, idx_out,
                       stream, true, false);
+}
+
+rv_status rv_admit_layers_tiled(int n_layers, const float* const* sal_tiles, int n_tokens, int budget,
+                                const void* const* K, const void* const* V, const rv_mem* mems, int frame_id,
+                                float* const* saliency_out, int32_t* const* idx_out, void* stream) {
+  if (!sal_tiles) return fail(RV_ERR_INVALID, "sal_tiles is NULL");
+  return admit_layers(n_layers, nullptr, K, V, nullptr, n_tokens, nullptr, budget, mems, frame_id, saliency_out,
+                      idx_out, stream, false, false, sal_tiles);
 }
 
 rv_status rv_admit_staged_layers(int n_layers, const void* const* Q, const float* const* lse, int n_tokens,

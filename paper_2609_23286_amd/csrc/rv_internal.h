@@ -10,6 +10,10 @@
 namespace rv {
 
 hipError_t launch_attention(const AttnArgs& a, int grid, bool merge, hipStream_t s);
+// The attention launch with the saliency in its epilogue: the forward launch, then one
+// merge workgroup per unit that forms the unit's outputs and LSE (when its key range was
+// split) and then the unit's row of per-block saliency (SalEpi).
+hipError_t launch_attention_saliency(const AttnArgs& a, const SalEpi& e, int grid, hipStream_t s);
 // Device address, on the current device, of the library's static partial-slot array
 // (kStaticScratchSlots slots of kAttnSlotFloats floats).
 hipError_t static_scratch_address(float** ptr);

@@ -62,6 +62,20 @@ constexpr size_t kAttnSlotBytes = (size_t)kAttnSlotFloats * 4;
 // more than the 1,040 the default plans on an MI355X (256 CUs, 8 XCDs) can take.
 constexpr int kStaticScratchSlots = 1152;
 
+// Saliency in the attention epilogue (Sec. 3.3, saliency score): the merge launch, once it
+// has each query's final LSE, sums exp(z_ij - LSE_i) over the sampled queries of its
+// 128-query block for every frame key j, into row b of tiles[h][b][j] (b = block).
+struct SalEpi {
+  float* tiles;            // [H][q_tiles][N]
+  const uint16_t* K;       // frame keys: row j of head h at K + j * kv_row + h * kv_head
+  int64_t kv_row;
+  int64_t kv_head;
+  int q_base;              // sampled query i of the frame: token q_base + r with r < grid_cells,
+  int grid_w;              //   (r / grid_w) % stride == 0 and (r % grid_w) % stride == 0
+  int grid_cells;
+  int stride;
+};
+
 // One layer's share of the saliency / selection / append kernel.
 struct AdmitLayer {
   const uint16_t* Q;       // [N][H][64]   (saliency)
@@ -71,6 +85,8 @@ struct AdmitLayer {
   int64_t kv_head;         // elements between heads' rows of one token
   const float* lse;        // [H][N]       (saliency)
   float* sal;              // [H][N]       written by saliency, read by selection
+                           //   ([H][sal_tiles][N] per-block rows when sal_tiles > 0)
+  float* sal_out;          // [H][N]       the summed saliency (sal_tiles > 0; optional)
   int32_t* idx;            // [H][budget]  optional output
   uint16_t* memK;          // [H][head_stride][64]
   uint16_t* memV;
@@ -104,6 +120,8 @@ struct AdmitArgs {
   int shared_select;       // selection: one top-k per layer on the head sum, shared by all heads
   int in_place;            // selection: K, V are the staged rows of the destination arena, so
                            //   the append is an in-place compaction (read before write)
+  int sal_tiles;           // selection: rows of per-block saliency per head, summed in block
+                           //   order before the selection (0: one row, the saliency itself)
 };
 
 constexpr int kSalQStride = kHeadDim + 8;  // staged sampled-query rows: 72 elements (144 bytes)

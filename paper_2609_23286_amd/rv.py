@@ -61,6 +61,8 @@ def _load():
         "rv_mem_save": ([vp, ctypes.c_char_p], i32),
         "rv_mem_load": ([vp, ctypes.c_char_p], i32),
         "rv_attend_frame": ([vp, vp, vp, i32, vp, vp, i64, i64, i32, i32, P(rv_qsub), vp, vp, vp, vp], i32),
+        "rv_attend_frame_fused": ([vp, vp, vp, i32, vp, vp, i64, i64, i32, i32, P(rv_qsub), vp, vp, vp, vp], i32),
+        "rv_admit_layers_tiled": ([i32, P(vp), i32, i32, P(vp), P(vp), P(vp), i32, P(vp), P(vp), vp], i32),
         "rv_attend_frame_noalloc": ([vp, vp, vp, i32, vp, vp, i64, i64, i32, i32, P(rv_qsub), vp, vp, vp, vp],
                                     i32),
         "rv_admit": ([vp, i32, vp, vp, i32, vp, i32, vp, vp], i32),
@@ -265,6 +267,40 @@ def attend_frame(Q, K, V, mem, out, lse, saliency=None, qs=None, stream=None,
         ctypes.byref(q) if q is not None else None,
         _ptr(out, shp, 2, "out"), _ptr(lse, (H, N), 4, "lse"),
         _ptr(saliency, (H, N), 4, "saliency"), _stream(stream)))
+
+
+QUERY_BLOCK = 128
+
+
+def attend_frame_fused(Q, K, V, mem, out, lse, sal_tiles, qs, stream=None):
+    """rv_attend_frame_fused: attention with the saliency formed in its epilogue, per
+    128-query block: sal_tiles [H, ceil(N / 128), N] fp32."""
+    N, H, d = Q.shape
+    mk, mv, hs = mem.view()
+    shp = (N, H, d)
+    q = qs if isinstance(qs, rv_qsub) else rv_qsub(*qs)
+    _check(_lib.rv_attend_frame_fused(
+        _ptr(Q, shp, 2, "Q"), _ptr(K, shp, 2, "K"), _ptr(V, shp, 2, "V"), N, ctypes.c_void_p(mk),
+        ctypes.c_void_p(mv), mem.len, hs, H, d, ctypes.byref(q), _ptr(out, shp, 2, "out"),
+        _ptr(lse, (H, N), 4, "lse"), _ptr(sal_tiles, (H, -(-N // QUERY_BLOCK), N), 4, "sal_tiles"),
+        _stream(stream)))
+
+
+def admit_layers_tiled(sal_tiles, budget, K, V, mems, frame_id, saliency_out=None, idx_out=None, stream=None):
+    """rv_admit_layers_tiled over lists of per-layer sal_tiles [H, ceil(N / 128), N], K, V
+    [N, H, 64] and Memory objects."""
+    L = len(mems)
+    N, H, d = K[0].shape
+    arr = ctypes.c_void_p * L
+
+    def pack(ts, shape, itemsize, what):
+        return arr(*[_ptr(t, shape, itemsize, f"{what}[{i}]") for i, t in enumerate(ts)])
+
+    sal = pack(saliency_out, (H, N), 4, "saliency_out") if saliency_out is not None else None
+    idx = pack(idx_out, (H, budget), 4, "idx_out") if idx_out is not None else None
+    _check(_lib.rv_admit_layers_tiled(
+        L, pack(sal_tiles, (H, -(-N // QUERY_BLOCK), N), 4, "sal_tiles"), N, budget, pack(K, (N, H, d), 2, "K"),
+        pack(V, (N, H, d), 2, "V"), arr(*[m.handle for m in mems]), frame_id, sal, idx, _stream(stream)))
 
 
 def attend_staged(Q, mem, out, lse, saliency=None, qs=None, stream=None):

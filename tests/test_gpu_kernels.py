@@ -553,3 +553,76 @@ def test_staged_calls_need_a_staged_frame(rv):
     k, v, hs = mem.stage(N)
     assert k and v and hs >= N and mem.len == 0
     mem.close()
+
+
+FUSED_CASES = [  # (N, H, M, qs, plan overrides): ragged blocks, empty memory, a block with no
+                 # sampled query, every query sampled, units covered whole by one chunk
+    (1041, 16, 0, (28, 37, 5, 2), {}),
+    (1041, 16, 2500, (28, 37, 5, 2), {}),
+    (1041, 16, 700, (28, 37, 5, 1), {}),
+    (300, 4, 700, (1, 300, 0, 2), {}),
+    (130, 3, 1000, (10, 13, 0, 3), {}),
+    (65, 2, 63, (5, 13, 0, 2), {}),
+    (1, 1, 0, (1, 1, 0, 1), {}),
+    (400, 2, 200, (0, 10, 400, 2), {}),                     # empty subset: every row 0
+    (333, 4, 1500, (9, 37, 0, 2), {"RV_ATTN_WG_PER_CU": "1", "RV_ATTN_MIN_CHUNK": "100000"}),
+]
+
+
+@pytest.mark.parametrize("N,H,M,qs,env", FUSED_CASES)
+def test_fused_saliency_matches_oracle(rv, N, H, M, qs, env, monkeypatch):
+    """rv_attend_frame_fused (saliency in the attention epilogue, per 128-query block) and
+    rv_admit_layers_tiled: out and LSE bit for bit rv_attend_frame's and within the oracle
+    bounds; every block's row against the oracle's column mass over that block's sampled
+    queries; the summed saliency against the oracle's; the selection exact on the GPU's own
+    saliency and under the band rule on the oracle's; the appended rows."""
+    import torch
+    for k_, v_ in env.items():
+        monkeypatch.setenv(k_, v_)
+    print(f"fused N={N} H={H} M={M} qs={qs} {env}", flush=True)
+    budget = min(10, N)
+    Q, K, V = frame(500 + N + M, N, H)
+    memK, memV = memory_rows(510 + N + M, H, M)
+    mem = rv.Memory(H, reserve_tokens=M + budget, max_tokens=M + budget)
+    if M:
+        mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+    Qd, Kd, Vd = to_dev(Q), to_dev(K), to_dev(V)
+    nb = -(-N // 128)
+    out = torch.empty_like(Qd)
+    lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
+    tiles = torch.full((H, nb, N), -1.0, dtype=torch.float32, device="cuda")
+    rv.attend_frame_fused(Qd, Kd, Vd, mem, out, lse, tiles, qs)
+    out_f = torch.empty_like(Qd)
+    lse_f = torch.empty_like(lse)
+    rv.attend_frame(Qd, Kd, Vd, mem, out_f, lse_f)
+    rv.device_status()
+    assert (out == out_f).all() and (lse == lse_f).all()
+    out_o, lse_o = oracle.attend(Q, K, V, memK, memV, M)
+    assert np.abs(bf16_to_f64(to_host_u16(out)) - out_o).max() <= OUT_ATOL
+    assert np.abs(lse.cpu().numpy() - lse_o).max() <= LSE_ATOL
+    qidx = oracle.qsub_index(*qs)
+    t_h = tiles.cpu().numpy().astype(np.float64)
+    for b in range(nb):
+        sel = qidx[(qidx >= 128 * b) & (qidx < 128 * (b + 1))]
+        ref = oracle.column_mass(Q, sel, lse_o[:, sel], K, "frame")
+        assert (np.abs(t_h[:, b] - ref) <= SAL_RTOL * ref).all(), f"block {b}"
+    sal_o = oracle.saliency(Q, K, lse_o, qidx)
+    sal = torch.full((H, N), -1.0, dtype=torch.float32, device="cuda")
+    idx = torch.full((H, budget), -1, dtype=torch.int32, device="cuda")
+    rv.admit_layers_tiled([tiles], budget, [Kd], [Vd], [mem], 6, [sal], [idx])
+    rv.device_status()
+    s_h = sal.cpu().numpy().astype(np.float64)
+    assert (np.abs(s_h - sal_o) <= SAL_RTOL * sal_o).all()
+    acc = t_h[:, 0].astype(np.float32)
+    for b in range(1, nb):
+        acc = acc + t_h[:, b].astype(np.float32)
+    assert (acc == s_h.astype(np.float32)).all()              # the rows summed in block order
+    i_h = idx.cpu().numpy()
+    assert (i_h == oracle.topk(s_h, budget)).all()
+    check_index_sets(i_h, sal_o, budget)
+    mk, mv, prov = (x.numpy() for x in mem.read())
+    for h in range(H):
+        assert (mk[h, M:].view(np.uint16) == K[i_h[h], h]).all()
+        assert (mv[h, M:].view(np.uint16) == V[i_h[h], h]).all()
+        assert (prov[h, M:, 0] == 6).all() and (prov[h, M:, 1] == i_h[h]).all()
+    mem.close()
