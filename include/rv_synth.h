@@ -23,12 +23,15 @@ extern "C" {
 
 /* One frame of n_layers layers (layers layer0 .. layer0+n_layers-1):
  * out = [n_layers][3][n_tokens][n_heads][head_dim] bf16, the three tensors being Q, K, V
- * of that layer, each N(0, sigma^2)-like; then, per (layer, head), n_plant key rows at
- * Philox-drawn positions are replaced by alpha * |k| along the sum of that head's
+ * of that layer, each N(0, sigma^2)-like; with key_lognormal_sigma > 0 every key row is
+ * then scaled by a log-normal factor exp(key_lognormal_sigma * xi) (heavy-tailed key
+ * norms; the fp64 exponential may differ from the CPU generator's in its last bit, which
+ * can move a rare key element by one bf16 step); then, per (layer, head), n_plant key rows
+ * at Philox-drawn positions are replaced by alpha * |k| along the sum of that head's
  * queries.  n_tokens <= 8192, head_dim == 64. */
 int rvs_frame_qkv(uint64_t seed, uint32_t frame, int layer0, int n_layers, int n_tokens,
                   int n_heads, int head_dim, float sigma, int n_plant, double alpha,
-                  uint16_t *out, void *stream);
+                  double key_lognormal_sigma, uint16_t *out, void *stream);
 
 /* Near-Gaussian bf16 tensor of n elements for counter stream (frame, layer, tag). */
 int rvs_normal_bf16(uint64_t seed, uint32_t frame, int layer, int tag, int64_t n, float sigma,

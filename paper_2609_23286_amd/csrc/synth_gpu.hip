@@ -12,6 +12,7 @@ constexpr uint32_t kW0 = 0x9E3779B9u, kW1 = 0xBB67AE85u;
 constexpr int kIHMean = 262140;
 constexpr double kIHSd = 53509.91992145008;  // sqrt(8 * (65536^2 - 1) / 12), as the CPU generator
 constexpr int kTagPlant = 3;  // Q, K, V use tags 0, 1, 2 (tensor index within a layer)
+constexpr int kTagLogn = 6;   // heavy-tailed key scales
 constexpr int kMaxPlantTokens = 8192;
 
 struct U4 {
@@ -50,9 +51,12 @@ __device__ __forceinline__ uint16_t normal_elem(uint64_t e, uint32_t frame, uint
   return f32_to_bf16_rne((float)(s - kIHMean) * scale);
 }
 
-// out = [n_layers][3][n][H][d]; grid-stride over all elements.
+// out = [n_layers][3][n][H][d]; grid-stride over all elements.  ln_sigma > 0: every key row
+// (token j, head h) is scaled by exp(ln_sigma * xi), xi the near-Gaussian of element j * H + h
+// of stream (frame, layer << 8 | 6): fp64 exponential, rounded to fp32, one fp32 multiply,
+// rounded to bf16 (the CPU generator's steps).
 __global__ void gen_qkv_kernel(uint64_t seed, uint32_t frame, int layer0, int n_layers, int64_t per_tensor,
-                               float scale, uint16_t* out) {
+                               float scale, double ln_sigma, uint16_t* out) {
   const int64_t total = per_tensor * 3 * n_layers;
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
   for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total;
@@ -61,7 +65,17 @@ __global__ void gen_qkv_kernel(uint64_t seed, uint32_t frame, int layer0, int n_
     const int64_t e = g - tensor * per_tensor;
     const int layer = layer0 + (int)(tensor / 3);
     const int tag = (int)(tensor % 3);
-    out[g] = normal_elem((uint64_t)e, frame, ((uint32_t)layer << 8) | (uint32_t)tag, k0, k1, scale);
+    uint16_t v = normal_elem((uint64_t)e, frame, ((uint32_t)layer << 8) | (uint32_t)tag, k0, k1, scale);
+    if (tag == 1 && ln_sigma > 0.0) {
+      const uint64_t row = (uint64_t)e / 64;  // token * H + head
+      const U4 w = philox10(U4{(uint32_t)row, (uint32_t)(row >> 32), frame, ((uint32_t)layer << 8) | (uint32_t)kTagLogn},
+                            k0, k1);
+      const int ih = (int)(w.x & 0xFFFFu) + (int)(w.x >> 16) + (int)(w.y & 0xFFFFu) + (int)(w.y >> 16) +
+                     (int)(w.z & 0xFFFFu) + (int)(w.z >> 16) + (int)(w.w & 0xFFFFu) + (int)(w.w >> 16) - kIHMean;
+      const float s = (float)exp(ln_sigma * ((double)ih / kIHSd));
+      v = f32_to_bf16_rne(bf16_to_f32(v) * s);
+    }
+    out[g] = v;
   }
 }
 
@@ -146,9 +160,10 @@ extern "C" int rvs_normal_bf16(uint64_t seed, uint32_t frame, int layer, int tag
 }
 
 extern "C" int rvs_frame_qkv(uint64_t seed, uint32_t frame, int layer0, int n_layers, int n_tokens, int n_heads,
-                             int head_dim, float sigma, int n_plant, double alpha, uint16_t* out, void* stream) {
+                             int head_dim, float sigma, int n_plant, double alpha, double key_lognormal_sigma,
+                             uint16_t* out, void* stream) {
   if (!out || layer0 < 0 || n_layers < 1 || n_tokens < 1 || n_tokens > kMaxPlantTokens || n_heads < 1 ||
-      head_dim != 64 || n_plant < 0 || n_plant > n_tokens)
+      head_dim != 64 || n_plant < 0 || n_plant > n_tokens || !(key_lognormal_sigma >= 0.0))
     return 1;
   const float scale = (float)((double)sigma / kIHSd);
   const int64_t per_tensor = (int64_t)n_tokens * n_heads * head_dim;
@@ -156,7 +171,7 @@ extern "C" int rvs_frame_qkv(uint64_t seed, uint32_t frame, int layer0, int n_la
   const int64_t blocks = (total + 255) / 256;
   hipStream_t s = (hipStream_t)stream;
   hipLaunchKernelGGL(gen_qkv_kernel, dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0, s, seed,
-                     frame, layer0, n_layers, per_tensor, scale, out);
+                     frame, layer0, n_layers, per_tensor, scale, key_lognormal_sigma, out);
   if (hipGetLastError() != hipSuccess) return 4;
   if (n_plant > 0) {
     hipLaunchKernelGGL(plant_kernel, dim3((unsigned)(n_layers * n_heads)), dim3(256), 0, s, seed, frame, layer0,

@@ -373,7 +373,7 @@ def _load_synth():
         s = ctypes.CDLL(SYNTH_LIB_PATH)
         s.rvs_frame_qkv.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_int, ctypes.c_double,
-                                    ctypes.c_void_p, ctypes.c_void_p]
+                                    ctypes.c_double, ctypes.c_void_p, ctypes.c_void_p]
         s.rvs_frame_qkv.restype = ctypes.c_int
         s.rvs_normal_bf16.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int, ctypes.c_int,
                                       ctypes.c_int64, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
@@ -385,11 +385,9 @@ def _load_synth():
 def gpu_frame_qkv(cfg, frame, out, layer0=0, n_layers=None, stream=None):
     """Fill out = [n_layers, 3, N, H, 64] (2-byte) with frame `frame` of cfg's stream."""
     n_layers = cfg.n_layers if n_layers is None else n_layers
-    if cfg.lognormal_sigma:
-        raise ValueError("the GPU generator does not draw heavy-tailed key norms")
     shape = (n_layers, 3, cfg.n_tokens, cfg.n_heads, cfg.head_dim)
     rc = _load_synth().rvs_frame_qkv(cfg.seed, frame & 0xFFFFFFFF, layer0, n_layers, cfg.n_tokens, cfg.n_heads,
-                                     cfg.head_dim, cfg.sigma, cfg.n_plant, cfg.alpha,
+                                     cfg.head_dim, cfg.sigma, cfg.n_plant, cfg.alpha, cfg.lognormal_sigma,
                                      _ptr(out, shape, 2, "out"), _stream(stream))
     if rc != 0:
         raise RVError(rc, "rvs_frame_qkv failed")

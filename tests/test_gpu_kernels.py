@@ -340,6 +340,26 @@ def test_gpu_generator_matches_cpu_generator(rv):
         assert (got[0, 1] == K).all()
 
 
+def test_gpu_generator_heavy_tailed_keys(rv):
+    """The square-resolution stream's log-normal key scales on the GPU: Q and V bit for bit
+    the CPU generator's; K too except where the two fp64 exponentials differ in their last
+    bit, which can move an element by one bf16 step (rare, and never more)."""
+    import torch
+    cfg = synth.CONFIGS["square_2000"]
+    out = torch.empty((2, 3, cfg.n_tokens, cfg.n_heads, 64), dtype=torch.int16, device="cuda")
+    rv.gpu_frame_qkv(cfg, 41, out, layer0=5, n_layers=2)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint16)
+    for i, layer in enumerate((5, 6)):
+        Q, K, V = synth.frame_qkv(cfg, layer, 41)
+        assert (got[i, 0] == Q).all() and (got[i, 2] == V).all()
+        diff = np.abs(got[i, 1].astype(np.int32) - K.astype(np.int32))   # bf16 steps (same sign)
+        assert diff.max() <= 1 and (diff > 0).mean() < 1e-4
+        # the planted rows carry the scaled norms: the keys really are heavy-tailed
+        norms = np.linalg.norm(bf16_to_f64(K), axis=2)
+        assert norms.max() / np.median(norms) > 3.0
+
+
 def test_memory_snapshot_round_trip(rv, tmp_path):
     """rv_mem_save / rv_mem_load: rows and provenance survive a round trip into a fresh
     memory (which grows to fit); a mismatched head count, an oversized snapshot, a

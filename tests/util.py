@@ -10,10 +10,13 @@ BAND = 1e-4          # relative band around the k-th largest oracle saliency
 
 
 def out_error_bound(out_oracle, v_absmax):
-    """Worst-case error of a bf16 attention output: the probabilities are rounded to
-    bf16 (relative error <= 2^-8 each, so <= 2^-8 max|v| after normalisation) and the
-    output is rounded to bf16 (<= 2^-8 |o|); fp32 accumulation adds ~1e-6."""
-    return 2.0 ** -8 * (float(np.abs(out_oracle).max()) + float(v_absmax)) + 1e-5
+    """Worst-case error of a bf16 attention output, with bf16's unit roundoff u = 2^-8:
+    the probabilities are rounded to bf16 for the value product (relative error <= u
+    each, so <= u max|v| after normalisation by the fp32 row sum); a split plan stores
+    each partial output -- a convex combination of value rows -- in bf16 (<= u max|v|
+    more, the merge weights summing to one); and the output is rounded to bf16
+    (<= u |o|).  fp32 accumulation adds ~1e-6."""
+    return 2.0 ** -8 * (float(np.abs(out_oracle).max()) + 2.0 * float(v_absmax)) + 1e-5
 
 
 def to_dev(a):
