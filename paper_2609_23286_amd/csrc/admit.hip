@@ -56,7 +56,14 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
   const int groups = a.sal_groups;
-  const int lh = blockIdx.x / groups, g = blockIdx.x - lh * groups;
+  // Workgroup b runs on XCD b % X (ids are dealt round-robin over the XCDs): the groups of
+  // (layer, head) lh = l_x X + x are ids (l_x groups + g) X + x, all on XCD x, so the
+  // head's sampled query rows and LSE that every group stages are read once from memory
+  // and then from that XCD's L2.  Placement only steers locality.
+  const int X = a.sal_xcds > 0 ? a.sal_xcds : 1;
+  const int xcd = blockIdx.x % X, rr = blockIdx.x / X;
+  const int lh = (rr / groups) * X + xcd, g = rr - (rr / groups) * groups;
+  if (lh >= a.n_layers * H) return;  // uniform: ids past the last (layer, head)
   const int layer = lh / H, h = lh - layer * H;
   const int n_blocks = (N + 31) / 32;
   const int per_group = (n_blocks + groups - 1) / groups;
@@ -552,7 +559,9 @@ hipError_t launch_admit(const AdmitArgs& a, int max_lds, hipStream_t s) {
   if (a.mode & kModeSaliency) {
     hipError_t e = set_lds_limit((const void*)sal_kernel, &sal_attr, limit);
     if (e != hipSuccess) return e;
-    const unsigned grid = (unsigned)(a.n_layers * a.n_heads) * (unsigned)a.sal_groups;
+    const unsigned X = (unsigned)(a.sal_xcds > 0 ? a.sal_xcds : 1);
+    const unsigned n_lh = (unsigned)(a.n_layers * a.n_heads);
+    const unsigned grid = (n_lh + X - 1) / X * X * (unsigned)a.sal_groups;
     hipLaunchKernelGGL(sal_kernel, dim3(grid), dim3(NT), sal_lds_bytes(a), s, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

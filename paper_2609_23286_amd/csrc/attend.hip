@@ -37,6 +37,8 @@
 //   synchronisation, so results do not depend on where the hardware places the
 //   workgroups; the merge workgroups follow the queues' XCD mapping only so that the
 //   partials are likely still in that XCD's L2).
+#include <type_traits>
+
 #include "rv_internal.h"
 
 namespace rv {
@@ -178,7 +180,10 @@ struct SoftmaxState {
   f32x16 o1;    // d = 32..63
 };
 
-// One 64-key tile for this wave's 32 queries.
+// One 64-key tile for this wave's 32 queries.  kFirst: the segment's first tile, whose
+// running reference is still unset, so its maximum is taken directly (the exact path of
+// a later tile, without the rescale of an empty state).
+template <bool kFirst>
 __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8 (&qf)[4], int lane, int valid,
                                              SoftmaxState& sm) {
   const int l32 = lane & 31, half = lane >> 5;
@@ -210,23 +215,17 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
   // as they would relative to the true maximum.
   bf16x8 p[4];
   float rsum = -0.f;  // -0 + x == x: the first add folds away
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], kScaleLog2, -sm.m));
-    const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], kScaleLog2, -sm.m));
-    rsum += e0 + e1;
-    p[r >> 3][r & 7] = (__bf16)e0;
-    p[2 + (r >> 3)][r & 7] = (__bf16)e1;
-  }
-  if (__any(!(rsum < kOverflowGuard))) {
+  auto exact = [&]() {
     float mx = fmaxf(s0[0], s1[0]);
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
     const float m_new = fmaxf(sm.m, half_max(mx) * kScaleLog2);
-    const float alpha = __builtin_amdgcn_exp2f(sm.m - m_new);
-    sm.l *= alpha;
-    sm.o0 *= alpha;
-    sm.o1 *= alpha;
+    if (!kFirst) {
+      const float alpha = __builtin_amdgcn_exp2f(sm.m - m_new);
+      sm.l *= alpha;
+      sm.o0 *= alpha;
+      sm.o1 *= alpha;
+    }
     sm.m = m_new;
     rsum = -0.f;
 #pragma unroll
@@ -237,6 +236,19 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
       p[r >> 3][r & 7] = (__bf16)e0;
       p[2 + (r >> 3)][r & 7] = (__bf16)e1;
     }
+  };
+  if (kFirst) {
+    exact();
+  } else {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s0[r], kScaleLog2, -sm.m));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s1[r], kScaleLog2, -sm.m));
+      rsum += e0 + e1;
+      p[r >> 3][r & 7] = (__bf16)e0;
+      p[2 + (r >> 3)][r & 7] = (__bf16)e1;
+    }
+    if (__any(!(rsum < kOverflowGuard))) exact();
   }
   sm.l += rsum;
 
@@ -399,14 +411,15 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   // Ring of NSTAGE (4) tiles, two computed per barrier: tile t0 + j lives in stage j % 4,
   // so every stage offset is a compile-time constant of the unrolled loop.  The next
   // pair streams into the two stages the previous pair used (freed at the last barrier)
-  // while this pair is computed.
-  auto step = [&](auto phase, int t) {
+  // while this pair is computed.  The first step is peeled off: its first tile sets the
+  // running reference.
+  auto step = [&](auto phase, auto first, int t) {
     constexpr int P = decltype(phase)::value;
     if (t + 2 < t1) load_tile<(P + 2) % NSTAGE>(tc, t + 2, ldsw);
     if (t + 3 < t1) load_tile<(P + 3) % NSTAGE>(tc, t + 3, ldsw);
     if (wave_active) {
-      tile_compute(lds + P * STAGE, qf, lane, tile_valid(tc, t), sm);
-      if (t + 1 < t1) tile_compute(lds + (P + 1) * STAGE, qf, lane, tile_valid(tc, t + 1), sm);
+      tile_compute<decltype(first)::value>(lds + P * STAGE, qf, lane, tile_valid(tc, t), sm);
+      if (t + 1 < t1) tile_compute<false>(lds + (P + 1) * STAGE, qf, lane, tile_valid(tc, t + 1), sm);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -415,10 +428,11 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   if (t0 + 1 < t1) load_tile<1>(tc, t0 + 1, ldsw);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  for (int t = t0; t < t1; t = uniform(t + 4)) {
-    step(StageConst<0>{}, t);
+  step(StageConst<0>{}, std::true_type{}, t0);
+  for (int t = t0 + 2; t < t1; t = uniform(t + 4)) {
+    step(StageConst<2>{}, std::false_type{}, t);
     if (t + 2 >= t1) break;
-    step(StageConst<2>{}, t + 2);
+    step(StageConst<0>{}, std::false_type{}, t + 2);
   }
 
   const float l_tot = half_sum(sm.l);

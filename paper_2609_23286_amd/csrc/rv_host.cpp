@@ -587,6 +587,7 @@ rv_status attend_impl(const void* Q, const void* K, const void* V, int n_tokens,
     b.n_heads = n_heads;
     b.n_layers = 1;
     b.mode = rv::kModeSaliency;
+    b.sal_xcds = ws->n_queues;
     rv::plan_saliency(&b, n_heads, ws->n_cus, ws->max_lds);
     RV_HIP(rv::launch_admit(b, ws->max_lds, s), "saliency launch");
   }
@@ -807,6 +808,7 @@ rv_status admit_layers(int n_layers, const void* const* Q, const void* const* K,
   } else {
     rv::set_qsub(&probe, *qs);
     probe.mode = rv::kModeBoth;
+    probe.sal_xcds = ws->n_queues;
     rv::plan_saliency(&probe, std::min(n_layers, rv::kMaxLayersPerLaunch) * H, ws->n_cus, ws->max_lds);
   }
   const size_t lds_cap = (size_t)rv::admit_max_dynamic_lds(ws->max_lds);

@@ -117,6 +117,8 @@ struct AdmitArgs {
   int stage_queries;       // saliency: stage the sampled query rows in LDS
   int q_pass;              // saliency: sampled query rows staged per pass (multiple of 32)
   int sal_groups;          // saliency: workgroups per (layer, head)
+  int sal_xcds;            // saliency: XCDs the workgroup ids are dealt over (a head's groups
+                           //   are numbered to share one; locality only)
   int shared_select;       // selection: one top-k per layer on the head sum, shared by all heads
   int in_place;            // selection: K, V are the staged rows of the destination arena, so
                            //   the append is an in-place compaction (read before write)
