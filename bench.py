@@ -240,6 +240,9 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
             for r in csv.DictReader(open(f)):
                 name = r["Kernel_Name"].replace("rv::(anonymous namespace)::", "").split("(")[0]
                 out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                if r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+                    out[name].setdefault("duration_ns", []).append(
+                        float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
         return out
 
     a, b = per_kernel(dir_a), per_kernel(dir_b)
@@ -251,15 +254,20 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
     for i, cs in enumerate(MFMA_PASSES):
         lines.append(f"timeout -s KILL 600 rocprofv3 --pmc {' '.join(cs)} --output-format csv -d <out>/m{i} "
                      f"-o m{i} -- python /root/repo/bench.py {bench_args()} --no-cpu-baseline")
-    lines += [f"python /root/repo/bench.py {bench_args()} --mfma-summary <out>/m0 <out>/m1 <bench json>", "```",
+    lines += [f"python /root/repo/bench.py {bench_args()} --mfma-summary <out>/m0 <out>/m1 <kernel-trace run's json>",
+              "```",
               "", "Counters are summed over the chip (GRBM_GUI_ACTIVE over its 8 XCDs).  Per dispatch:",
               "`busy` = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024 SIMDs), the fraction of SIMD",
-              "cycles the matrix core is busy (rocprofv3's MfmaUtil); `coexec` = SQ_VALU_MFMA_COEXEC_CYCLES /",
+              "cycles the matrix core is busy (rocprofv3's MfmaUtil); `busy@2.4` = the same busy cycles over",
+              "1024 SIMDs x the dispatch's duration (its timestamps) x 2.4 GHz, i.e. executed MFMA work as a",
+              "fraction of the dense peak (dispatches run one at a time under counter collection, so the",
+              "durations are a little longer than in the kernel trace); `coexec` = SQ_VALU_MFMA_COEXEC_CYCLES /",
               "SQ_VALU_MFMA_BUSY_CYCLES, the share of those cycles in which a vector instruction was also",
               "issued; `valu` = 4 x SQ_ACTIVE_INST_VALU / (GRBM_GUI_ACTIVE / 8 x 1024), vector-ALU cycles per",
               "SIMD cycle (quad-cycle units); `bf16 flops` = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16.", "",
-              "| Kernel | dispatches | GUI cycles / XCD | busy | coexec | valu | MFMA instrs | bf16 flops | "
-              "VALU instrs | exp/log (f32 trans) instrs |", "|---|---|---|---|---|---|---|---|---|---|"]
+              "| Kernel | dispatches | duration us | GUI cycles / XCD | busy | busy@2.4 | coexec | valu | MFMA instrs | "
+              "bf16 flops | VALU instrs | exp/log (f32 trans) instrs |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     rows = {}
     for name in sorted(set(a) | set(b)):
         if name not in KERNEL_SOURCES:
@@ -268,7 +276,9 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
         try:
             gui = mean(ca["GRBM_GUI_ACTIVE"]) / MI355X_XCDS
             busy = mean(ca["SQ_VALU_MFMA_BUSY_CYCLES"])
+            dur = mean(ca["duration_ns"])
             r = {"n": len(ca["GRBM_GUI_ACTIVE"]), "gui": gui, "busy": busy / (gui * MI355X_SIMDS),
+                 "dur": dur, "busy24": busy / (MI355X_SIMDS * dur * 2.4),
                  "coexec": mean(ca["SQ_VALU_MFMA_COEXEC_CYCLES"]) / max(busy, 1.0),
                  "mfma": mean(ca["SQ_INSTS_MFMA"]), "flops": 512.0 * mean(ca["SQ_INSTS_VALU_MFMA_MOPS_BF16"]),
                  "valu": 4.0 * mean(cb["SQ_ACTIVE_INST_VALU"]) / (mean(cb["GRBM_GUI_ACTIVE"]) / MI355X_XCDS
@@ -277,17 +287,20 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
         except KeyError as e:
             raise SystemExit(f"{name}: counter {e} missing from the CSVs")
         rows[name] = r
-        lines.append(f"| `{name}` | {r['n']} | {r['gui']:.0f} | {100 * r['busy']:.1f} % | {100 * r['coexec']:.1f} % | "
+        lines.append(f"| `{name}` | {r['n']} | {r['dur'] / 1e3:.1f} | {r['gui']:.0f} | {100 * r['busy']:.1f} % | "
+                     f"{100 * r['busy24']:.1f} % | {100 * r['coexec']:.1f} % | "
                      f"{100 * r['valu']:.1f} % | {r['mfma']:.0f} | {r['flops']:.3e} | {r['vinst']:.0f} | "
                      f"{r['trans']:.0f} |")
     f = rows.get("attn_fwd_kernel")
     if f:
         alg = bench["roofline"]["algorithmic_flops_per_launch"]
-        lines += ["", "The attention forward kernel against the benchmark line of the same command:", "",
+        lines += ["", "The attention forward kernel against the benchmark line of the same command (its kernel-trace",
+                  "run, whose line is not distorted by counter collection):", "",
                   f"- algorithmic flops per launch (4 x 64 per query-key pair): {alg:.4e}; bf16 MFMA flops "
                   f"executed per dispatch: {f['flops']:.4e} (x{f['flops'] / alg:.3f}: query tiles padded to 128 "
                   "rows and key tiles to 64)",
-                  f"- matrix core busy {100 * f['busy']:.1f} % of SIMD cycles; a vector instruction issued in "
+                  f"- executed MFMA work {100 * f['busy24']:.1f} % of the dense peak over the dispatch's own "
+                  f"duration; matrix core busy {100 * f['busy']:.1f} % of SIMD cycles; a vector instruction issued in "
                   f"{100 * f['coexec']:.1f} % of those; vector ALU active {100 * f['valu']:.1f} % of SIMD cycles",
                   f"- benchmark line: {bench['roofline']['achieved']:.1f} TFLOP/s = "
                   f"{100 * bench['roofline']['frac']:.1f} % of {bench['roofline']['peak']} TFLOP/s for the "
