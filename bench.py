@@ -405,6 +405,63 @@ def cpu_baseline(cfg, samples, budget, qs, mem_len, mean_ctx):
                        f"and to the timed frames' mean context {mean_ctx:.0f}")}
 
 
+def unit_rates():
+    """Matrix-core and vector-ALU (exponential) rates and their overlap on this GPU: one
+    workgroup of eight waves per CU runs the probe of rvs_unit_rates; prints one JSON line
+    (--unit-rates-summary turns it into profiles/unit_rates__mi355x.md)."""
+    import ctypes
+    import torch
+    from paper_2609_23286_amd import rv
+    torch.cuda.set_device(0)
+    n_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    iters = 4000
+    s = rv._load_synth()
+    s.rvs_unit_rates.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
+    s.rvs_unit_rates.restype = ctypes.c_int
+    ns = (ctypes.c_float * 6)()
+    if s.rvs_unit_rates(n_cus, iters, ns):
+        raise SystemExit("rvs_unit_rates failed")
+    keys = ("mfma_wave", "valu_wave", "mfma_wave_and_valu_wave", "one_wave_both", "two_mfma_waves",
+            "two_mfma_waves_zero_operands")
+    print(json.dumps({"ns_per_iter": dict(zip(keys, (float(x) for x in ns))), "cus": n_cus, "iterations": iters}),
+          flush=True)
+
+
+def unit_rates_summary(json_path):
+    r = json.loads(open(json_path).read().strip().splitlines()[-1])
+    t = r["ns_per_iter"]
+    t_m, t_v, t_mv, t_b, t_mm, t_mz = (t[k] for k in ("mfma_wave", "valu_wave", "mfma_wave_and_valu_wave",
+                                                      "one_wave_both", "two_mfma_waves",
+                                                      "two_mfma_waves_zero_operands"))
+    hidden = (t_m + t_v - t_mv) / t_m
+    lines = ["# Unit rates on one MI355X: matrix core, vector-ALU exponentials, and their overlap", "",
+             "Command (on the MI355X, from the repository root):", "", "```",
+             "python bench.py --unit-rates > unit_rates.json",
+             "python bench.py --unit-rates-summary unit_rates.json", "```", "",
+             f"One workgroup of eight waves per CU ({r['cus']} CUs; wave w runs on SIMD w % 4), "
+             f"{r['iterations']} iterations of:",
+             "MFMA body = 4 independent `v_mfma_f32_32x32x16_bf16`; VALU body = 8 independent chains of",
+             "2 x (FMA, `v_exp_f32`, add) = 16 exponentials + 32 FMA/add.  Time per iteration:", "",
+             "| Waves per SIMD | ns per iteration |", "|---|---|",
+             f"| one MFMA wave | {t_m:.1f} |", f"| two MFMA waves | {t_mm:.1f} (two bodies) |",
+             f"| two MFMA waves, all-zero operands | {t_mz:.1f} (two bodies) |",
+             f"| one VALU wave | {t_v:.1f} |", f"| one MFMA wave + one VALU wave | {t_mv:.1f} |",
+             f"| one wave running both bodies | {t_b:.1f} |", "",
+             f"- one 32x32x16 bf16 MFMA per SIMD: {t_mm / 8:.1f} ns with two waves issuing = "
+             f"{t_mm / 8 * 2.4:.1f} cycles at 2.4 GHz (32 at the dense peak: the matrix core sustains "
+             f"{100 * 32 / (t_mm / 8 * 2.4):.0f} % of it under this load); {t_m / 4:.1f} ns with one wave; "
+             f"{t_mz / 8:.1f} ns = {t_mz / 8 * 2.4:.1f} cycles with all-zero operands "
+             f"({100 * 32 / (t_mz / 8 * 2.4):.0f} %; the operand values move the rate by "
+             f"{100 * (t_mm - t_mz) / t_mm:.0f} % only; the clock under a whole-chip matrix load is not measured here)",
+             f"- VALU iteration: {t_v:.1f} ns = {t_v * 2.4:.0f} cycles at 2.4 GHz for 16 exponentials and 32 "
+             "other instructions (16 x 16 + 32 x 4 = 384 with the exponential at a quarter of the VALU rate)",
+             f"- share of the MFMA time hidden under VALU work on the same SIMD: {100 * hidden:.0f} %"]
+    path = os.path.join(PROFILES, "unit_rates__mi355x.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(f"wrote {path}")
+
+
 def stratified(n_stream, n):
     """n frames of an n_stream-frame stream, one from the middle of each of n equal
     stretches: t_i = floor((i + 1/2) n_stream / n)."""
@@ -451,10 +508,19 @@ def main():
     p.add_argument("--mfma-summary", nargs=3, metavar=("PASS0_DIR", "PASS1_DIR", "BENCH_JSON"),
                    help="summarise the two rocprofv3 --pmc passes of MFMA_PASSES over this command into "
                         "profiles/ and exit")
+    p.add_argument("--unit-rates", action="store_true",
+                   help="measure the matrix-core and exponential rates and their overlap (one JSON line) and exit")
+    p.add_argument("--unit-rates-summary", metavar="JSON", help="write profiles/unit_rates__mi355x.md and exit")
     p.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
                    help="summarise a rocprofv3 --kernel-trace --stats run of this command into profiles/ "
                         "and exit")
     args = p.parse_args()
+    if args.unit_rates:
+        unit_rates()
+        return
+    if args.unit_rates_summary:
+        unit_rates_summary(args.unit_rates_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this path has no multi-GPU mode "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)

@@ -146,7 +146,80 @@ __global__ __launch_bounds__(256) void plant_kernel(uint64_t seed, uint32_t fram
   }
 }
 
+// ---- unit-rate probe (benchmark support, not part of the method) ----------------------
+// Waves of 512-thread workgroups (wave w runs on SIMD w % 4) repeat a fixed loop body:
+// MFMA body = 4 independent v_mfma_f32_32x32x16_bf16; VALU body = 8 independent chains of
+// 2 x (FMA, v_exp_f32, add), i.e. 16 exponentials and 32 other VALU instructions.
+// mode 0: waves 0-3 MFMA only; 1: waves 0-3 VALU only; 2: waves 0-3 MFMA and waves 4-7
+// VALU (one of each per SIMD); 3: waves 0-3 both bodies in one instruction stream; 4: all
+// eight waves MFMA only (two per SIMD); 5: as 4 with all-zero MFMA operands.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+template <int MODE>
+__global__ __launch_bounds__(512) void unit_rate_kernel(float* out, int iters) {
+  const int w = threadIdx.x >> 6;
+  const bool do_mfma = MODE == 1 ? false : MODE >= 4 ? true : w < 4;
+  const bool do_valu = MODE == 0 ? false : MODE == 2 ? w >= 4 : w < 4;
+  bf16x8_t a, b;
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(MODE == 5 ? 0.f : 0.001f * (threadIdx.x + i));
+    b[i] = (__bf16)(MODE == 5 ? 0.f : 0.002f * i);
+  }
+  f32x16_t c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  float x[8];
+  for (int i = 0; i < 8; ++i) x[i] = 0.01f * (threadIdx.x & 7) + i;
+  for (int it = 0; it < iters; ++it) {
+    if (do_mfma) {
+      c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
+      c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
+      c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+    }
+    if (do_valu) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = __builtin_amdgcn_exp2f(fmaf(x[i], 0.5f, -0.25f)) + 0.1f;
+    }
+  }
+  float s = 0.f;
+  for (int i = 0; i < 16; ++i) s += c0[i] + c1[i] + c2[i] + c3[i];
+  for (int i = 0; i < 8; ++i) s += x[i];
+  out[(int64_t)blockIdx.x * 512 + threadIdx.x] = s;
+}
+
 }  // namespace
+
+extern "C" int rvs_unit_rates(int n_workgroups, int iters, float* ns_per_iter) {
+  if (n_workgroups < 1 || n_workgroups > 65536 || iters < 1 || !ns_per_iter) return 1;
+  float* out = nullptr;
+  if (hipMalloc(&out, (size_t)n_workgroups * 512 * sizeof(float)) != hipSuccess) return 4;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = 0;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) rc = 4;
+  for (int m = 0; rc == 0 && m < 6; ++m) {
+    for (int rep = 0; rc == 0 && rep < 2; ++rep) {  // the first launch warms up
+      if (hipEventRecord(e0, nullptr) != hipSuccess) rc = 4;
+      if (m == 0) hipLaunchKernelGGL(unit_rate_kernel<0>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 1) hipLaunchKernelGGL(unit_rate_kernel<1>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 2) hipLaunchKernelGGL(unit_rate_kernel<2>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 3) hipLaunchKernelGGL(unit_rate_kernel<3>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 4) hipLaunchKernelGGL(unit_rate_kernel<4>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 5) hipLaunchKernelGGL(unit_rate_kernel<5>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (hipGetLastError() != hipSuccess || hipEventRecord(e1, nullptr) != hipSuccess ||
+          hipEventSynchronize(e1) != hipSuccess)
+        rc = 4;
+      float ms = 0.f;
+      if (rc == 0 && hipEventElapsedTime(&ms, e0, e1) != hipSuccess) rc = 4;
+      if (rc == 0) ns_per_iter[m] = ms * 1e6f / (float)iters;
+    }
+  }
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  (void)hipFree(out);
+  return rc;
+}
 
 extern "C" int rvs_normal_bf16(uint64_t seed, uint32_t frame, int layer, int tag, int64_t n, float sigma,
                                uint16_t* out, void* stream) {
