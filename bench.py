@@ -449,7 +449,8 @@ def unit_rates_summary(json_path):
              f"| one wave running both bodies | {t_b:.1f} |", "",
              f"- one 32x32x16 bf16 MFMA per SIMD: {t_mm / 8:.1f} ns with two waves issuing = "
              f"{t_mm / 8 * 2.4:.1f} cycles at 2.4 GHz (32 at the dense peak: the matrix core sustains "
-             f"{100 * 32 / (t_mm / 8 * 2.4):.0f} % of it under this load); {t_m / 4:.1f} ns with one wave; "
+             f"{100 * 32 / (t_mm / 8 * 2.4):.0f} % of it under this load); {t_m / 4:.1f} ns with one wave (its four "
+             f"independent accumulator chains leave the matrix core idle {100 * (1 - 32 / (t_m / 4 * 2.4)):.0f} % of the time); "
              f"{t_mz / 8:.1f} ns = {t_mz / 8 * 2.4:.1f} cycles with all-zero operands "
              f"({100 * 32 / (t_mz / 8 * 2.4):.0f} %; the operand values move the rate by "
              f"{100 * (t_mm - t_mz) / t_mm:.0f} % only; the clock under a whole-chip matrix load is not measured here)",

@@ -160,7 +160,7 @@ template <int MODE>
 __global__ __launch_bounds__(512) void unit_rate_kernel(float* out, int iters) {
   const int w = threadIdx.x >> 6;
   const bool do_mfma = MODE == 1 ? false : MODE >= 4 ? true : w < 4;
-  const bool do_valu = MODE == 0 ? false : MODE == 2 ? w >= 4 : w < 4;
+  const bool do_valu = (MODE == 0 || MODE >= 4) ? false : MODE == 2 ? w >= 4 : w < 4;
   bf16x8_t a, b;
   for (int i = 0; i < 8; ++i) {
     a[i] = (__bf16)(MODE == 5 ? 0.f : 0.001f * (threadIdx.x + i));
