@@ -447,15 +447,13 @@ def unit_rates_summary(json_path):
              f"| two MFMA waves, all-zero operands | {t_mz:.1f} (two bodies) |",
              f"| one VALU wave | {t_v:.1f} |", f"| one MFMA wave + one VALU wave | {t_mv:.1f} |",
              f"| one wave running both bodies | {t_b:.1f} |", "",
-             f"- one 32x32x16 bf16 MFMA per SIMD: {t_mm / 8:.1f} ns with two waves issuing = "
-             f"{t_mm / 8 * 2.4:.1f} cycles at 2.4 GHz (32 at the dense peak: the matrix core sustains "
-             f"{100 * 32 / (t_mm / 8 * 2.4):.0f} % of it under this load); {t_m / 4:.1f} ns with one wave (its four "
-             f"independent accumulator chains leave the matrix core idle {100 * (1 - 32 / (t_m / 4 * 2.4)):.0f} % of the time); "
-             f"{t_mz / 8:.1f} ns = {t_mz / 8 * 2.4:.1f} cycles with all-zero operands "
-             f"({100 * 32 / (t_mz / 8 * 2.4):.0f} %; the operand values move the rate by "
-             f"{100 * (t_mm - t_mz) / t_mm:.0f} % only; the clock under a whole-chip matrix load is not measured here)",
-             f"- VALU iteration: {t_v:.1f} ns = {t_v * 2.4:.0f} cycles at 2.4 GHz for 16 exponentials and 32 "
-             "other instructions (16 x 16 + 32 x 4 = 384 with the exponential at a quarter of the VALU rate)",
+             f"- two MFMA waves per SIMD: {t_mm / 8:.1f} ns per 32x32x16 bf16 MFMA; at its 32 cycles the SIMD "
+             f"runs at {32 / (t_mm / 8):.2f} GHz ({100 * 32 / (t_mm / 8) / 2.4:.0f} % of the 2.4 GHz of the dense "
+             f"peak); {t_mz / 8:.1f} ns with all-zero operands ({32 / (t_mz / 8):.2f} GHz at the same cycle count)",
+             f"- one VALU wave: {t_v:.1f} ns for 16 exponentials at 16 cycles and 32 FMA/add at 4 = 384 cycles, "
+             f"i.e. {384 / t_v:.2f} GHz with the exponential at a quarter of the VALU rate",
+             f"- one MFMA wave alone: {t_m / 4:.1f} ns per MFMA (one wave's loop leaves issue gaps that a second "
+             "wave fills)",
              f"- share of the MFMA time hidden under VALU work on the same SIMD: {100 * hidden:.0f} %"]
     path = os.path.join(PROFILES, "unit_rates__mi355x.md")
     with open(path, "w") as fh:

@@ -166,6 +166,9 @@ __global__ __launch_bounds__(512) void unit_rate_kernel(float* out, int iters) {
     a[i] = (__bf16)(MODE == 5 ? 0.f : 0.001f * (threadIdx.x + i));
     b[i] = (__bf16)(MODE == 5 ? 0.f : 0.002f * i);
   }
+  // Opaque to the compiler: otherwise it rebuilds the constant operand inside the loop,
+  // and each rewrite waits for the previous MFMAs to finish reading it.
+  asm volatile("" : "+v"(a), "+v"(b));
   f32x16_t c0 = {}, c1 = {}, c2 = {}, c3 = {};
   float x[8];
   for (int i = 0; i < 8; ++i) x[i] = 0.01f * (threadIdx.x & 7) + i;
