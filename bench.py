@@ -461,6 +461,130 @@ def unit_rates_summary(json_path):
     print(f"wrote {path}")
 
 
+def library_context(config_name):
+    """The attention layer step beside the vendor stack on the same inputs: rv_attend_frame
+    (outputs and LSE) against torch's fused scaled_dot_product_attention (flash, then
+    memory-efficient backend; never the unfused path) over the same [memory ; frame] keys,
+    at several memory lengths, plus a dense bf16 GEMM for the sustained matrix rate.  Prints
+    one JSON line (--library-context-summary writes the profile)."""
+    import torch
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    from paper_2609_23286_amd import rv, synth
+    cfg = synth.CONFIGS[config_name]
+    N, H, d = cfg.n_tokens, cfg.n_heads, cfg.head_dim
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    rv.init()
+    reps = 50
+    m_list = [0, 2000, 5000, 9990]
+    buf = torch.empty((1, 3, N, H, d), dtype=torch.int16, device=dev)
+    rv.gpu_frame_qkv(cfg, 1, buf, 0, 1)
+    Qf, Kf, Vf = buf[0, 0], buf[0, 1], buf[0, 2]
+    mk = torch.empty((H, max(m_list), d), dtype=torch.int16, device=dev)
+    mv = torch.empty_like(mk)
+    rv.gpu_normal(cfg.seed, synth.PREFILL_FRAME, 0, synth.TAG_MEMK, mk, cfg.sigma)
+    rv.gpu_normal(cfg.seed, synth.PREFILL_FRAME, 0, synth.TAG_MEMV, mv, cfg.sigma)
+    rv.reserve_workspace(N, H, max(m_list), 1)
+    out = torch.empty_like(Qf)
+    lse = torch.empty((H, N), dtype=torch.float32, device=dev)
+    q_b = Qf.view(torch.bfloat16).permute(1, 0, 2).unsqueeze(0).contiguous()
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    rows = []
+    for M in m_list:
+        mkM = mk[:, :M].contiguous()
+        mvM = mv[:, :M].contiguous()
+        ctx = M + N
+        flops = attention_flops(N, H, d, ctx)
+        row = {"mem_len": M, "context": ctx, "flops": flops}
+        rv.attend_frame(Qf, Kf, Vf, None, out, lse, memK=mkM, memV=mvM, mem_len=M, head_stride=M)
+        # raw C call with pre-marshalled arguments, so that the host stays ahead of the GPU
+        import ctypes
+        lib, vp = rv.lib(), ctypes.c_void_p
+        c_args = (vp(Qf.data_ptr()), vp(Kf.data_ptr()), vp(Vf.data_ptr()), N, vp(mkM.data_ptr() if M else 0),
+                  vp(mvM.data_ptr() if M else 0), M, M, H, d, None, vp(out.data_ptr()), vp(lse.data_ptr()), None,
+                  vp(torch.cuda.current_stream().cuda_stream))
+        if lib.rv_attend_frame(*c_args):
+            raise rv.RVError(1, lib.rv_last_error().decode())
+        row["rv_us"] = timed(lambda: lib.rv_attend_frame(*c_args))
+        k_b = torch.cat([mkM, Kf.permute(1, 0, 2)], dim=1).view(torch.bfloat16).unsqueeze(0).contiguous()
+        v_b = torch.cat([mvM, Vf.permute(1, 0, 2)], dim=1).view(torch.bfloat16).unsqueeze(0).contiguous()
+        ours = (out.view(torch.bfloat16).float().permute(1, 0, 2))
+        for name, backend in (("flash", SDPBackend.FLASH_ATTENTION), ("efficient", SDPBackend.EFFICIENT_ATTENTION)):
+            try:
+                with sdpa_kernel([backend]):
+                    o = F.scaled_dot_product_attention(q_b, k_b, v_b)
+                    torch.cuda.synchronize()
+                    row[f"{name}_us"] = timed(lambda: F.scaled_dot_product_attention(q_b, k_b, v_b))
+                row[f"{name}_max_abs_diff"] = float((o[0].float() - ours).abs().max())
+            except RuntimeError as exc:
+                row[f"{name}_us"] = None
+                row[f"{name}_error"] = str(exc).splitlines()[0][:160]
+        rows.append(row)
+        log(json.dumps(row))
+        del k_b, v_b, mkM, mvM
+    n = 8192
+    a = torch.randn((n, n), dtype=torch.bfloat16, device=dev)
+    b = torch.randn((n, n), dtype=torch.bfloat16, device=dev)
+    c = torch.empty((n, n), dtype=torch.bfloat16, device=dev)
+    gemm_us = timed(lambda: torch.matmul(a, b, out=c))
+    gemm = {"m": n, "n": n, "k": n, "us": gemm_us, "tflops": 2 * n ** 3 / gemm_us / 1e6}
+    print(json.dumps({"config": config_name, "tokens": N, "heads": H, "head_dim": d, "reps": reps,
+                      "rows": rows, "gemm_bf16": gemm, "torch": torch.__version__,
+                      "hip": getattr(torch.version, "hip", None)}), flush=True)
+
+
+def library_context_summary(json_path):
+    r = json.loads(open(json_path).read().strip().splitlines()[-1])
+    N, H, d = r["tokens"], r["heads"], r["head_dim"]
+    lines = [f"# Attention layer step ({N} queries x {H} heads x {d}, memory + frame keys) beside torch's fused "
+             "attention on one MI355X", "",
+             "Command (on the MI355X, from the repository root):", "", "```",
+             f"python bench.py --config {r['config']} --library-context > library_context.json",
+             "python bench.py --library-context-summary library_context.json", "```", "",
+             f"Same inputs for both (frame 1 of the {r['config']} stream, layer 0; memory rows from the prefill "
+             f"generator), mean of {r['reps']} back-to-back calls after one untimed call, HIP events on one "
+             f"stream.  `rv_attend_frame` also writes the per-query LSE; torch's call returns the output only "
+             f"(torch {r['torch']}, HIP {r['hip']}).  TFLOP/s counts 4 N H d (M + N) per call; the peak is "
+             f"{PEAK_BF16_TFLOPS} TFLOP/s.", "",
+             "| memory rows M | rv_attend_frame us | TFLOP/s (% peak) | torch flash us | torch mem-efficient us "
+             "| rv speed-up vs best torch | max abs diff of outputs |",
+             "|---|---|---|---|---|---|---|"]
+    for row in r["rows"]:
+        tf = row["flops"] / row["rv_us"] / 1e6
+        cand = [row.get("flash_us"), row.get("efficient_us")]
+        cand = [c for c in cand if c]
+        best = min(cand) if cand else None
+        fmt = lambda v: f"{v:.1f}" if v else "n/a"
+        diffs = [row.get(k) for k in ("flash_max_abs_diff", "efficient_max_abs_diff") if row.get(k) is not None]
+        lines.append(f"| {row['mem_len']} | {row['rv_us']:.1f} | {tf:.0f} ({100 * tf / PEAK_BF16_TFLOPS:.1f} %) | "
+                     f"{fmt(row.get('flash_us'))} | {fmt(row.get('efficient_us'))} | "
+                     f"{(best / row['rv_us']) if best else float('nan'):.2f}x | "
+                     f"{max(diffs) if diffs else float('nan'):.3g} |")
+    errs = sorted({row[k] for row in r["rows"] for k in ("flash_error", "efficient_error") if row.get(k)})
+    for e in errs:
+        lines.append(f"\nA torch backend was unavailable: {e}")
+    g = r["gemm_bf16"]
+    lines += ["", f"Dense bf16 GEMM through torch.matmul ({g['m']} x {g['n']} x {g['k']}): {g['us']:.0f} us = "
+              f"{g['tflops']:.0f} TFLOP/s = {100 * g['tflops'] / PEAK_BF16_TFLOPS:.1f} % of the dense peak "
+              "(the library's sustained matrix rate on this GPU)."]
+    path = os.path.join(PROFILES, f"attention_vs_torch_sdpa__{r['config']}_layer_step.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(f"wrote {path}")
+
+
 def stratified(n_stream, n):
     """n frames of an n_stream-frame stream, one from the middle of each of n equal
     stretches: t_i = floor((i + 1/2) n_stream / n)."""
@@ -510,6 +634,11 @@ def main():
     p.add_argument("--unit-rates", action="store_true",
                    help="measure the matrix-core and exponential rates and their overlap (one JSON line) and exit")
     p.add_argument("--unit-rates-summary", metavar="JSON", help="write profiles/unit_rates__mi355x.md and exit")
+    p.add_argument("--library-context", action="store_true",
+                   help="time the attention layer step beside torch's fused attention on the same inputs "
+                        "(one JSON line) and exit")
+    p.add_argument("--library-context-summary", metavar="JSON",
+                   help="write profiles/attention_vs_torch_sdpa__<config>_layer_step.md and exit")
     p.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
                    help="summarise a rocprofv3 --kernel-trace --stats run of this command into profiles/ "
                         "and exit")
@@ -519,6 +648,12 @@ def main():
         return
     if args.unit_rates_summary:
         unit_rates_summary(args.unit_rates_summary)
+        return
+    if args.library_context:
+        library_context(args.config)
+        return
+    if args.library_context_summary:
+        library_context_summary(args.library_context_summary)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this path has no multi-GPU mode "
