@@ -115,8 +115,11 @@ int64_t rv_mem_capacity(rv_mem m);
 rv_status rv_mem_view(rv_mem m, const void **memK, const void **memV,
                       int64_t *head_stride_tokens);
 
-/* Ensures capacity >= tokens (<= max_tokens).  Growth allocates new arenas, copies the
- * valid rows on `stream` and then synchronises `stream` before freeing the old ones. */
+/* Ensures capacity >= tokens (<= max_tokens).  Growth is stream-ordered on `stream` and
+ * does not synchronise: new arenas (hipMallocAsync), a copy of the valid rows, and the
+ * release of the old arenas (hipFreeAsync) are enqueued in that order, so work on
+ * another stream must wait for `stream` before it uses the grown memory.  Arenas at
+ * creation are ready for every stream. */
 rv_status rv_mem_reserve(rv_mem m, int64_t tokens, void *stream);
 
 /* Sets the length to 0 (arena contents are left as they are). */

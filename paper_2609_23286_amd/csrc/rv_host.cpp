@@ -161,18 +161,26 @@ struct rv_mem_s {
 
 namespace {
 
-rv_status arena_alloc(int n_heads, int64_t cap, uint16_t** K, uint16_t** V, int32_t** prov) {
+// Arenas are stream-ordered allocations (hipMallocAsync / hipFreeAsync on the stream of
+// the call that creates, grows or frees them), so that growth needs no host
+// synchronisation: the new arenas, the copy of the valid rows and the release of the old
+// ones all take their place in the stream's order.
+void arena_free(uint16_t* K, uint16_t* V, int32_t* prov, hipStream_t s) {
+  if (K) (void)hipFreeAsync(K, s);
+  if (V) (void)hipFreeAsync(V, s);
+  if (prov) (void)hipFreeAsync(prov, s);
+}
+
+rv_status arena_alloc(int n_heads, int64_t cap, uint16_t** K, uint16_t** V, int32_t** prov, hipStream_t s) {
   *K = *V = nullptr;
   *prov = nullptr;
   if (cap == 0) return RV_OK;
   const size_t rows = (size_t)n_heads * (size_t)cap;
-  hipError_t e = hipMalloc(K, rows * rv::kHeadDim * 2);
-  if (e == hipSuccess) e = hipMalloc(V, rows * rv::kHeadDim * 2);
-  if (e == hipSuccess) e = hipMalloc(prov, rows * 2 * sizeof(int32_t));
+  hipError_t e = hipMallocAsync(reinterpret_cast<void**>(K), rows * rv::kHeadDim * 2, s);
+  if (e == hipSuccess) e = hipMallocAsync(reinterpret_cast<void**>(V), rows * rv::kHeadDim * 2, s);
+  if (e == hipSuccess) e = hipMallocAsync(reinterpret_cast<void**>(prov), rows * 2 * sizeof(int32_t), s);
   if (e != hipSuccess) {
-    if (*K) (void)hipFree(*K);
-    if (*V) (void)hipFree(*V);
-    if (*prov) (void)hipFree(*prov);
+    arena_free(*K, *V, *prov, s);
     *K = *V = nullptr;
     *prov = nullptr;
     return hip_fail(e, "memory arena allocation");
@@ -180,7 +188,9 @@ rv_status arena_alloc(int n_heads, int64_t cap, uint16_t** K, uint16_t** V, int3
   return RV_OK;
 }
 
-// Grows m to hold at least `tokens` rows per head; strong guarantee on failure.
+// Grows m to hold at least `tokens` rows per head; strong guarantee on failure (every
+// step that can fail does so when it is enqueued, before m changes).  Stream-ordered on
+// s: the old arenas are released on s after the copy that reads them.
 rv_status arena_reserve(rv_mem m, int64_t tokens, hipStream_t s) {
   if (tokens <= m->cap) return RV_OK;
   if (tokens > m->max_tokens)
@@ -189,7 +199,7 @@ rv_status arena_reserve(rv_mem m, int64_t tokens, hipStream_t s) {
   int64_t cap = std::max<int64_t>(tokens, std::min<int64_t>(m->max_tokens, std::max<int64_t>(256, m->cap * 2)));
   uint16_t *K, *V;
   int32_t* prov;
-  rv_status st = arena_alloc(m->n_heads, cap, &K, &V, &prov);
+  rv_status st = arena_alloc(m->n_heads, cap, &K, &V, &prov, s);
   if (st != RV_OK) return st;
   hipError_t e = hipSuccess;
   if (m->len > 0) {
@@ -203,16 +213,11 @@ rv_status arena_reserve(rv_mem m, int64_t tokens, hipStream_t s) {
       e = hipMemcpy2DAsync(prov, cap * 8, m->prov, m->cap * 8, m->len * 8, m->n_heads,
                            hipMemcpyDeviceToDevice, s);
   }
-  if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) {
-    (void)hipFree(K);
-    (void)hipFree(V);
-    (void)hipFree(prov);
+    arena_free(K, V, prov, s);
     return hip_fail(e, "memory growth copy");
   }
-  if (m->K) (void)hipFree(m->K);
-  if (m->V) (void)hipFree(m->V);
-  if (m->prov) (void)hipFree(m->prov);
+  arena_free(m->K, m->V, m->prov, s);
   m->K = K;
   m->V = V;
   m->prov = prov;
@@ -259,7 +264,14 @@ rv_status rv_mem_create(int n_heads, int head_dim, int64_t reserve_tokens, int64
   }
   m->n_heads = n_heads;
   m->max_tokens = max_tokens;
-  rv_status st = arena_alloc(n_heads, reserve_tokens, &m->K, &m->V, &m->prov);
+  rv_status st = arena_alloc(n_heads, reserve_tokens, &m->K, &m->V, &m->prov, nullptr);
+  if (st == RV_OK) {  // ready for every stream
+    e = hipStreamSynchronize(nullptr);
+    if (e != hipSuccess) {
+      arena_free(m->K, m->V, m->prov, nullptr);
+      st = hip_fail(e, "memory arena allocation");
+    }
+  }
   if (st != RV_OK) {
     delete m;
     return st;
@@ -275,9 +287,8 @@ rv_status rv_mem_destroy(rv_mem m) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(m->device);
   (void)hipDeviceSynchronize();
-  if (m->K) (void)hipFree(m->K);
-  if (m->V) (void)hipFree(m->V);
-  if (m->prov) (void)hipFree(m->prov);
+  arena_free(m->K, m->V, m->prov, nullptr);
+  (void)hipStreamSynchronize(nullptr);
   (void)hipSetDevice(prev);
   delete m;
   return RV_OK;

@@ -43,11 +43,13 @@ def gpu_frame_step(rv, mem, Q, K, V, qs, budget, frame_id):
             sal.cpu().numpy().astype(np.float64), idx.cpu().numpy())
 
 
-def run_free_stream(rv, cfg, n_frames, anchor=False, row_sample=None):
+def run_free_stream(rv, cfg, n_frames, anchor=False, row_sample=None, reserve=None):
     """Free-running stream: the GPU and the oracle each keep their own memory.  With
     row_sample, the oracle computes only the sampled queries (all of them, for the
     saliency) and the given output rows -- the rest of the attention is not needed for
-    the admission -- and outputs are compared on those rows."""
+    the admission -- and outputs are compared on those rows.  reserve: rows the GPU
+    memory starts with (default: the whole stream's), so that smaller values make it
+    grow inside the admissions."""
     import torch
     H, N, k = cfg.n_heads, cfg.n_tokens, cfg.budget
     qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
@@ -57,7 +59,7 @@ def run_free_stream(rv, cfg, n_frames, anchor=False, row_sample=None):
         rows = np.unique(np.concatenate([qidx, np.asarray(row_sample, dtype=np.int32)])).astype(np.int32)
         pos = np.searchsorted(rows, qidx)
     cap = (N if anchor else 0) + n_frames * k + 8
-    mem = rv.Memory(H, reserve_tokens=cap, max_tokens=cap)
+    mem = rv.Memory(H, reserve_tokens=cap if reserve is None else reserve, max_tokens=cap)
     omem = oracle.Memory(H, cfg.head_dim, cap)
     resyncs = 0
     for t in range(n_frames):
@@ -114,6 +116,22 @@ def test_vitl_layer_stream_free_running(rv):
     sample = np.array([0, 1, 4, 5, 31, 32, 63, 64, 127, 128, 129, 511, 512, N - 2, N - 1], dtype=np.int32)
     sample = np.concatenate([sample, np.arange(3, N, 53, dtype=np.int32)])
     assert run_free_stream(rv, cfg, cfg.n_frames, row_sample=sample) == 0
+
+
+def test_memory_grows_in_stream_order_on_a_side_stream(rv):
+    """The first 60 frames of the single-layer ViT-L stream from a memory created empty,
+    every call on a non-default stream: the arenas grow inside the admissions (0 -> 256
+    -> 512 -> 608 rows, allocation, copy and release all stream-ordered, no host
+    synchronisation) and every frame still matches the oracle's own stream, memory bytes
+    included."""
+    import torch
+    cfg = synth.CONFIGS["vitl_layer"]
+    N = cfg.n_tokens
+    sample = np.array([0, 1, 63, 64, 511, 512, N - 1], dtype=np.int32)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        assert run_free_stream(rv, cfg, 60, row_sample=sample, reserve=0) == 0
+    side.synchronize()
 
 
 def test_stream_continues_bit_identically_after_restore(rv, tmp_path):
