@@ -220,7 +220,9 @@ def summarize_pmc(fetch_dir, write_dir, workload):
 MFMA_PASSES = (("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_COEXEC_CYCLES",
                 "SQ_INSTS_MFMA", "GRBM_GUI_ACTIVE"),
                ("SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_BUSY_CYCLES",
-                "GRBM_GUI_ACTIVE"))
+                "GRBM_GUI_ACTIVE"),
+               ("SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY", "SQ_LDS_IDX_ACTIVE",
+                "SQ_LDS_BANK_CONFLICT", "GRBM_GUI_ACTIVE"))
 MI355X_XCDS, MI355X_SIMDS = 8, 1024    # 8 XCDs x 32 CUs x 4 SIMDs
 
 
@@ -228,10 +230,10 @@ def mfma_path(workload):
     return os.path.join(PROFILES, f"attn_fwd_kernel__{workload}__mfma.md")
 
 
-def summarize_mfma(dir_a, dir_b, bench_json, workload):
-    """Reduce two rocprofv3 --pmc runs of this benchmark (the counters of MFMA_PASSES) into
-    per-dispatch matrix-core and vector-ALU activity of each kernel, and tie the attention
-    kernel's to the benchmark line of the same command (bench_json)."""
+def summarize_mfma(dir_a, dir_b, dir_c, bench_json, workload):
+    """Reduce three rocprofv3 --pmc runs of this benchmark (the counters of MFMA_PASSES) into
+    per-dispatch matrix-core, vector-ALU and wave-state activity of each kernel, and tie the
+    attention kernel's to the benchmark line of the same command (bench_json)."""
     import csv
 
     def per_kernel(d):
@@ -245,16 +247,17 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
                         float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
         return out
 
-    a, b = per_kernel(dir_a), per_kernel(dir_b)
+    a, b, w = per_kernel(dir_a), per_kernel(dir_b), per_kernel(dir_c)
     bench = json.loads(open(bench_json).read().strip().splitlines()[-1])
     mean = lambda v: sum(v) / len(v)
     lines = [f"# Matrix-core and vector-ALU activity per dispatch, {workload}", "",
-             "Two counter passes over the benchmark command (one run each, the program after `--`):", "",
+             "Three counter passes over the benchmark command (one run each, the program after `--`):", "",
              "```", "cd /tmp && export TMPDIR=/tmp"]
     for i, cs in enumerate(MFMA_PASSES):
         lines.append(f"timeout -s KILL 600 rocprofv3 --pmc {' '.join(cs)} --output-format csv -d <out>/m{i} "
                      f"-o m{i} -- python /root/repo/bench.py {bench_args()} --no-cpu-baseline")
-    lines += [f"python /root/repo/bench.py {bench_args()} --mfma-summary <out>/m0 <out>/m1 <kernel-trace run's json>",
+    lines += [f"python /root/repo/bench.py {bench_args()} --mfma-summary <out>/m0 <out>/m1 <out>/m2 "
+              "<kernel-trace run's json>",
               "```",
               "", "Counters are summed over the chip (GRBM_GUI_ACTIVE over its 8 XCDs).  Per dispatch:",
               "`busy` = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024 SIMDs), the fraction of SIMD",
@@ -264,15 +267,19 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
               "durations are a little longer than in the kernel trace); `coexec` = SQ_VALU_MFMA_COEXEC_CYCLES /",
               "SQ_VALU_MFMA_BUSY_CYCLES, the share of those cycles in which a vector instruction was also",
               "issued; `valu` = 4 x SQ_ACTIVE_INST_VALU / (GRBM_GUI_ACTIVE / 8 x 1024), vector-ALU cycles per",
-              "SIMD cycle (quad-cycle units); `bf16 flops` = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16.", "",
+              "SIMD cycle (quad-cycle units); `bf16 flops` = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16.  Wave states",
+              "(shares of SQ_WAVE_CYCLES, the cycles waves are resident): `issuing` = SQ_ACTIVE_INST_ANY,",
+              "`waiting` = SQ_WAIT_ANY (on a counter -- memory, LDS -- or a barrier), `ready` = SQ_WAIT_INST_ANY",
+              "(an instruction ready but not issued); `lds conflict` = SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE.",
+              "",
               "| Kernel | dispatches | duration us | GUI cycles / XCD | busy | busy@2.4 | coexec | valu | MFMA instrs | "
-              "bf16 flops | VALU instrs | exp/log (f32 trans) instrs |",
-              "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+              "bf16 flops | VALU instrs | exp/log (f32 trans) instrs | issuing | waiting | ready | lds conflict |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
     rows = {}
     for name in sorted(set(a) | set(b)):
         if name not in KERNEL_SOURCES:
             continue
-        ca, cb = a.get(name, {}), b.get(name, {})
+        ca, cb, cw = a.get(name, {}), b.get(name, {}), w.get(name, {})
         try:
             gui = mean(ca["GRBM_GUI_ACTIVE"]) / MI355X_XCDS
             busy = mean(ca["SQ_VALU_MFMA_BUSY_CYCLES"])
@@ -284,13 +291,18 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
                  "valu": 4.0 * mean(cb["SQ_ACTIVE_INST_VALU"]) / (mean(cb["GRBM_GUI_ACTIVE"]) / MI355X_XCDS
                                                                  * MI355X_SIMDS),
                  "vinst": mean(cb["SQ_INSTS_VALU"]), "trans": mean(cb["SQ_INSTS_VALU_TRANS_F32"])}
+            wc = max(mean(cw["SQ_WAVE_CYCLES"]), 1.0)
+            r.update({"issuing": mean(cw["SQ_ACTIVE_INST_ANY"]) / wc, "waiting": mean(cw["SQ_WAIT_ANY"]) / wc,
+                      "ready": mean(cw["SQ_WAIT_INST_ANY"]) / wc,
+                      "ldsconf": mean(cw["SQ_LDS_BANK_CONFLICT"]) / max(mean(cw["SQ_LDS_IDX_ACTIVE"]), 1.0)})
         except KeyError as e:
             raise SystemExit(f"{name}: counter {e} missing from the CSVs")
         rows[name] = r
         lines.append(f"| `{name}` | {r['n']} | {r['dur'] / 1e3:.1f} | {r['gui']:.0f} | {100 * r['busy']:.1f} % | "
                      f"{100 * r['busy24']:.1f} % | {100 * r['coexec']:.1f} % | "
                      f"{100 * r['valu']:.1f} % | {r['mfma']:.0f} | {r['flops']:.3e} | {r['vinst']:.0f} | "
-                     f"{r['trans']:.0f} |")
+                     f"{r['trans']:.0f} | {100 * r['issuing']:.0f} % | {100 * r['waiting']:.0f} % | "
+                     f"{100 * r['ready']:.0f} % | {100 * r['ldsconf']:.0f} % |")
     f = rows.get("attn_fwd_kernel")
     if f:
         alg = bench["roofline"]["algorithmic_flops_per_launch"]
@@ -302,6 +314,9 @@ def summarize_mfma(dir_a, dir_b, bench_json, workload):
                   f"- executed MFMA work {100 * f['busy24']:.1f} % of the dense peak over the dispatch's own "
                   f"duration; matrix core busy {100 * f['busy']:.1f} % of SIMD cycles; a vector instruction issued in "
                   f"{100 * f['coexec']:.1f} % of those; vector ALU active {100 * f['valu']:.1f} % of SIMD cycles",
+                  f"- waves issue in {100 * f['issuing']:.0f} % of their resident cycles, wait on a counter or barrier "
+                  f"in {100 * f['waiting']:.0f} % and hold a ready instruction that is not issued in "
+                  f"{100 * f['ready']:.0f} %",
                   f"- benchmark line: {bench['roofline']['achieved']:.1f} TFLOP/s = "
                   f"{100 * bench['roofline']['frac']:.1f} % of {bench['roofline']['peak']} TFLOP/s for the "
                   f"attention step (forward + merge launches, {bench['roofline']['avg_launch_us']:.1f} us per "
@@ -418,11 +433,11 @@ def unit_rates():
     s = rv._load_synth()
     s.rvs_unit_rates.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
     s.rvs_unit_rates.restype = ctypes.c_int
-    ns = (ctypes.c_float * 6)()
+    ns = (ctypes.c_float * 7)()
     if s.rvs_unit_rates(n_cus, iters, ns):
         raise SystemExit("rvs_unit_rates failed")
     keys = ("mfma_wave", "valu_wave", "mfma_wave_and_valu_wave", "one_wave_both", "two_mfma_waves",
-            "two_mfma_waves_zero_operands")
+            "two_mfma_waves_zero_operands", "two_valu_waves")
     print(json.dumps({"ns_per_iter": dict(zip(keys, (float(x) for x in ns))), "cus": n_cus, "iterations": iters}),
           flush=True)
 
@@ -430,10 +445,12 @@ def unit_rates():
 def unit_rates_summary(json_path):
     r = json.loads(open(json_path).read().strip().splitlines()[-1])
     t = r["ns_per_iter"]
-    t_m, t_v, t_mv, t_b, t_mm, t_mz = (t[k] for k in ("mfma_wave", "valu_wave", "mfma_wave_and_valu_wave",
-                                                      "one_wave_both", "two_mfma_waves",
-                                                      "two_mfma_waves_zero_operands"))
+    t_m, t_v, t_mv, t_b, t_mm, t_mz, t_vv = (t[k] for k in (
+        "mfma_wave", "valu_wave", "mfma_wave_and_valu_wave", "one_wave_both", "two_mfma_waves",
+        "two_mfma_waves_zero_operands", "two_valu_waves"))
     hidden = (t_m + t_v - t_mv) / t_m
+    clk_mfma = 32 / (t_mm / 8)        # GHz if an MFMA takes its 32 cycles
+    clk_valu = 2 * (16 * 8 + 32 * 4) / t_vv   # GHz if an exponential takes 8 cycles, the rest 4
     lines = ["# Unit rates on one MI355X: matrix core, vector-ALU exponentials, and their overlap", "",
              "Command (on the MI355X, from the repository root):", "", "```",
              "python bench.py --unit-rates > unit_rates.json",
@@ -445,17 +462,78 @@ def unit_rates_summary(json_path):
              "| Waves per SIMD | ns per iteration |", "|---|---|",
              f"| one MFMA wave | {t_m:.1f} |", f"| two MFMA waves | {t_mm:.1f} (two bodies) |",
              f"| two MFMA waves, all-zero operands | {t_mz:.1f} (two bodies) |",
-             f"| one VALU wave | {t_v:.1f} |", f"| one MFMA wave + one VALU wave | {t_mv:.1f} |",
+             f"| one VALU wave | {t_v:.1f} |", f"| two VALU waves | {t_vv:.1f} (two bodies) |",
+             f"| one MFMA wave + one VALU wave | {t_mv:.1f} |",
              f"| one wave running both bodies | {t_b:.1f} |", "",
              f"- two MFMA waves per SIMD: {t_mm / 8:.1f} ns per 32x32x16 bf16 MFMA; at its 32 cycles the SIMD "
-             f"runs at {32 / (t_mm / 8):.2f} GHz ({100 * 32 / (t_mm / 8) / 2.4:.0f} % of the 2.4 GHz of the dense "
-             f"peak); {t_mz / 8:.1f} ns with all-zero operands ({32 / (t_mz / 8):.2f} GHz at the same cycle count)",
-             f"- one VALU wave: {t_v:.1f} ns for 16 exponentials at 16 cycles and 32 FMA/add at 4 = 384 cycles, "
-             f"i.e. {384 / t_v:.2f} GHz with the exponential at a quarter of the VALU rate",
+             f"runs at {clk_mfma:.2f} GHz ({100 * clk_mfma / 2.4:.0f} % of the 2.4 GHz of the dense peak); "
+             f"{t_mz / 8:.1f} ns with all-zero operands ({32 / (t_mz / 8):.2f} GHz at the same cycle count)",
+             f"- two VALU waves per SIMD: {t_vv:.1f} ns for two bodies; with the exponential at 8 cycles per "
+             f"wave (half the rate of an FMA or add, 4) that is 512 cycles at {clk_valu:.2f} GHz (at 16 cycles "
+             f"per exponential it would need {clk_valu * (16 * 16 + 32 * 4) / (16 * 8 + 32 * 4):.2f} GHz, above "
+             "the chip's 2.4)",
+             f"- one VALU wave alone: {t_v:.1f} ns per body, {t_v / (t_vv / 2):.2f}x the two-wave time per body: one "
+             "wave's exponential-to-add dependencies leave the vector ALU idle part of the time",
              f"- one MFMA wave alone: {t_m / 4:.1f} ns per MFMA (one wave's loop leaves issue gaps that a second "
              "wave fills)",
-             f"- share of the MFMA time hidden under VALU work on the same SIMD: {100 * hidden:.0f} %"]
+             f"- share of the MFMA time hidden under VALU work on the same SIMD (one wave of each): "
+             f"{100 * hidden:.0f} %"]
     path = os.path.join(PROFILES, "unit_rates__mi355x.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(f"wrote {path}")
+
+
+UNIT_RATE_COUNTERS = ("SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_VALU_MFMA_BUSY_CYCLES",
+                      "GRBM_GUI_ACTIVE")
+UNIT_RATE_MODES = ("one MFMA wave", "one VALU wave", "one MFMA wave + one VALU wave", "one wave running both bodies",
+                   "two MFMA waves", "two MFMA waves, all-zero operands", "two VALU waves")
+
+
+def unit_rates_counters(counter_dir, iters=4000):
+    """Write profiles/unit_rates__mi355x__counters.md from a rocprofv3 --pmc run (the
+    counters of UNIT_RATE_COUNTERS) of `bench.py --unit-rates`: per probe mode, the clock
+    the chip ran at and how busy the vector ALU and the matrix core were."""
+    import csv
+    import re
+    acc = {}
+    for f in glob.glob(os.path.join(counter_dir, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            m = re.search(r"unit_rate_kernel<(\d+)>", r["Kernel_Name"])
+            if not m:
+                continue
+            d = acc.setdefault((int(m.group(1)), r["Dispatch_Id"]), {})
+            d[r["Counter_Name"]] = float(r["Counter_Value"])
+            d["ns"] = float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    if not acc:
+        raise SystemExit(f"no unit_rate_kernel dispatches under {counter_dir}")
+    lines = ["# Unit-rate probe under counters: clock, vector-ALU and matrix-core activity per mode", "",
+             "Command (on the MI355X, from the repository root; the program after `--`):", "", "```",
+             "cd /tmp && export TMPDIR=/tmp",
+             f"timeout -s KILL 120 rocprofv3 --pmc {' '.join(UNIT_RATE_COUNTERS)} --output-format csv "
+             "-d <out>/ur -o ur -- python /root/repo/bench.py --unit-rates",
+             "python /root/repo/bench.py --unit-rates-counters <out>/ur", "```", "",
+             "Each mode launches twice with the same iteration count (a warm-up, then the timed launch); the",
+             "rows average both.  `clock` = GRBM_GUI_ACTIVE / 8 XCDs / the dispatch's duration; `valu busy` =",
+             "4 x SQ_ACTIVE_INST_VALU / (GUI cycles per XCD x 1024 SIMDs), counted over all SIMDs whether or",
+             "not the mode gives them VALU work; `mfma busy` = SQ_VALU_MFMA_BUSY_CYCLES over the same SIMD",
+             f"cycles; instructions are per VALU-issuing wave and iteration ({iters} iterations).", "",
+             "| Mode | ns per iteration | clock GHz | valu busy | mfma busy | VALU instrs / wave / iter | "
+             "of them exp |", "|---|---|---|---|---|---|---|"]
+    valu_waves = {0: 4, 1: 4, 2: 8, 3: 4, 4: 8, 5: 8, 6: 8}  # waves per workgroup issuing VALU (MFMA counts)
+    for mode in sorted({k[0] for k in acc}):
+        ds = [d for (m, _), d in acc.items() if m == mode]
+        mean = lambda key: sum(d[key] for d in ds) / len(ds)
+        ns = mean("ns")
+        gui = mean("GRBM_GUI_ACTIVE") / MI355X_XCDS
+        simd = gui * MI355X_SIMDS
+        n_waves = 256 * valu_waves[mode]
+        lines.append(f"| {UNIT_RATE_MODES[mode] if mode < len(UNIT_RATE_MODES) else mode} | "
+                     f"{ns / iters:.1f} | {gui / ns:.2f} | {100 * 4 * mean('SQ_ACTIVE_INST_VALU') / simd:.1f} % | "
+                     f"{100 * mean('SQ_VALU_MFMA_BUSY_CYCLES') / simd:.1f} % | "
+                     f"{mean('SQ_INSTS_VALU') / n_waves / iters:.1f} | "
+                     f"{mean('SQ_INSTS_VALU_TRANS_F32') / n_waves / iters:.1f} |")
+    path = os.path.join(PROFILES, "unit_rates__mi355x__counters.md")
     with open(path, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print(f"wrote {path}")
@@ -628,12 +706,15 @@ def main():
                    help="run a 256 MiB device copy before the stream (HBM counter calibration)")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="summarise two rocprofv3 --pmc runs of this command into profiles/ and exit")
-    p.add_argument("--mfma-summary", nargs=3, metavar=("PASS0_DIR", "PASS1_DIR", "BENCH_JSON"),
-                   help="summarise the two rocprofv3 --pmc passes of MFMA_PASSES over this command into "
+    p.add_argument("--mfma-summary", nargs=4, metavar=("PASS0_DIR", "PASS1_DIR", "PASS2_DIR", "BENCH_JSON"),
+                   help="summarise the three rocprofv3 --pmc passes of MFMA_PASSES over this command into "
                         "profiles/ and exit")
     p.add_argument("--unit-rates", action="store_true",
                    help="measure the matrix-core and exponential rates and their overlap (one JSON line) and exit")
     p.add_argument("--unit-rates-summary", metavar="JSON", help="write profiles/unit_rates__mi355x.md and exit")
+    p.add_argument("--unit-rates-counters", metavar="DIR",
+                   help="write profiles/unit_rates__mi355x__counters.md from a rocprofv3 --pmc run of --unit-rates "
+                        "and exit")
     p.add_argument("--library-context", action="store_true",
                    help="time the attention layer step beside torch's fused attention on the same inputs "
                         "(one JSON line) and exit")
@@ -648,6 +729,9 @@ def main():
         return
     if args.unit_rates_summary:
         unit_rates_summary(args.unit_rates_summary)
+        return
+    if args.unit_rates_counters:
+        unit_rates_counters(args.unit_rates_counters)
         return
     if args.library_context:
         library_context(args.config)

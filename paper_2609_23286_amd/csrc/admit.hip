@@ -12,8 +12,8 @@
 // registers) and sweeps the sampled queries in blocks of 32 with
 // v_mfma_f32_32x32x16_bf16 (Z = Q~ K^T, each lane owning one key column).  The
 // exponentials are summed in fp32 in a fixed order -- in-lane, over query blocks, then
-// across the two lane halves -- so S is bit-reproducible with no atomics.  The work is
-// VALU-bound: one FMA, one exp and one add per (query, key).
+// across the two lane halves -- so S is bit-reproducible with no atomics.  The vector-ALU
+// work is one FMA, one exp and one add per (query, key).
 //
 // select_kernel (Sec. 3.3 Eq. 6, head-specific retention): one workgroup per
 // (layer, head) takes the `budget` largest S_j, equal values ordered by lower index.

@@ -152,15 +152,16 @@ __global__ __launch_bounds__(256) void plant_kernel(uint64_t seed, uint32_t fram
 // 2 x (FMA, v_exp_f32, add), i.e. 16 exponentials and 32 other VALU instructions.
 // mode 0: waves 0-3 MFMA only; 1: waves 0-3 VALU only; 2: waves 0-3 MFMA and waves 4-7
 // VALU (one of each per SIMD); 3: waves 0-3 both bodies in one instruction stream; 4: all
-// eight waves MFMA only (two per SIMD); 5: as 4 with all-zero MFMA operands.
+// eight waves MFMA only (two per SIMD); 5: as 4 with all-zero MFMA operands; 6: all eight
+// waves VALU only (two per SIMD).
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 template <int MODE>
 __global__ __launch_bounds__(512) void unit_rate_kernel(float* out, int iters) {
   const int w = threadIdx.x >> 6;
-  const bool do_mfma = MODE == 1 ? false : MODE >= 4 ? true : w < 4;
-  const bool do_valu = (MODE == 0 || MODE >= 4) ? false : MODE == 2 ? w >= 4 : w < 4;
+  const bool do_mfma = (MODE == 1 || MODE == 6) ? false : (MODE == 4 || MODE == 5) ? true : w < 4;
+  const bool do_valu = MODE == 6 ? true : (MODE == 0 || MODE >= 4) ? false : MODE == 2 ? w >= 4 : w < 4;
   bf16x8_t a, b;
   for (int i = 0; i < 8; ++i) {
     a[i] = (__bf16)(MODE == 5 ? 0.f : 0.001f * (threadIdx.x + i));
@@ -201,7 +202,7 @@ extern "C" int rvs_unit_rates(int n_workgroups, int iters, float* ns_per_iter) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
   int rc = 0;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) rc = 4;
-  for (int m = 0; rc == 0 && m < 6; ++m) {
+  for (int m = 0; rc == 0 && m < 7; ++m) {
     for (int rep = 0; rc == 0 && rep < 2; ++rep) {  // the first launch warms up
       if (hipEventRecord(e0, nullptr) != hipSuccess) rc = 4;
       if (m == 0) hipLaunchKernelGGL(unit_rate_kernel<0>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
@@ -210,6 +211,7 @@ extern "C" int rvs_unit_rates(int n_workgroups, int iters, float* ns_per_iter) {
       if (m == 3) hipLaunchKernelGGL(unit_rate_kernel<3>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
       if (m == 4) hipLaunchKernelGGL(unit_rate_kernel<4>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
       if (m == 5) hipLaunchKernelGGL(unit_rate_kernel<5>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 6) hipLaunchKernelGGL(unit_rate_kernel<6>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
       if (hipGetLastError() != hipSuccess || hipEventRecord(e1, nullptr) != hipSuccess ||
           hipEventSynchronize(e1) != hipSuccess)
         rc = 4;
