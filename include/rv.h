@@ -325,10 +325,12 @@ rv_status rv_device_status(void);
  * and the RV_ATTN_* overrides apply here as there.  Query tiles of 128 and key tiles of
  * 64 make n_units = n_heads * q_tiles units of T key tiles each; queue q owns units
  * unit_base[q] .. unit_base[q+1]-1, laid out as iterations i = u * U + t (t < U; tiles
- * t >= T are padding).  Chunk c (0 <= c < n_chunks[q]) of queue q covers iterations
- * [start(c), min(start(c+1), units_q * U)) with start(c) = c * E for c < n_first and
- * n_first * E + (c - n_first) * E1 after; chunk_base[q] numbers the chunks of all
- * queues consecutively, and grid = n_queues * max(n_chunks) workgroups are launched.
+ * t >= T are padding).  Chunk lengths E (the first n_first chunks of a queue) and E1
+ * (the others) are in 1/256 iterations: chunk c (0 <= c < n_chunks[q]) of queue q covers
+ * iterations [cut(c), min(cut(c+1), units_q * U)) with cut(c) = floor(c E / 256) for
+ * c < n_first and floor((n_first E + (c - n_first) E1) / 256) after; chunk_base[q]
+ * numbers the chunks of all queues consecutively, and grid = n_queues * max(n_chunks)
+ * workgroups are launched.
  * RV_ERR_INVALID for out-of-range sizes or a NULL `out`. */
 typedef struct rv_attn_plan {
     int n_units, q_tiles, T, U, E, E1, n_first, n_queues, grid, total_chunks;

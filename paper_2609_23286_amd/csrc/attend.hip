@@ -286,15 +286,8 @@ constexpr int kSlotStatsFloat = BQ * D / 2;
 constexpr int kMergeRows = 32;   // output rows per merge workgroup (8 threads per row)
 constexpr int kMergeMax = 8;     // partials whose loads are in flight together
 
-// First iteration of chunk c of a queue: chunks 0 .. n_first-1 hold E tiles, the later
-// ones E1; and the chunk holding iteration `it`.
-__device__ __forceinline__ int64_t chunk_start(const AttnArgs& a, int c) {
-  return c < a.n_first ? (int64_t)c * a.E : (int64_t)a.n_first * a.E + (int64_t)(c - a.n_first) * a.E1;
-}
-__device__ __forceinline__ int chunk_of(const AttnArgs& a, int64_t it) {
-  const int64_t first = (int64_t)a.n_first * a.E;
-  return it < first ? (int)(it / a.E) : a.n_first + (int)((it - first) / a.E1);
-}
+// First iteration of chunk c of a queue (chunk arithmetic: rv_plan.h).
+__device__ __forceinline__ int64_t chunk_start(const AttnArgs& a, int c) { return chunk_cut(a, c); }
 
 // Partial slot of chunk c's segment of unit ui: slot 0 if the chunk starts inside the
 // unit, slot 1 if it began in an earlier unit.
@@ -477,9 +470,9 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
 // Requests a field from every 64-byte line of the argument block at once: the reads that
 // follow (some of them through indices that other arguments give) then hit the scalar
 // cache, instead of each line's first read costing a round trip of its own.
-// (The scalars before the tables lie in the lines of Q and lse; each table spans at most
-// two lines, holding its first and last entries.)
-static_assert(offsetof(AttnArgs, lse) >= 64 && offsetof(AttnArgs, unit_base) <= 2 * 64 &&
+// (The scalars before the tables lie in the lines of Q, lse and unit_base[0]; each table
+// spans at most two lines, holding its first and last entries.)
+static_assert(offsetof(AttnArgs, lse) / 64 == 1 && offsetof(AttnArgs, unit_base) / 64 == 2 &&
                   offsetof(AttnArgs, chunk_base) + 4 * kMaxQueues + 8 > sizeof(AttnArgs) && kMaxQueues <= 16,
               "touch_args names a field in every line of the argument block");
 __device__ __forceinline__ void touch_args(const AttnArgs& a) {
@@ -497,9 +490,10 @@ __global__ __launch_bounds__(kAttnThreads, kAttnWgPerCu) void attn_fwd_kernel(At
   const int c = (int)(blockIdx.x / (unsigned)a.n_queues);
   if (c >= a.n_chunks[q]) return;
   const int ub = a.unit_base[q];
-  const int total = (a.unit_base[q + 1] - ub) * a.U;
-  int it = (int)chunk_start(a, c);
-  const int it_end = (int)min((int64_t)total, chunk_start(a, c + 1));
+  int64_t first, end;
+  chunk_iters(a, c, (int64_t)(a.unit_base[q + 1] - ub) * a.U, &first, &end);
+  int it = (int)first;
+  const int it_end = (int)end;
   while (it < it_end) {
     const int ui = it / a.U;
     const int t0 = it - ui * a.U;
@@ -525,8 +519,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_merge_kernel(AttnArgs a) {
   const int ui = j / (BQ / kMergeRows), rb = j % (BQ / kMergeRows);
   if (ui >= a.unit_base[q + 1] - a.unit_base[q]) return;
   const int unit = a.unit_base[q] + ui;
-  const int c_first = chunk_of(a, (int64_t)ui * a.U);
-  const int c_last = chunk_of(a, (int64_t)ui * a.U + a.T - 1);
+  const int c_first = chunk_holding(a, (int64_t)ui * a.U);
+  const int c_last = chunk_holding(a, (int64_t)ui * a.U + a.T - 1);
   if (c_first == c_last) return;  // written whole by its only chunk
   merge_rows(a, q, unit, ui, rb, c_first, c_last);
 }
@@ -585,8 +579,8 @@ __global__ __launch_bounds__(kAttnThreads) void attn_merge_sal_kernel(AttnArgs a
   const int unit = a.unit_base[q] + ui;
   const int h = unit / a.q_tiles, qt = unit % a.q_tiles;
   const int N = a.n_tokens;
-  const int c_first = chunk_of(a, (int64_t)ui * a.U);
-  const int c_last = chunk_of(a, (int64_t)ui * a.U + a.T - 1);
+  const int c_first = chunk_holding(a, (int64_t)ui * a.U);
+  const int c_last = chunk_holding(a, (int64_t)ui * a.U + a.T - 1);
 
   // ---- this group's output rows, and the LSE of all the block's rows ----
   if (c_first != c_last) merge_rows(a, q, unit, ui, g, c_first, c_last);

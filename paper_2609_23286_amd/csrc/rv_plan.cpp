@@ -53,10 +53,10 @@ AttnPlan plan_attention(int n_cus, int n_queues, int n_tokens, int n_fkeys, int6
   }
   p.n_first = 0;
   if (k >= 1) {
-    p.E = (int)std::max<int64_t>(e_min, ceil_div(p.T, k));
-    k = (int)ceil_div(p.T, p.E);  // pieces that hold tiles
-    p.U = k * p.E;
-    p.E1 = p.E;
+    const int e = (int)std::min<int64_t>((int64_t)1 << 22, std::max<int64_t>(e_min, ceil_div(p.T, k)));
+    k = (int)ceil_div(p.T, e);  // pieces that hold tiles
+    p.U = k * e;
+    p.E = p.E1 = e * kCutScale;
   } else {
     // Stream-K.  Workgroup ids are dealt round-robin over the XCDs and then over the
     // CUs, so a queue's first n_cus / nq chunks go to the workgroups dispatched first
@@ -69,15 +69,19 @@ AttnPlan plan_attention(int n_cus, int n_queues, int n_tokens, int n_fkeys, int6
     // (no second workgroup per CU to favour the first over: uniform chunks)
     const int n_first = n_cus / nq < wgq ? std::max(0, n_cus / nq) : 0;
     const int n_rest = wgq - n_first;
-    p.E1 = (int)std::max<int64_t>(e_min, ceil_div(work * 100, (int64_t)n_first * pct + (int64_t)n_rest * 100));
-    p.E = (int)std::max<int64_t>(e_min, ceil_div((int64_t)p.E1 * pct, 100));
+    // (lengths are kept below 2^30 scaled positions: a chunk that long only arises with a
+    // handful of workgroup slots, and more, shorter chunks are then used instead)
+    const int64_t e_lo = (int64_t)e_min * kCutScale, e_hi = (int64_t)1 << 30;
+    const int64_t e1 = std::max<int64_t>(e_lo, ceil_div(work * kCutScale * 100, (int64_t)n_first * pct + (int64_t)n_rest * 100));
+    p.E1 = (int)std::min(e_hi, e1);
+    p.E = (int)std::min(e_hi, std::max<int64_t>(e_lo, ceil_div((int64_t)p.E1 * pct, 100)));
     p.n_first = p.E == p.E1 ? 0 : n_first;
     if (p.n_first == 0) p.E = p.E1;  // (no first workgroups to favour)
   }
   p.total_chunks = 0;
   int max_chunks = 0;
   for (int q = 0; q < nq; ++q) {
-    const int64_t iters = (int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.U;
+    const int64_t iters = (int64_t)(p.unit_base[q + 1] - p.unit_base[q]) * p.U * kCutScale;  // scaled
     const int64_t first = (int64_t)p.n_first * p.E;
     p.n_chunks[q] = iters <= first ? (int)ceil_div(iters, p.E) : p.n_first + (int)ceil_div(iters - first, p.E1);
     p.chunk_base[q] = p.total_chunks;
@@ -92,8 +96,8 @@ AttnPlan plan_attention(int n_cus, int n_queues, int n_tokens, int n_fkeys, int6
   return p;
 }
 
-bool plan_splits_units(const AttnPlan& p) {
-  return (int64_t)p.E < p.T || p.U != p.T || (int64_t)p.T % p.E != 0 || p.E1 != p.E;
+bool plan_splits_units(const AttnPlan& p) {  // unless every chunk is exactly one unit
+  return !(p.E1 == p.E && p.U == p.T && (int64_t)p.E == (int64_t)p.U * kCutScale);
 }
 
 // Without a forced split, a queue's chunk count is set by its workgroup slots: the

@@ -8,6 +8,13 @@
 
 #include "../../include/rv.h"
 
+// Functions shared with the kernels are compiled for both sides under the HIP compiler.
+#if defined(__HIPCC__)
+#define RV_HD __host__ __device__
+#else
+#define RV_HD
+#endif
+
 namespace rv {
 
 constexpr int kHeadDim = 64;     // head dimension supported by every kernel
@@ -20,13 +27,15 @@ constexpr int kMaxLayersPerLaunch = 24;
 
 constexpr int kMaxQueues = 16;     // work queues (one per XCD) in the attention kernel
 constexpr int kAttnWgPerCu = 2;    // attention workgroups resident per CU
+constexpr int kCutScale = 256;     // chunk lengths are planned in 1/256 iterations
 
 // Attention forward with per-query LSE over [memory ; frame], XCD-local stream-K.
 //
 // A unit is (head, 128-query tile); its context is T key tiles of 64 keys.  Units are
 // dealt to per-XCD queues (contiguous unit ranges); each queue's (unit, key tile)
 // iteration space is cut into chunks of E tiles, chunk c of queue q going to workgroup
-// c * n_queues + q, which the hardware places on queue q's XCD.
+// c * n_queues + q, which the hardware places on queue q's XCD.  Chunk lengths are
+// fractional (planned in 1/kCutScale tiles), so every workgroup slot gets a chunk.
 struct AttnArgs {
   const uint16_t* Q;       // [N][H][64]
   const uint16_t* K;
@@ -48,8 +57,8 @@ struct AttnArgs {
   int U;                   // iteration stride per unit: T (stream-K) or k * E >= T (k-way split)
   int n_units;             // n_heads * q_tiles
   int n_queues;
-  int E;                   // key tiles per chunk (the first n_first chunks of a queue)
-  int E1;                  // key tiles per later chunk (E1 = E unless n_first > 0)
+  int E;                   // chunk length in 1/kCutScale iterations (the first n_first
+  int E1;                  //   chunks of a queue; E1: the later ones, E1 = E unless n_first > 0)
   int n_first;             // chunks per queue of E tiles; the rest hold E1
   int unit_base[kMaxQueues + 1];
   int n_chunks[kMaxQueues];
@@ -140,6 +149,29 @@ struct AttnPlan {
   int n_chunks[kMaxQueues];
   int chunk_base[kMaxQueues];
 };
+
+// Chunk arithmetic of a plan or of the kernel arguments built from it (both carry E, E1,
+// n_first).  Chunk lengths are E (the first n_first chunks of a queue) and E1 in
+// 1/kCutScale iterations, and chunk c starts at the iteration its scaled start rounds
+// down to, so that the rounding is spread over all chunks.
+template <class A>
+RV_HD inline int64_t chunk_cut(const A& a, int c) {
+  const int64_t x = c < a.n_first ? (int64_t)c * a.E : (int64_t)a.n_first * a.E + (int64_t)(c - a.n_first) * a.E1;
+  return x / kCutScale;
+}
+// The chunk holding iteration `it`: the last chunk that starts at or before it.
+template <class A>
+RV_HD inline int chunk_holding(const A& a, int64_t it) {
+  const int64_t x = (it + 1) * kCutScale - 1, first = (int64_t)a.n_first * a.E;
+  return x < first ? (int)(x / a.E) : a.n_first + (int)((x - first) / a.E1);
+}
+// Iterations [first, end) of chunk c of a queue of `iters` iterations.
+template <class A>
+RV_HD inline void chunk_iters(const A& a, int c, int64_t iters, int64_t* first, int64_t* end) {
+  const int64_t e = chunk_cut(a, c + 1);
+  *first = chunk_cut(a, c);
+  *end = e < iters ? e : iters;
+}
 
 // Plan for n_tokens queries over mem_len memory keys then n_fkeys frame keys, on a
 // device of n_cus CUs and n_queues XCDs (1..kMaxQueues).  Reads the RV_ATTN_* overrides.

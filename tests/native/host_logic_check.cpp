@@ -21,11 +21,8 @@ static int g_fail = 0;
     }                                                    \
   } while (0)
 
-static int64_t chunk_start(const rv::AttnPlan& p, int c) {
-  return c < p.n_first ? (int64_t)c * p.E : (int64_t)p.n_first * p.E + (int64_t)(c - p.n_first) * p.E1;
-}
-
-// Every queue's iterations are covered exactly once by its chunks, in order.
+// Every queue's iterations are covered exactly once by its chunks, in order, through the
+// chunk arithmetic the kernels use.
 static void check_attention(int n_tokens, int n_fkeys, int64_t mem_len, int n_heads, int n_cus, int n_queues,
                             bool forced_split) {
   const rv::AttnPlan p = rv::plan_attention(n_cus, n_queues, n_tokens, n_fkeys, mem_len, n_heads);
@@ -47,8 +44,16 @@ static void check_attention(int n_tokens, int n_fkeys, int64_t mem_len, int n_he
       CHECK(n == 0, "empty queue has chunks");
       continue;
     }
-    for (int c = 0; c < n; ++c) CHECK(chunk_start(p, c) < chunk_start(p, c + 1), "chunk order");
-    CHECK(chunk_start(p, n - 1) < iters && iters <= chunk_start(p, n), "chunks cover the queue");
+    int64_t at = 0;
+    for (int c = 0; c < n; ++c) {
+      int64_t s0, s1;
+      rv::chunk_iters(p, c, iters, &s0, &s1);
+      CHECK(s0 == at && s0 < s1 && s1 <= iters, "chunk %d of queue %d: [%lld, %lld) after %lld", c, q,
+            (long long)s0, (long long)s1, (long long)at);
+      CHECK(rv::chunk_holding(p, s0) == c && rv::chunk_holding(p, s1 - 1) == c, "chunk of an iteration");
+      at = s1;
+    }
+    CHECK(at == iters, "chunks cover the queue");
   }
   CHECK(total == p.total_chunks, "total chunks");
   // the workspace rv_init allocates holds every plan that RV_ATTN_SPLIT does not force
@@ -102,7 +107,8 @@ int main() {
                              {"0", "100", nullptr, nullptr},         {"0", "101", nullptr, nullptr},
                              {"0", "400", nullptr, nullptr},         {nullptr, nullptr, "1", nullptr},
                              {nullptr, nullptr, "4", "1"},           {nullptr, "250", "3", "1"},
-                             {nullptr, nullptr, nullptr, "100000"}};
+                             {nullptr, nullptr, nullptr, "100000"},  {"0", "133", nullptr, "1"},
+                             {"0", "400", "4", "1"}};
   for (const Env& e : envs) {
     auto set = [](const char* k, const char* v) {
       if (v)

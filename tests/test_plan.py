@@ -1,7 +1,7 @@
 """The attention work plan (host logic, no device): every queue's iterations are cut
 into chunks that cover them exactly once, whatever the shape, device and overrides.
 
-The kernel derives a chunk's iteration range from the plan alone (chunk_start below
+The kernel derives a chunk's iteration range from the plan alone (chunk_range below
 restates the rule `include/rv.h` documents for rv_attention_plan), so a partition
 failure here would mean keys attended twice or never."""
 import itertools
@@ -21,19 +21,24 @@ OVERRIDES = [  # RV_ATTN_SPLIT, RV_ATTN_FIRST_PCT, RV_ATTN_WG_PER_CU, RV_ATTN_MI
     {"RV_ATTN_SPLIT": "0", "RV_ATTN_FIRST_PCT": "100"}, {"RV_ATTN_SPLIT": "0", "RV_ATTN_FIRST_PCT": "101"},
     {"RV_ATTN_SPLIT": "0", "RV_ATTN_FIRST_PCT": "400"}, {"RV_ATTN_WG_PER_CU": "1"},
     {"RV_ATTN_WG_PER_CU": "4", "RV_ATTN_MIN_CHUNK": "1"}, {"RV_ATTN_MIN_CHUNK": "100000"},
+    {"RV_ATTN_SPLIT": "0", "RV_ATTN_FIRST_PCT": "133", "RV_ATTN_MIN_CHUNK": "1"},
 ]
+ENV_KEYS = ("RV_ATTN_SPLIT", "RV_ATTN_FIRST_PCT", "RV_ATTN_WG_PER_CU", "RV_ATTN_MIN_CHUNK", "RV_ATTN_SPLIT_SLACK")
 
 
-def chunk_start(p, c):
-    return c * p.E if c < p.n_first else p.n_first * p.E + (c - p.n_first) * p.E1
+def chunk_range(p, c, units):
+    """Iterations [first, end) of chunk c of a queue of `units` units (the rule of include/rv.h)."""
+    def cut(c):  # lengths in 1/256 iterations
+        return (c * p.E if c < p.n_first else p.n_first * p.E + (c - p.n_first) * p.E1) // 256
+    return cut(c), min(cut(c + 1), units * p.U)
 
 
 def check_plan(p, n_tokens, n_fkeys, mem_len, n_heads, n_queues):
     q_tiles = -(-n_tokens // 128)
     T = -(-mem_len // 64) + -(-n_fkeys // 64)
     assert (p.q_tiles, p.n_units, p.T, p.n_queues) == (q_tiles, q_tiles * n_heads, T, n_queues)
-    assert p.U >= p.T and p.E >= 1 and p.E1 >= 1 and p.E >= p.E1
-    assert p.U == p.T or (p.U % p.E == 0 and p.n_first == 0 and p.E1 == p.E)  # stream-K or aligned pieces
+    assert p.U >= p.T and p.E >= 256 and p.E1 >= 256 and p.E >= p.E1
+    assert p.U == p.T or (p.E % 256 == 0 and p.U % (p.E // 256) == 0 and p.n_first == 0 and p.E1 == p.E)
     base = list(p.unit_base)[: n_queues + 1]
     assert base[0] == 0 and base[-1] == p.n_units and base == sorted(base)
     per_queue = p.grid // n_queues
@@ -47,16 +52,16 @@ def check_plan(p, n_tokens, n_fkeys, mem_len, n_heads, n_queues):
         if iters == 0:
             assert n == 0
             continue
-        starts = [chunk_start(p, c) for c in range(n + 1)]
+        ranges = [chunk_range(p, c, base[q + 1] - base[q]) for c in range(n)]
         # consecutive, non-empty chunks from iteration 0 whose last one reaches the end
-        assert starts[0] == 0 and all(a < b for a, b in zip(starts, starts[1:]))
-        assert starts[n - 1] < iters <= starts[n]
+        assert ranges[0][0] == 0 and ranges[-1][1] == iters
+        assert all(a < b for a, b in ranges) and all(r[1] == s[0] for r, s in zip(ranges, ranges[1:]))
     assert total == p.total_chunks
 
 
 @pytest.mark.parametrize("shape", SHAPES)
 def test_chunks_partition_every_queue(shape, monkeypatch):
-    for k in ("RV_ATTN_SPLIT", "RV_ATTN_FIRST_PCT", "RV_ATTN_WG_PER_CU", "RV_ATTN_MIN_CHUNK", "RV_ATTN_SPLIT_SLACK"):
+    for k in ENV_KEYS:
         monkeypatch.delenv(k, raising=False)
     for (n_cus, n_queues), env in itertools.product(DEVICES, OVERRIDES):
         with monkeypatch.context() as m:
@@ -67,14 +72,20 @@ def test_chunks_partition_every_queue(shape, monkeypatch):
 
 
 def test_first_dispatched_chunks_are_longer_in_stream_k(monkeypatch):
-    """At the benchmark's long contexts the plan is stream-K, and the first chunk of each
-    CU's pair holds 140 % of the other's tiles (rounded up)."""
-    for k in ("RV_ATTN_SPLIT", "RV_ATTN_FIRST_PCT", "RV_ATTN_WG_PER_CU", "RV_ATTN_MIN_CHUNK"):
+    """At the benchmark's long contexts the plan is stream-K, the first chunk of each CU's
+    pair holds 140 % of the other's tiles (rounded up, in 1/256 tiles), and the fractional
+    lengths give every one of the 512 workgroup slots a chunk of one of two neighbouring
+    integer lengths."""
+    for k in ENV_KEYS:
         monkeypatch.delenv(k, raising=False)
     p = rv.attention_plan(1041, 1041, 9990, 16, 256, 8)
     assert p.U == p.T == 174 and p.n_first == 32
     assert p.E == -(-p.E1 * 140 // 100)
     assert p.grid == 512
+    units = p.unit_base[1] - p.unit_base[0]
+    lengths = [b - a for a, b in (chunk_range(p, c, units) for c in range(p.n_chunks[0]))]
+    assert set(lengths[:32]) <= {p.E // 256, -(-p.E // 256)}
+    assert set(lengths[32:-1]) <= {p.E1 // 256, -(-p.E1 // 256)} and 1 <= lengths[-1] <= -(-p.E1 // 256)
 
 
 def test_plan_rejects_bad_sizes():
