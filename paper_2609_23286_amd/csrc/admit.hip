@@ -10,10 +10,11 @@
 // a contiguous range of 32-key blocks.  The sampled query rows and their LSE are staged
 // in LDS once per workgroup; each wave then takes its blocks two at a time (K rows in
 // registers) and sweeps the sampled queries in blocks of 32 with
-// v_mfma_f32_32x32x16_bf16 (Z = Q~ K^T, each lane owning one key column).  The
-// exponentials are summed in fp32 in a fixed order -- in-lane, over query blocks, then
-// across the two lane halves -- so S is bit-reproducible with no atomics.  The vector-ALU
-// work is one FMA, one exp and one add per (query, key).
+// v_mfma_f32_32x32x16_bf16 (Z = Q~ K^T, each lane owning one key column), each block's
+// accumulator seeded with -8 LSE of its rows so that the MFMAs leave 8 (z - LSE).  The
+// exponentials are summed in fp32 in a fixed order -- pairwise in-lane, over query
+// blocks, then across the two lane halves -- so S is bit-reproducible with no atomics.
+// The vector-ALU work is one multiply, one exp and one add per (query, key).
 //
 // select_kernel (Sec. 3.3 Eq. 6, head-specific retention): one workgroup per
 // (layer, head) takes the `budget` largest S_j, equal values ordered by lower index.
@@ -64,7 +65,8 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
   const int xcd = blockIdx.x % X, rr = blockIdx.x / X;
   const int lh = (rr / groups) * X + xcd, g = rr - (rr / groups) * groups;
   if (lh >= a.n_layers * H) return;  // uniform: ids past the last (layer, head)
-  const int layer = lh / H, h = lh - layer * H;
+  // (uniform: the layer's operand addresses then live in scalar registers)
+  const int layer = __builtin_amdgcn_readfirstlane(lh / H), h = __builtin_amdgcn_readfirstlane(lh - layer * H);
   const int n_blocks = (N + 31) / 32;
   const int per_group = (n_blocks + groups - 1) / groups;
   const int blk0 = g * per_group, blk1 = min(n_blocks, blk0 + per_group);
@@ -82,20 +84,23 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
     for (int j = blk0 * 32 + tid; j < min(N, blk1 * 32); j += NT) sal_h[j] = 0.f;
     return;
   }
-  float* s_lse2 = reinterpret_cast<float*>(smem);
+  float* s_nlse8 = reinterpret_cast<float*>(smem);
   uint16_t* s_q = reinterpret_cast<uint16_t*>(smem + (size_t)nq_pad * 4);
 
-  // LSE of the sampled queries in log2 units (padding rows: +inf -> weight 0) and, when
+  // -8 LSE of the sampled queries (the initial value of the score accumulators, so that
+  // an accumulator ends as q.k - 8 LSE = 8 (z - LSE); padding rows: -inf -> weight 0) and, when
   // they fit, the sampled query rows (padding rows zero), a pass of q_pass rows at a
-  // time.  Loads are issued in batches of kStageBatch per thread before any is stored,
-  // so a batch costs one round trip.
+  // time.  Every load reads a clamped, valid address and padding is selected afterwards,
+  // so no load sits behind a branch and its own wait: a pass's LSE and first batch of
+  // rows are requested together, then the K rows of the wave's first step, and the
+  // staging waits only for the former.
   auto q_token = [&](int i) {
     const int qi = i / a.q_cols;
     return a.q_base + qi * a.q_row_stride + (i - qi * a.q_cols) * a.q_col_stride;
   };
   // K rows (B operands, K^T) of a step's blocks: lane's key, dims ds*16 + half*8 ..;
-  // a pass's first step's rows are requested before its staging, each next step's
-  // rows while the current step computes.
+  // a pass's first step's rows are requested with its staging, each next step's rows
+  // while the current step computes.
   auto load_k = [&](int bb, bf16x8 (&kf)[kBlocksPerStep][4]) {
 #pragma unroll
     for (int b = 0; b < kBlocksPerStep; ++b) {
@@ -105,47 +110,57 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
       for (int ds = 0; ds < 4; ++ds) kf[b][ds] = *reinterpret_cast<const bf16x8*>(kp + ds * 16);
     }
   };
+  auto lse_load = [&](int i0, float (&v)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * NT + tid;
+      const float x = lse_h[q_token(min(i, a.n_q - 1))];
+      v[u] = i < a.n_q ? x : __builtin_inff();
+    }
+  };
+  auto lse_store = [&](int i0, const float (&v)[4]) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * NT + tid;
+      if (i < nq_pad) s_nlse8[i] = -8.0f * v[u];
+    }
+  };
+  // 16-byte chunk c (row p0 + c/8) of a pass's query rows
+  auto rows_load = [&](int p0, int c0, uint4 (&v)[kStageBatch]) {
+#pragma unroll
+    for (int u = 0; u < kStageBatch; ++u) {
+      const int c = c0 + u * NT + tid, i = p0 + (c >> 3), ch = c & 7;
+      const uint4 x = *reinterpret_cast<const uint4*>(Qh + (int64_t)q_token(min(i, a.n_q - 1)) * H * D + ch * 8);
+      v[u] = i < a.n_q ? x : uint4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto rows_store = [&](int rows, int c0, const uint4 (&v)[kStageBatch]) {
+#pragma unroll
+    for (int u = 0; u < kStageBatch; ++u) {
+      const int c = c0 + u * NT + tid, ch = c & 7;
+      if (c < rows * 8) *reinterpret_cast<uint4*>(&s_q[(c >> 3) * QS_STRIDE + ch * 8]) = v[u];
+    }
+  };
   bf16x8 kf[kBlocksPerStep][4], kn[kBlocksPerStep][4];
-  if (blk0 + wave * kBlocksPerStep < blk1) load_k(blk0 + wave * kBlocksPerStep, kf);
-
   for (int i0 = 0; i0 < nq_pad; i0 += NT * 4) {
-    float v[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u * NT + tid;
-      v[u] = i < a.n_q ? lse_h[q_token(i)] : __builtin_inff();
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u * NT + tid;
-      if (i < nq_pad) s_lse2[i] = v[u] * kLog2e;
-    }
+    float lv[4];
+    lse_load(i0, lv);
+    lse_store(i0, lv);
   }
 
   // Passes over the sampled queries; each key's sum is carried from pass to pass by the
   // lane that owns it (fixed order).
   const int q_pass = kStaged ? a.q_pass : nq_pad;
   for (int p0 = 0; p0 < nq_pad; p0 += q_pass) {
-    const int p1 = min(nq_pad, p0 + q_pass);
-    if (p0 > 0 && blk0 + wave * kBlocksPerStep < blk1) load_k(blk0 + wave * kBlocksPerStep, kf);
+    const int p1 = min(nq_pad, p0 + q_pass), rows = p1 - p0;
     if (kStaged) {
-      const int rows = p1 - p0;
       for (int c0 = 0; c0 < rows * 8; c0 += NT * kStageBatch) {
-        uint4 v[kStageBatch];
-#pragma unroll
-        for (int u = 0; u < kStageBatch; ++u) {
-          const int c = c0 + u * NT + tid, i = p0 + (c >> 3), ch = c & 7;
-          v[u] = uint4{0u, 0u, 0u, 0u};
-          if (c < rows * 8 && i < a.n_q)
-            v[u] = *reinterpret_cast<const uint4*>(Qh + (int64_t)q_token(i) * H * D + ch * 8);
-        }
-#pragma unroll
-        for (int u = 0; u < kStageBatch; ++u) {
-          const int c = c0 + u * NT + tid, ch = c & 7;
-          if (c < rows * 8) *reinterpret_cast<uint4*>(&s_q[(c >> 3) * QS_STRIDE + ch * 8]) = v[u];
-        }
+        uint4 qv[kStageBatch];
+        rows_load(p0, c0, qv);
+        rows_store(rows, c0, qv);
       }
     }
+    load_k(blk0 + wave * kBlocksPerStep, kf);  // (a wave without blocks loads rows it never uses)
     __syncthreads();
 
     for (int bb = blk0 + wave * kBlocksPerStep; bb < blk1; bb += NW * kBlocksPerStep) {
@@ -154,40 +169,52 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
       auto sweep = [&](auto nb_c) {
         constexpr int NB = decltype(nb_c)::value;
         float acc[NB] = {};
-        for (int qb = p0; qb < p1; qb += 32) {
-          bf16x8 qf[4];
+        // A operand (query rows qb + l32) of a query block, from LDS or memory.
+        auto load_q = [&](int qb, bf16x8 (&qf)[4]) {
           if (kStaged) {
 #pragma unroll
             for (int ds = 0; ds < 4; ++ds)
               qf[ds] = *reinterpret_cast<const bf16x8*>(&s_q[(qb - p0 + l32) * QS_STRIDE + ds * 16 + half * 8]);
           } else {
-            // Query row of sampled query qb + l32 for the A operand, read from memory.
             const uint16_t* qp = Qh + (int64_t)q_token(min(qb + l32, a.n_q - 1)) * H * D + half * 8;
 #pragma unroll
             for (int ds = 0; ds < 4; ++ds) qf[ds] = *reinterpret_cast<const bf16x8*>(qp + ds * 16);
           }
-          // LSE of this lane's 16 accumulator rows: queries qb + 8*(r/4) + 4*half + r%4
-          float l2[16];
+        };
+        bf16x8 qf[4];
+        load_q(p0, qf);
+        for (int qb = p0; qb < p1; qb += 32) {
+          // Each block's accumulator starts at -8 LSE of its 16 rows (queries
+          // qb + 8*(r/4) + 4*half + r%4), so the MFMAs leave 8 (z - LSE) in it and the
+          // two blocks' chains are independent.
+          f32x16 z[NB];
 #pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) {
-            const float4 v = *reinterpret_cast<const float4*>(&s_lse2[qb + 8 * r4 + 4 * half]);
-            l2[4 * r4] = v.x;
-            l2[4 * r4 + 1] = v.y;
-            l2[4 * r4 + 2] = v.z;
-            l2[4 * r4 + 3] = v.w;
-          }
+          for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+              const float4 v = *reinterpret_cast<const float4*>(&s_nlse8[qb + 8 * r4 + 4 * half]);
+              z[b][4 * r4] = v.x;
+              z[b][4 * r4 + 1] = v.y;
+              z[b][4 * r4 + 2] = v.z;
+              z[b][4 * r4 + 3] = v.w;
+            }
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int ds = 0; ds < 4; ++ds) z[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z[b], 0, 0, 0);
+          if (qb + 32 < p1) load_q(qb + 32, qf);  // the next block's rows, under this block's exponentials
 #pragma unroll
           for (int b = 0; b < NB; ++b) {
-            f32x16 z = {};
+            // exp(z - LSE) = 2^(8 (z - LSE) log2(e) / 8), all 16 independent, then a fixed
+            // pairwise sum.
+            float e[16];
 #pragma unroll
-            for (int ds = 0; ds < 4; ++ds) z = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z, 0, 0, 0);
-            float s0 = 0.f, s1 = 0.f;
+            for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(z[b][r] * kScaleLog2);
 #pragma unroll
-            for (int r = 0; r < 16; r += 2) {
-              s0 += __builtin_amdgcn_exp2f(fmaf(z[r], kScaleLog2, -l2[r]));
-              s1 += __builtin_amdgcn_exp2f(fmaf(z[r + 1], kScaleLog2, -l2[r + 1]));
-            }
-            acc[b] += s0 + s1;
+            for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+              for (int r = 0; r < w; ++r) e[r] = e[r] + e[r + w];
+            acc[b] += e[0];
           }
         }
 #pragma unroll
