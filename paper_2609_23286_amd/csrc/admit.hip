@@ -20,8 +20,8 @@
 // (layer, head) takes the `budget` largest S_j, equal values ordered by lower index.
 // The order is that of the 64-bit key (bits of S, ~j): fp32 bit patterns order like
 // the values for S >= 0.  Budgets up to kWaveTopK: each wave extracts the top `budget`
-// of its quarter by repeated wave-wide maxima, and the 4 x budget candidates are ranked
-// against each other.  Larger budgets: an MSB-first radix select over the bit patterns
+// of its quarter by repeated wave-wide maxima, and one wave extracts the top `budget` of
+// the 4 x budget candidates the same way.  Larger budgets: an MSB-first radix select over the bit patterns
 // finds the threshold value and how many of its ties to take, and block scans emit the
 // indices.  Either way the indices come out ascending and the chosen K/V rows are copied
 // to the memory arena at rows mem_len.. with their provenance.
@@ -358,47 +358,45 @@ __device__ __forceinline__ uint64_t rank_key(float v, int j) {
 }
 
 template <int CTRL>
-__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, 0xF, 0xF, false);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, 0xF, 0xF, false);
-  return ((uint64_t)hi << 32) | lo;
+__device__ __forceinline__ uint32_t max_dpp(uint32_t x) {
+  return max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false));
 }
 
-__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
-
-// The larger key of the pair a v_permlane*_swap leaves in (lo, hi): the two lanes'
-// values, in some order on every lane.
+// The larger value of the pair a v_permlane*_swap leaves: the two lanes' values, in some
+// order on every lane.
 template <class Pair>
-__device__ __forceinline__ uint64_t pair_max_u64(const Pair& lo, const Pair& hi) {
-  const uint64_t x = ((uint64_t)hi[0] << 32) | lo[0];
-  const uint64_t y = ((uint64_t)hi[1] << 32) | lo[1];
-  return max_u64(x, y);
+__device__ __forceinline__ uint32_t pair_max(const Pair& p) {
+  return max((uint32_t)p[0], (uint32_t)p[1]);
 }
 
 // Maximum over the wave's 64 lanes, left on every lane: DPP within each 16-lane row
-// (quad swaps, half mirror, mirror), then rows paired by v_permlane16_swap and halves by
-// v_permlane32_swap.
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
-  x = max_u64(x, dpp_u64<0xB1>(x));   // quad_perm [1,0,3,2]
-  x = max_u64(x, dpp_u64<0x4E>(x));   // quad_perm [2,3,0,1]
-  x = max_u64(x, dpp_u64<0x141>(x));  // row_half_mirror
-  x = max_u64(x, dpp_u64<0x140>(x));  // row_mirror
-  uint32_t lo = (uint32_t)x, hi = (uint32_t)(x >> 32);
-  x = pair_max_u64(__builtin_amdgcn_permlane16_swap(lo, lo, false, false),
-                   __builtin_amdgcn_permlane16_swap(hi, hi, false, false));
-  lo = (uint32_t)x;
-  hi = (uint32_t)(x >> 32);
-  return pair_max_u64(__builtin_amdgcn_permlane32_swap(lo, lo, false, false),
-                      __builtin_amdgcn_permlane32_swap(hi, hi, false, false));
+// (quad swaps, half mirror, mirror: each a max with a DPP operand), then rows paired by
+// v_permlane16_swap and halves by v_permlane32_swap.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+  x = max_dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  x = max_dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  x = max_dpp<0x141>(x);  // row_half_mirror
+  x = max_dpp<0x140>(x);  // row_mirror
+  x = pair_max(__builtin_amdgcn_permlane16_swap(x, x, false, false));
+  return pair_max(__builtin_amdgcn_permlane32_swap(x, x, false, false));
+}
+
+// The largest 64-bit key of the wave, on every lane, in two 32-bit reductions: the
+// largest upper half (the saliency bits), then the largest lower half (~index) among
+// the lanes holding that upper half.
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
+  const uint32_t hi = wave_max_u32((uint32_t)(k >> 32));
+  const uint32_t lo = wave_max_u32((uint32_t)(k >> 32) == hi ? (uint32_t)k : 0u);
+  return ((uint64_t)hi << 32) | lo;
 }
 
 // Top-`budget` (budget <= kWaveTopK) of sal[0..N), ascending, into s_idx.  Wave w owns
 // tokens [w*Q, (w+1)*Q), lane l the tokens w*Q + l + 64 m (m < kLaneSlots), kept as
 // keys sorted in registers.  Each round the wave's best remaining key is found by a
-// wave-wide maximum and its lane drops it.  The 4 x budget winners are then ranked
-// among themselves.
+// wave-wide maximum and its lane drops it.  Wave 0 then extracts the top `budget` of
+// the 4 x budget winners the same way (two per lane) and orders them by index.
 constexpr int kWaveTopK = 32;
-static_assert(NW * kWaveTopK % 8 == 0, "candidates are ranked in groups of eight");
+static_assert(NW * kWaveTopK <= 128, "the final extraction holds two candidates per lane");
 constexpr int kLaneSlots = 8;  // tokens per lane: the wave path takes N <= 4 * 64 * 8
 
 __device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx, uint64_t* s_cand) {
@@ -421,7 +419,7 @@ __device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx
     }
   }
   for (int r = 0; r < budget; ++r) {
-    const uint64_t win = wave_max_u64(v[0]);
+    const uint64_t win = wave_max_key(v[0]);
     if (lane == 0) s_cand[wave * budget + r] = win;
     if (win != 0 && win == v[0]) {  // this lane owns the winner (keys are distinct)
 #pragma unroll
@@ -430,42 +428,29 @@ __device__ void select_small(const float* sal, int N, int budget, int32_t* s_idx
     }
   }
   __syncthreads();
-  // candidate c is chosen if fewer than `budget` candidates outrank it; its output slot
-  // is the number of chosen candidates with a lower token index.  The candidates are
-  // read eight at a time (broadcast LDS reads in flight together); s_cand and s_chosen
-  // hold NW * kWaveTopK entries, a multiple of eight, so a group never reads past them
-  // (entries from nc on are masked out).
-  const int nc = NW * budget;
-  __shared__ int s_chosen[NW * kWaveTopK];
-  for (int c = tid; c < nc; c += NT) {
-    const uint64_t kc = s_cand[c];
-    int above = 0;
-    for (int u0 = 0; u0 < nc; u0 += 8) {
-      uint64_t x[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = s_cand[u0 + e];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) above += (u0 + e < nc) & (x[e] > kc);
+  if (wave == 0) {
+    // The overall top `budget` lie among the NW * budget winners: two per lane, sorted.
+    const int nc = NW * budget;
+    uint64_t c0 = lane < nc ? s_cand[lane] : 0, c1 = lane + 64 < nc ? s_cand[lane + 64] : 0;
+    if (c1 > c0) {
+      const uint64_t t = c0;
+      c0 = c1;
+      c1 = t;
     }
-    s_chosen[c] = kc != 0 && above < budget;
-  }
-  __syncthreads();
-  for (int c = tid; c < nc; c += NT) {
-    if (!s_chosen[c]) continue;
-    const uint32_t jc = ~(uint32_t)s_cand[c];
-    int pos = 0;
-    for (int u0 = 0; u0 < nc; u0 += 8) {
-      uint64_t x[8];
-      int ch[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        x[e] = s_cand[u0 + e];
-        ch[e] = s_chosen[u0 + e];
+    uint32_t mine = 0;  // lane r: ~index of the r-th winner
+    for (int r = 0; r < budget; ++r) {
+      const uint64_t win = wave_max_key(c0);
+      if (lane == r) mine = (uint32_t)win;
+      if (win == c0) {  // (a real key: fewer than budget + 1 tokens never reach this path)
+        c0 = c1;
+        c1 = 0;
       }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) pos += (u0 + e < nc) & (ch[e] != 0) & (~(uint32_t)x[e] < jc);
     }
-    s_idx[pos] = (int32_t)jc;
+    // lane r < budget: output slot = number of winners with a lower index
+    const uint32_t jr = ~mine;
+    int pos = 0;
+    for (int u = 0; u < budget; ++u) pos += ~(uint32_t)__builtin_amdgcn_readlane((int)mine, u) < jr;
+    if (lane < budget) s_idx[pos] = (int32_t)jr;
   }
   __syncthreads();
 }
