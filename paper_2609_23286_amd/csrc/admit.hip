@@ -41,6 +41,7 @@ constexpr int NW = NT / 64;
 constexpr int kBlocksPerStep = 2;  // 32-key blocks a saliency wave holds at once
 static_assert(kBlocksPerStep == 2, "a range's last step holds one block or two");
 constexpr int QS_STRIDE = kSalQStride;  // staged sampled-query rows, 144 bytes
+constexpr int kPrefetchQBlock = 4;  // query block of a step at which the next step's K rows are requested
 constexpr int kStageBatch = 9;     // 16-byte query-row loads in flight per thread (one pass of 288 rows)
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kScaleLog2 = kLog2e * 0.125f;
@@ -164,7 +165,12 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
     __syncthreads();
 
     for (int bb = blk0 + wave * kBlocksPerStep; bb < blk1; bb += NW * kBlocksPerStep) {
-      if (bb + NW * kBlocksPerStep < blk1) load_k(bb + NW * kBlocksPerStep, kn);
+      // The next step's K rows are requested a few query blocks into this step, not at
+      // its start: every workgroup of the launch stages at once, and the workgroups
+      // served first would otherwise queue their next step's rows ahead of the staging
+      // loads of those served last.
+      const bool prefetch = bb + NW * kBlocksPerStep < blk1;
+      const int q_prefetch = p0 + 32 * min(kPrefetchQBlock, (p1 - p0) / 32 - 1);
       // NB blocks held (the range's last step may hold fewer than kBlocksPerStep).
       auto sweep = [&](auto nb_c) {
         constexpr int NB = decltype(nb_c)::value;
@@ -184,6 +190,7 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
         bf16x8 qf[4];
         load_q(p0, qf);
         for (int qb = p0; qb < p1; qb += 32) {
+          if (prefetch && qb == q_prefetch) load_k(bb + NW * kBlocksPerStep, kn);
           // Each block's accumulator starts at -8 LSE of its 16 rows (queries
           // qb + 8*(r/4) + 4*half + r%4), so the MFMAs leave 8 (z - LSE) in it and the
           // two blocks' chains are independent.
