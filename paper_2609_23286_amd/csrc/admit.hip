@@ -58,19 +58,22 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
   const int groups = a.sal_groups;
-  // Workgroup b runs on XCD b % X (ids are dealt round-robin over the XCDs): the groups of
-  // (layer, head) lh = l_x X + x are ids (l_x groups + g) X + x, all on XCD x, so the
-  // head's sampled query rows and LSE that every group stages are read once from memory
-  // and then from that XCD's L2.  Placement only steers locality.
+  // Workgroup b runs on XCD b % X (ids are dealt round-robin over the XCDs): group g of
+  // (layer, head) lh = l_x X + x is id (g HX + l_x) X + x (HX = pairs per XCD), all of a
+  // head's groups on XCD x, so the head's sampled query rows and LSE that every group
+  // stages are read once from memory and then from that XCD's L2.  The first groups of
+  // all heads come first, so a head's groups are dispatched in different rounds and the
+  // later ones find the head's rows in L2.  Placement only affects speed.
   const int X = a.sal_xcds > 0 ? a.sal_xcds : 1;
+  const int HX = (a.n_layers * H + X - 1) / X;
   const int xcd = blockIdx.x % X, rr = blockIdx.x / X;
-  const int lh = (rr / groups) * X + xcd, g = rr - (rr / groups) * groups;
-  if (lh >= a.n_layers * H) return;  // uniform: ids past the last (layer, head)
+  const int g = rr / HX, lh = (rr - g * HX) * X + xcd;
+  if (g >= groups || lh >= a.n_layers * H) return;  // uniform: ids past the last (layer, head)
   // (uniform: the layer's operand addresses then live in scalar registers)
   const int layer = __builtin_amdgcn_readfirstlane(lh / H), h = __builtin_amdgcn_readfirstlane(lh - layer * H);
   const int n_blocks = (N + 31) / 32;
-  const int per_group = (n_blocks + groups - 1) / groups;
-  const int blk0 = g * per_group, blk1 = min(n_blocks, blk0 + per_group);
+  int blk0, blk1;
+  sal_group_blocks(a, g, n_blocks, &blk0, &blk1);
   if (blk0 >= blk1) return;  // uniform over the workgroup
   // The layer's operands, read once: this head's frame keys, query rows, LSE and
   // saliency row.

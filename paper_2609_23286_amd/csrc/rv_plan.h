@@ -210,4 +210,13 @@ int admit_max_dynamic_lds(int max_lds);
 // a->sal_groups, a->q_pass and a->stage_queries (rows staged when they fit max_lds).
 void plan_saliency(AdmitArgs* a, int n_lh, int n_cus, int max_lds);
 
+// 32-key blocks [*b0, *b1) of a head's saliency group g: a.sal_groups equal shares of
+// n_blocks, in order (the kernel and the host checks share this arithmetic).
+RV_HD inline void sal_group_blocks(const AdmitArgs& a, int g, int n_blocks, int* b0, int* b1) {
+  const int per = (n_blocks + a.sal_groups - 1) / a.sal_groups;
+  const int s = g * per, e = s + per;
+  *b0 = s < n_blocks ? s : n_blocks;
+  *b1 = e < n_blocks ? e : n_blocks;
+}
+
 }  // namespace rv

@@ -84,6 +84,16 @@ static void check_saliency(int grid_h, int grid_w, int n_special, int stride, in
   rv::plan_saliency(&a, n_lh, n_cus, max_lds);
   const int nq_pad = (a.n_q + 31) & ~31;
   CHECK(a.sal_groups >= 1, "saliency groups");
+  // the groups' block ranges partition the frame's 32-key blocks, in order
+  const int n_blocks = (n_tokens + 31) / 32;
+  int at = 0;
+  for (int g = 0; g < a.sal_groups; ++g) {
+    int b0, b1;
+    rv::sal_group_blocks(a, g, n_blocks, &b0, &b1);
+    CHECK(b0 <= b1 && (b0 == b1 || b0 == at), "group %d blocks [%d, %d) after %d", g, b0, b1, at);
+    if (b1 > b0) at = b1;
+  }
+  CHECK(at == n_blocks, "saliency groups cover %d of %d blocks", at, n_blocks);
   if (a.stage_queries) {
     CHECK(a.q_pass >= 32 && a.q_pass % 32 == 0, "pass size %d", a.q_pass);
     CHECK(rv::sal_lds_bytes(a) <= (size_t)rv::admit_max_dynamic_lds(max_lds), "staged rows exceed LDS");
