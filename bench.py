@@ -433,11 +433,12 @@ def unit_rates():
     s = rv._load_synth()
     s.rvs_unit_rates.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float)]
     s.rvs_unit_rates.restype = ctypes.c_int
-    ns = (ctypes.c_float * 7)()
+    ns = (ctypes.c_float * 11)()
     if s.rvs_unit_rates(n_cus, iters, ns):
         raise SystemExit("rvs_unit_rates failed")
     keys = ("mfma_wave", "valu_wave", "mfma_wave_and_valu_wave", "one_wave_both", "two_mfma_waves",
-            "two_mfma_waves_zero_operands", "two_valu_waves")
+            "two_mfma_waves_zero_operands", "two_valu_waves", "fma_wave", "two_fma_waves", "exp_wave",
+            "two_exp_waves")
     print(json.dumps({"ns_per_iter": dict(zip(keys, (float(x) for x in ns))), "cus": n_cus, "iterations": iters}),
           flush=True)
 
@@ -448,9 +449,14 @@ def unit_rates_summary(json_path):
     t_m, t_v, t_mv, t_b, t_mm, t_mz, t_vv = (t[k] for k in (
         "mfma_wave", "valu_wave", "mfma_wave_and_valu_wave", "one_wave_both", "two_mfma_waves",
         "two_mfma_waves_zero_operands", "two_valu_waves"))
+    t_f, t_ff, t_e, t_ee = (t[k] for k in ("fma_wave", "two_fma_waves", "exp_wave", "two_exp_waves"))
     hidden = (t_m + t_v - t_mv) / t_m
     clk_mfma = 32 / (t_mm / 8)        # GHz if an MFMA takes its 32 cycles
-    clk_valu = 2 * (16 * 8 + 32 * 4) / t_vv   # GHz if an exponential takes 8 cycles, the rest 4
+    clk = 2.4                          # the vector-ALU modes' clock under counters (2.37-2.40 GHz)
+    fma_1, fma_2 = t_f * clk / 32, t_ff * clk / 64      # SIMD cycles per FMA: one wave, two waves
+    exp_1, exp_2 = t_e * clk / 32, t_ee * clk / 64
+    # the chained VALU body (16 exponentials, 32 FMA/add) at the single-unit costs of two waves
+    body_pred = 16 * exp_2 + 32 * fma_2
     lines = ["# Unit rates on one MI355X: matrix core, vector-ALU exponentials, and their overlap", "",
              "Command (on the MI355X, from the repository root):", "", "```",
              "python bench.py --unit-rates > unit_rates.json",
@@ -458,22 +464,27 @@ def unit_rates_summary(json_path):
              f"One workgroup of eight waves per CU ({r['cus']} CUs; wave w runs on SIMD w % 4), "
              f"{r['iterations']} iterations of:",
              "MFMA body = 4 independent `v_mfma_f32_32x32x16_bf16`; VALU body = 8 independent chains of",
-             "2 x (FMA, `v_exp_f32`, add) = 16 exponentials + 32 FMA/add.  Time per iteration:", "",
+             "2 x (FMA, `v_exp_f32`, add) = 16 exponentials + 32 FMA/add; FMA body = 32 independent FMAs;",
+             "exp body = 32 independent `v_exp_f32`.  Time per iteration:", "",
              "| Waves per SIMD | ns per iteration |", "|---|---|",
              f"| one MFMA wave | {t_m:.1f} |", f"| two MFMA waves | {t_mm:.1f} (two bodies) |",
              f"| two MFMA waves, all-zero operands | {t_mz:.1f} (two bodies) |",
              f"| one VALU wave | {t_v:.1f} |", f"| two VALU waves | {t_vv:.1f} (two bodies) |",
              f"| one MFMA wave + one VALU wave | {t_mv:.1f} |",
-             f"| one wave running both bodies | {t_b:.1f} |", "",
+             f"| one wave running both bodies | {t_b:.1f} |",
+             f"| one FMA wave | {t_f:.1f} |", f"| two FMA waves | {t_ff:.1f} (two bodies) |",
+             f"| one exp wave | {t_e:.1f} |", f"| two exp waves | {t_ee:.1f} (two bodies) |", "",
              f"- two MFMA waves per SIMD: {t_mm / 8:.1f} ns per 32x32x16 bf16 MFMA; at its 32 cycles the SIMD "
              f"runs at {clk_mfma:.2f} GHz ({100 * clk_mfma / 2.4:.0f} % of the 2.4 GHz of the dense peak); "
              f"{t_mz / 8:.1f} ns with all-zero operands ({32 / (t_mz / 8):.2f} GHz at the same cycle count)",
-             f"- two VALU waves per SIMD: {t_vv:.1f} ns for two bodies; with the exponential at 8 cycles per "
-             f"wave (half the rate of an FMA or add, 4) that is 512 cycles at {clk_valu:.2f} GHz (at 16 cycles "
-             f"per exponential it would need {clk_valu * (16 * 16 + 32 * 4) / (16 * 8 + 32 * 4):.2f} GHz, above "
-             "the chip's 2.4)",
+             f"- independent FMAs (cycles at {clk} GHz, about the clock of the vector-ALU modes under "
+             f"counters): {fma_1:.1f} SIMD cycles each from one wave (one wave's issue limit), {fma_2:.1f} from two",
+             f"- independent exponentials: {exp_1:.1f} SIMD cycles each from one wave, {exp_2:.1f} from two: with "
+             f"two waves issuing, `v_exp_f32` holds the vector ALU {exp_2 / fma_2:.1f}x as long as an FMA",
+             f"- two VALU waves per SIMD: {t_vv:.1f} ns for two bodies = {t_vv * clk / 2:.0f} cycles per body "
+             f"against {body_pred:.0f} at the single-unit costs above (the chains' dependencies cost the rest)",
              f"- one VALU wave alone: {t_v:.1f} ns per body, {t_v / (t_vv / 2):.2f}x the two-wave time per body: one "
-             "wave's exponential-to-add dependencies leave the vector ALU idle part of the time",
+             "wave's issue limit and its exponential-to-add dependencies leave the vector ALU idle part of the time",
              f"- one MFMA wave alone: {t_m / 4:.1f} ns per MFMA (one wave's loop leaves issue gaps that a second "
              "wave fills)",
              f"- share of the MFMA time hidden under VALU work on the same SIMD (one wave of each): "
@@ -487,7 +498,8 @@ def unit_rates_summary(json_path):
 UNIT_RATE_COUNTERS = ("SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_VALU_MFMA_BUSY_CYCLES",
                       "GRBM_GUI_ACTIVE")
 UNIT_RATE_MODES = ("one MFMA wave", "one VALU wave", "one MFMA wave + one VALU wave", "one wave running both bodies",
-                   "two MFMA waves", "two MFMA waves, all-zero operands", "two VALU waves")
+                   "two MFMA waves", "two MFMA waves, all-zero operands", "two VALU waves", "one FMA wave",
+                   "two FMA waves", "one exp wave", "two exp waves")
 
 
 def unit_rates_counters(counter_dir, iters=4000):
@@ -499,7 +511,7 @@ def unit_rates_counters(counter_dir, iters=4000):
     acc = {}
     for f in glob.glob(os.path.join(counter_dir, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
-            m = re.search(r"unit_rate_kernel<(\d+)>", r["Kernel_Name"])
+            m = re.search(r"(?:unit|issue)_rate_kernel<(\d+)>", r["Kernel_Name"])
             if not m:
                 continue
             d = acc.setdefault((int(m.group(1)), r["Dispatch_Id"]), {})
@@ -520,7 +532,7 @@ def unit_rates_counters(counter_dir, iters=4000):
              f"cycles; instructions are per VALU-issuing wave and iteration ({iters} iterations).", "",
              "| Mode | ns per iteration | clock GHz | valu busy | mfma busy | VALU instrs / wave / iter | "
              "of them exp |", "|---|---|---|---|---|---|---|"]
-    valu_waves = {0: 4, 1: 4, 2: 8, 3: 4, 4: 8, 5: 8, 6: 8}  # waves per workgroup issuing VALU (MFMA counts)
+    valu_waves = {0: 4, 1: 4, 2: 8, 3: 4, 4: 8, 5: 8, 6: 8, 7: 4, 8: 8, 9: 4, 10: 8}  # waves issuing VALU (MFMA counts)
     for mode in sorted({k[0] for k in acc}):
         ds = [d for (m, _), d in acc.items() if m == mode]
         mean = lambda key: sum(d[key] for d in ds) / len(ds)

@@ -35,11 +35,12 @@ int rvs_frame_qkv(uint64_t seed, uint32_t frame, int layer0, int n_layers, int n
 
 /* Unit-rate probe (benchmark support): n_workgroups workgroups of eight waves repeat a loop
  * of four independent 32x32x16 bf16 MFMAs and/or a loop of 16 v_exp_f32 with 32 FMA/add
- * iters times; ns_per_iter[7] receives the time per iteration with (0) one MFMA wave per
+ * iters times; ns_per_iter[11] receives the time per iteration with (0) one MFMA wave per
  * SIMD, (1) one VALU wave per SIMD, (2) one MFMA and one VALU wave per SIMD, (3) both
  * bodies in one wave per SIMD, (4) two MFMA waves per SIMD, (5) as (4) with all-zero MFMA
- * operands, (6) two VALU waves per SIMD.  Synchronous; allocates and frees its own output
- * buffer. */
+ * operands, (6) two VALU waves per SIMD, and for a loop of 32 independent FMAs (7) one,
+ * (8) two waves per SIMD, of 32 independent v_exp_f32 (9) one, (10) two waves per SIMD.
+ * Synchronous; allocates and frees its own output buffer. */
 int rvs_unit_rates(int n_workgroups, int iters, float *ns_per_iter);
 
 /* Near-Gaussian bf16 tensor of n elements for counter stream (frame, layer, tag). */

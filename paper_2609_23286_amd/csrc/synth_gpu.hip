@@ -153,7 +153,9 @@ __global__ __launch_bounds__(256) void plant_kernel(uint64_t seed, uint32_t fram
 // mode 0: waves 0-3 MFMA only; 1: waves 0-3 VALU only; 2: waves 0-3 MFMA and waves 4-7
 // VALU (one of each per SIMD); 3: waves 0-3 both bodies in one instruction stream; 4: all
 // eight waves MFMA only (two per SIMD); 5: as 4 with all-zero MFMA operands; 6: all eight
-// waves VALU only (two per SIMD).
+// waves VALU only (two per SIMD).  Single-unit bodies (issue_rate_kernel): 7 / 8: 32
+// independent FMAs per iteration on one / two waves per SIMD; 9 / 10: 32 independent
+// v_exp_f32 per iteration on one / two waves per SIMD.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
@@ -193,6 +195,29 @@ __global__ __launch_bounds__(512) void unit_rate_kernel(float* out, int iters) {
   out[(int64_t)blockIdx.x * 512 + threadIdx.x] = s;
 }
 
+// MODE 7/8: FMA body, 9/10: exponential body; one wave per SIMD (waves 0-3) in 7 and 9,
+// two (all eight) in 8 and 10.  Every FMA and every exponential of an iteration is
+// independent of the others, so only the unit's rate and one wave's issue limit it.
+template <int MODE>
+__global__ __launch_bounds__(512) void issue_rate_kernel(float* out, int iters) {
+  const bool active = (MODE == 8 || MODE == 10) || (threadIdx.x >> 6) < 4;
+  float x[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) x[i] = 0.001f * (threadIdx.x & 15) + 0.01f * i;
+  float a = 0.5f + 0.0001f * threadIdx.x, b = -0.25f;
+  asm volatile("" : "+v"(a), "+v"(b));
+  if (active) {
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int i = 0; i < 32; ++i) x[i] = (MODE == 7 || MODE == 8) ? fmaf(x[i], a, b) : __builtin_amdgcn_exp2f(-x[i]);
+    }
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) s += x[i];
+  out[(int64_t)blockIdx.x * 512 + threadIdx.x] = s;
+}
+
 }  // namespace
 
 extern "C" int rvs_unit_rates(int n_workgroups, int iters, float* ns_per_iter) {
@@ -202,7 +227,7 @@ extern "C" int rvs_unit_rates(int n_workgroups, int iters, float* ns_per_iter) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
   int rc = 0;
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) rc = 4;
-  for (int m = 0; rc == 0 && m < 7; ++m) {
+  for (int m = 0; rc == 0 && m < 11; ++m) {
     for (int rep = 0; rc == 0 && rep < 2; ++rep) {  // the first launch warms up
       if (hipEventRecord(e0, nullptr) != hipSuccess) rc = 4;
       if (m == 0) hipLaunchKernelGGL(unit_rate_kernel<0>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
@@ -212,6 +237,10 @@ extern "C" int rvs_unit_rates(int n_workgroups, int iters, float* ns_per_iter) {
       if (m == 4) hipLaunchKernelGGL(unit_rate_kernel<4>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
       if (m == 5) hipLaunchKernelGGL(unit_rate_kernel<5>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
       if (m == 6) hipLaunchKernelGGL(unit_rate_kernel<6>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 7) hipLaunchKernelGGL(issue_rate_kernel<7>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 8) hipLaunchKernelGGL(issue_rate_kernel<8>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 9) hipLaunchKernelGGL(issue_rate_kernel<9>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
+      if (m == 10) hipLaunchKernelGGL(issue_rate_kernel<10>, dim3(n_workgroups), dim3(512), 0, nullptr, out, iters);
       if (hipGetLastError() != hipSuccess || hipEventRecord(e1, nullptr) != hipSuccess ||
           hipEventSynchronize(e1) != hipSuccess)
         rc = 4;

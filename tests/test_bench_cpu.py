@@ -46,19 +46,24 @@ def _lines(path):
         return fh.read()
 
 
-def test_unit_rates_summary_derives_the_clocks(tmp_path, monkeypatch):
-    """Two MFMA waves at 16 ns per 32-cycle MFMA mean a 2.00 GHz clock; two VALU bodies of
-    16 exponentials at 8 cycles and 32 FMA/add at 4 (512 cycles) in 256 ns, 2.00 GHz too."""
+def test_unit_rates_summary_derives_the_rates(tmp_path, monkeypatch):
+    """Two MFMA waves at 16 ns per 32-cycle MFMA mean a 2.00 GHz clock; at 2.4 GHz, 32 FMAs
+    in 32 ns from one wave are 2.4 cycles each, 64 in 40 ns from two are 1.5; 32
+    exponentials in 160 ns from one wave are 12 cycles each, 64 in 240 ns from two 9.0
+    (6.0x the two-wave FMA); the chained body then costs 16 x 9.0 + 32 x 1.5 = 192 cycles."""
     import json
     monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
     ns = {"mfma_wave": 80.0, "valu_wave": 200.0, "mfma_wave_and_valu_wave": 208.0, "one_wave_both": 210.0,
-          "two_mfma_waves": 128.0, "two_mfma_waves_zero_operands": 120.0, "two_valu_waves": 256.0}
+          "two_mfma_waves": 128.0, "two_mfma_waves_zero_operands": 120.0, "two_valu_waves": 256.0,
+          "fma_wave": 32.0, "two_fma_waves": 40.0, "exp_wave": 160.0, "two_exp_waves": 240.0}
     src = tmp_path / "ur.json"
     src.write_text(json.dumps({"ns_per_iter": ns, "cus": 256, "iterations": 4000}) + "\n")
     bench.unit_rates_summary(str(src))
     text = _lines(tmp_path / "unit_rates__mi355x.md")
     assert "16.0 ns per 32x32x16 bf16 MFMA" in text and "runs at 2.00 GHz (83 %" in text
-    assert "that is 512 cycles at 2.00 GHz" in text
+    assert "2.4 SIMD cycles each from one wave (one wave's issue limit), 1.5 from two" in text
+    assert "12.0 SIMD cycles each from one wave, 9.0 from two" in text and "6.0x as long as an FMA" in text
+    assert "= 307 cycles per body against 192 at the single-unit costs" in text  # 256 * 2.4 / 2
     assert "hidden under VALU work on the same SIMD (one wave of each): 90 %" in text  # (80 + 200 - 208) / 80
 
 
@@ -77,14 +82,16 @@ def test_unit_rates_counters_summary(tmp_path, monkeypatch):
     simd = 2_000_000 * 1024
     values = {"GRBM_GUI_ACTIVE": gui, "SQ_ACTIVE_INST_VALU": simd / 4 * 0.5, "SQ_VALU_MFMA_BUSY_CYCLES": simd * 0.25,
               "SQ_INSTS_VALU": 256 * 8 * 4000 * 48, "SQ_INSTS_VALU_TRANS_F32": 256 * 8 * 4000 * 16}
-    for disp in (1, 2):
+    for disp, kernel in ((1, "unit_rate_kernel<6>"), (2, "unit_rate_kernel<6>"), (3, "issue_rate_kernel<9>")):
         for name, v in values.items():
-            rows.append(f'{disp},{disp},"Agent 1",1,1,1,131072,7,"void (anonymous namespace)::unit_rate_kernel<6>'
+            rows.append(f'{disp},{disp},"Agent 1",1,1,1,131072,7,"void (anonymous namespace)::{kernel}'
                         f'(float*, int)",512,0,0,40,0,16,"{name}",{v},1000,{1000 + dur}\n')
     (d / "ur_counter_collection.csv").write_text(header + "".join(rows))
     bench.unit_rates_counters(str(d))
     text = _lines(tmp_path / "unit_rates__mi355x__counters.md")
     assert "| two VALU waves | 250.0 | 2.00 | 50.0 % | 25.0 % | 48.0 | 16.0 |" in text
+    # the exponential probe issues from four waves per workgroup: twice the instructions per wave
+    assert "| one exp wave | 250.0 | 2.00 | 50.0 % | 25.0 % | 96.0 | 32.0 |" in text
 
 
 def test_library_context_summary(tmp_path, monkeypatch):
