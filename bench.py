@@ -923,15 +923,18 @@ def main():
                 st = lib.rv_mem_truncate(mems[l].handle, mem_len(l, t))
                 if st:
                     raise rv.RVError(st, lib.rv_last_error().decode())
+        # Timing events, two per frame (three with staging): the frame's start, which also
+        # ends the previous frame's admission (every event costs the GPU a few
+        # microseconds, so adjacent boundaries share one), and the end of its attention.
+        if ev is not None:
+            ev[0].record(stream)
         if args.staged:  # the producer's part: the frame's K/V into each arena's tail
-            if ev is not None:
-                ev[3].record(stream)
             for l in range(L):
                 st = lib.rv_mem_stage_frame(mems[l].handle, vp(kp[l]), vp(vpp[l]), N, s_h)
                 if st:
                     raise rv.RVError(st, lib.rv_last_error().decode())
-        if ev is not None:
-            ev[0].record(stream)
+            if ev is not None:
+                ev[1].record(stream)
         for l in range(L):
             if args.staged:
                 st = lib.rv_attend_staged(vp(qp[l]), N, mems[l].handle, None, out_p[l], lse_p[l], None, s_h)
@@ -948,7 +951,7 @@ def main():
             if st:
                 raise rv.RVError(st, lib.rv_last_error().decode())
         if ev is not None:
-            ev[1].record(stream)
+            ev[2].record(stream)
         if anchor and t == 0:  # the global anchor: the first frame whole, in every layer (Eq. 4)
             if args.staged:
                 st = lib.rv_admit_staged_layers(L, qa, lse_arr, N, qref, N, mem_arr, t, sal_arr, None, s_h)
@@ -968,8 +971,6 @@ def main():
             st = 0
         if st:
             raise rv.RVError(st, lib.rv_last_error().decode())
-        if ev is not None:
-            ev[2].record(stream)
 
     # ---- warm-up, then the timed frames --------------------------------------------
     initial = (lambda l: mem_len(l, 0)) if full else (lambda l: rows_max[l])
@@ -981,27 +982,35 @@ def main():
     # cut the memories back, and cutting back is the only length change between frames)
     fill_memories(initial)
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in timed]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in timed]
+    end_event = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i, t in enumerate(timed):
         run_frame(t, events[i])
         if (i + 1) % 250 == 0:
             log(f"enqueued {i + 1} frames")
+    end_event.record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     rv.device_status()
     if full:
         assert all(m.len == mem_len(l, n_stream) for l, m in enumerate(mems))
 
+    # frame i: attention from its start (after the staging copies, when staged) to its
+    # attention end; admission from there to the next frame's start (the last: end_event)
+    attn_start = (lambda i: events[i][1]) if args.staged else (lambda i: events[i][0])
+    frame_end = lambda i: events[i + 1][0] if i + 1 < len(timed) else end_event
+    attn_ms_i = lambda i: attn_start(i).elapsed_time(events[i][2])
+    admit_ms_i = lambda i: events[i][2].elapsed_time(frame_end(i))
     for i in sorted({0, len(timed) // 2, len(timed) - 1}):
         t = timed[i]
-        log(f"frame {t}: attention {events[i][0].elapsed_time(events[i][1]) * 1e3 / L:.1f} us/launch "
+        log(f"frame {t}: attention {attn_ms_i(i) * 1e3 / L:.1f} us/launch "
             f"(context {mem_len(regulated[0] if regulated else 0, t) + N}), "
-            f"admission {events[i][1].elapsed_time(events[i][2]) * 1e3:.1f} us")
-    attn_ms = sum(e[0].elapsed_time(e[1]) for e in events)
-    admit_ms = sum(e[1].elapsed_time(e[2]) for e in events)
-    stage_ms = sum(e[3].elapsed_time(e[0]) for e in events) if args.staged else None
+            f"admission {admit_ms_i(i) * 1e3:.1f} us")
+    attn_ms = sum(attn_ms_i(i) for i in range(len(timed)))
+    admit_ms = sum(admit_ms_i(i) for i in range(len(timed)))
+    stage_ms = sum(events[i][0].elapsed_time(events[i][1]) for i in range(len(timed))) if args.staged else None
     n_timed = len(timed)
     flops = sum(attention_flops(N, H, d, mem_len(l, t) + N) for t in timed for l in range(L))
     n_attn = n_timed * L
