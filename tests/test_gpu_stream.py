@@ -8,7 +8,8 @@
 * Full size, in the launch configuration the benchmark times (24-layer ViT-L stack,
   1041 tokens x 16 heads, memory of 9,990 rows = frame 1000): the oracle computes the
   sampled queries row by row (all 266 saliency queries plus tile-edge rows); saliency,
-  the admitted sets and the appended rows are compared in full.
+  the admitted sets and the appended rows are compared in full -- per layer, and for the
+  benchmark's one admission launch over all 24 layers.
 """
 import numpy as np
 import pytest
@@ -215,6 +216,47 @@ def test_full_size_frame_sampled_rows(rv, name, layer, M):
     for h in range(H):
         assert (mk[h, M:] == K[idx[h], h]).all() and (mv[h, M:] == V[idx[h], h]).all()
     mem.close()
+
+
+def test_layer_batched_admission_at_benchmark_shape(rv):
+    """The admission launch the benchmark times: rv_admit_layers over all 24 layers of the
+    ViT-L stack (1041 tokens x 16 heads, 266 sampled queries, budget 10; two saliency
+    workgroups per (layer, head), 768 in the launch) on each layer's GPU attention LSE,
+    against the oracle layer by layer: every key's saliency within SAL_RTOL of the
+    column mass the oracle forms from its own LSE of the sampled queries, the selection
+    the exact top-k of the GPU saliency and valid under the band rule, the appended rows
+    bit for bit."""
+    import torch
+    cfg = synth.CONFIGS["vitl_stack_1000"]
+    L, H, N, k = cfg.n_layers, cfg.n_heads, cfg.n_tokens, cfg.budget
+    print(f"layer-batched admission L={L} H={H} N={N} budget={k}", flush=True)
+    qs = (cfg.grid_h, cfg.grid_w, cfg.n_special, cfg.stride)
+    qidx = oracle.qsub_index(*qs)
+    frames = [synth.frame_qkv(cfg, l, 500) for l in range(L)]
+    Qd, Kd, Vd, lse, sal, idx, mems = [], [], [], [], [], [], []
+    for Q, K, V in frames:
+        mem = rv.Memory(H, reserve_tokens=k, max_tokens=k)
+        q, kk, v = to_dev(Q), to_dev(K), to_dev(V)
+        out = torch.empty_like(q)
+        ls = torch.empty((H, N), dtype=torch.float32, device="cuda")
+        rv.attend_frame(q, kk, v, mem, out, ls)
+        Qd.append(q), Kd.append(kk), Vd.append(v), lse.append(ls), mems.append(mem)
+        sal.append(torch.empty((H, N), dtype=torch.float32, device="cuda"))
+        idx.append(torch.empty((H, k), dtype=torch.int32, device="cuda"))
+    rv.admit_layers(Qd, Kd, Vd, lse, qs, k, mems, 500, sal, idx)
+    rv.device_status()
+    for l, (Q, K, V) in enumerate(frames):
+        _, lse_o = oracle.attend(Q, K, V, rows=qidx)
+        sal_o = oracle.column_mass(Q, qidx, lse_o, K, "frame")
+        s = sal[l].cpu().numpy().astype(np.float64)
+        ix = idx[l].cpu().numpy()
+        assert (np.abs(s - sal_o) <= SAL_RTOL * sal_o).all(), f"layer {l}"
+        assert (ix == oracle.topk(s, k)).all(), f"layer {l}"
+        check_index_sets(ix, sal_o, k)
+        mk, mv, _ = (x.numpy().view(np.uint16) if x.dtype != torch.int32 else x.numpy() for x in mems[l].read())
+        for h in range(H):
+            assert (mk[h] == K[ix[h], h]).all() and (mv[h] == V[ix[h], h]).all(), f"layer {l} head {h}"
+        mems[l].close()
 
 
 def test_largest_frame_sampled_rows(rv):
