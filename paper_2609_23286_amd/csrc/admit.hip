@@ -21,10 +21,11 @@
 // The order is that of the 64-bit key (bits of S, ~j): fp32 bit patterns order like
 // the values for S >= 0.  Budgets up to kWaveTopK: each wave extracts the top `budget`
 // of its quarter by repeated wave-wide maxima, and one wave extracts the top `budget` of
-// the 4 x budget candidates the same way.  Larger budgets: an MSB-first radix select over the bit patterns
-// finds the threshold value and how many of its ties to take, and block scans emit the
-// indices.  Either way the indices come out ascending and the chosen K/V rows are copied
-// to the memory arena at rows mem_len.. with their provenance.
+// the 4 x budget candidates the same way.  Larger budgets: an MSB-first radix select
+// over the bit patterns finds the threshold value and how many of its ties to take, and
+// block scans emit the indices.  Either way the indices come out ascending and the
+// chosen K/V rows are copied to the memory arena at rows mem_len.. with their
+// provenance.
 #include <type_traits>
 
 #include "rv_internal.h"
@@ -92,18 +93,19 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
   uint16_t* s_q = reinterpret_cast<uint16_t*>(smem + (size_t)nq_pad * 4);
 
   // -8 LSE of the sampled queries (the initial value of the score accumulators, so that
-  // an accumulator ends as q.k - 8 LSE = 8 (z - LSE); padding rows: -inf -> weight 0) and, when
-  // they fit, the sampled query rows (padding rows zero), a pass of q_pass rows at a
-  // time.  Every load reads a clamped, valid address and padding is selected afterwards,
-  // so no load sits behind a branch and its own wait: a pass's LSE and first batch of
-  // rows are requested together, then the K rows of the wave's first step, and the
-  // staging waits only for the former.
+  // an accumulator ends as q.k - 8 LSE = 8 (z - LSE); padding rows: -inf -> weight 0)
+  // and, when they fit, the sampled query rows (padding rows zero), a pass of q_pass
+  // rows at a time.  Every load reads a clamped, valid address and padding is selected
+  // afterwards, so no load sits behind a branch with a wait of its own: the LSE loads go
+  // out together, then each batch of kStageBatch row loads per thread, and the K rows of
+  // the wave's first step are requested after the staged data, so that the staging
+  // does not wait for them.
   auto q_token = [&](int i) {
     const int qi = i / a.q_cols;
     return a.q_base + qi * a.q_row_stride + (i - qi * a.q_cols) * a.q_col_stride;
   };
   // K rows (B operands, K^T) of a step's blocks: lane's key, dims ds*16 + half*8 ..;
-  // a pass's first step's rows are requested with its staging, each next step's rows
+  // a pass's first step's rows are requested after its staging, each next step's rows
   // while the current step computes.
   auto load_k = [&](int bb, bf16x8 (&kf)[kBlocksPerStep][4]) {
 #pragma unroll
