@@ -285,10 +285,13 @@ def test_bad_shapes_are_rejected(rv):
     assert e.value.status == rv.RV_ERR_INVALID
 
 
-def test_admit_layers_is_bit_identical_to_per_layer_calls(rv):
-    """Deferred, layer-batched admission == per-layer saliency + admit, bit for bit."""
+@pytest.mark.parametrize("L", [3, 26])
+def test_admit_layers_is_bit_identical_to_per_layer_calls(rv, L):
+    """Deferred, layer-batched admission == per-layer saliency + admit, bit for bit (26
+    layers: two launches, of 24 layers and of 2)."""
     import torch
-    L, N, H, M, budget = 3, 300, 4, 200, 5
+    N, H, M, budget = 300, 4, 200, 5
+    print(f"admit_layers L={L}", flush=True)
     qs = (10, 30, 0, 2)
     results = []
     for batched in (False, True):
