@@ -95,18 +95,21 @@ __device__ __forceinline__ float half_sum(float x) {
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // LDS tile layout: 64 rows of 128 bytes, no padding.  The 16-byte chunk c of row r is
-// stored at chunk c ^ ((r >> 1) & 7) of that row: any 16 consecutive rows then map a
-// given logical chunk to 16 distinct (bank half, chunk) slots, so the 16-byte K reads
-// (one row per lane) and the transposing V reads (4 rows x 32 bytes per 16 lanes) are
-// free of bank conflicts.
-__device__ __forceinline__ int swz(int row, int chunk) { return row * D + ((chunk ^ ((row >> 1) & 7)) << 3); }
+// stored at chunk c ^ sw(r), sw(r) = (2 (r & 3) | (r >> 2) & 1) ^ 2 ((r >> 3) & 1), which
+// takes 8 distinct values on every 8 aligned rows and, with the row's parity, 16 distinct
+// (parity, chunk) pairs on every 16: the 16-byte K reads (one row per lane, 8 or 16
+// lanes a cycle) and the transposing V reads (4 rows x 32 bytes per 16 lanes, the rows'
+// 32-byte pieces on disjoint chunk pairs) are free of bank conflicts whether the LDS
+// serves 128 or 256 bytes a cycle.
+__device__ __forceinline__ int sw(int row) { return ((2 * (row & 3)) | ((row >> 2) & 1)) ^ (((row >> 3) & 1) << 1); }
+__device__ __forceinline__ int swz(int row, int chunk) { return row * D + ((chunk ^ sw(row)) << 3); }
 
 // Key/value rows of one head: the memory segment (row stride 64) followed by the frame
 // (row stride H*64).  Tiles go straight from global memory to LDS
 // (global_load_lds_dwordx4: lane l of a wave writes 16 bytes at the wave's LDS base +
 // 16 l), so each thread fetches the global chunk that belongs at its LDS slot: thread
 // tid fills physical chunk tid % 8 of rows tid / 8 and tid / 8 + 32, i.e. the global
-// chunk (tid % 8) ^ ((row >> 1) & 7) of those rows.  Addresses are a wave-uniform base
+// chunk (tid % 8) ^ sw(row) of those rows.  Addresses are a wave-uniform base
 // plus a 32-bit per-thread byte offset fixed for the whole segment; the last tile of
 // each part re-reads its last row in place of the rows past the end (always in
 // bounds; their scores are masked).
@@ -376,7 +379,7 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
     tc.mem_tail = a.nt_mem > 0 ? (int)(a.mem_len - (int64_t)(a.nt_mem - 1) * BK) : BK;
     tc.tok_tail = a.T > a.nt_mem ? a.n_fkeys - (a.T - 1 - a.nt_mem) * BK : BK;
     const int r1 = r + 32;
-    const int g0 = (c8 ^ (((r >> 1) & 7) << 3)), g1 = (c8 ^ (((r1 >> 1) & 7) << 3));
+    const int g0 = c8 ^ (sw(r) << 3), g1 = c8 ^ (sw(r1) << 3);
     tc.off_m0 = 2u * (uint32_t)(r * D + g0);
     tc.off_m1 = 2u * (uint32_t)(r1 * D + g1);
     tc.off_c0 = 2u * (uint32_t)(r * rs + g0);
