@@ -101,7 +101,7 @@ __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirs
 // lanes a cycle) and the transposing V reads (4 rows x 32 bytes per 16 lanes, the rows'
 // 32-byte pieces on disjoint chunk pairs) are free of bank conflicts whether the LDS
 // serves 128 or 256 bytes a cycle.
-__device__ __forceinline__ int sw(int row) { return ((2 * (row & 3)) | ((row >> 2) & 1)) ^ (((row >> 3) & 1) << 1); }
+__device__ __forceinline__ int sw(int row) { return attn_tile_swizzle(row); }
 __device__ __forceinline__ int swz(int row, int chunk) { return row * D + ((chunk ^ sw(row)) << 3); }
 
 // Key/value rows of one head: the memory segment (row stride 64) followed by the frame

@@ -154,6 +154,12 @@ struct AttnPlan {
 // n_first).  Chunk lengths are E (the first n_first chunks of a queue) and E1 in
 // 1/kCutScale iterations, and chunk c starts at the iteration its scaled start rounds
 // down to, so that the rounding is spread over all chunks.
+// Chunk (of 8) that holds logical 16-byte chunk 0 of row r of an attention K/V tile in
+// LDS (logical chunk c lies at c ^ attn_tile_swizzle(r)): 8 distinct values on every 8
+// aligned rows, 16 distinct (row parity, value) pairs on every 16 (the kernels and the
+// host checks share this).
+RV_HD inline int attn_tile_swizzle(int r) { return ((2 * (r & 3)) | ((r >> 2) & 1)) ^ (((r >> 3) & 1) << 1); }
+
 template <class A>
 RV_HD inline int64_t chunk_cut(const A& a, int c) {
   const int64_t x = c < a.n_first ? (int64_t)c * a.E : (int64_t)a.n_first * a.E + (int64_t)(c - a.n_first) * a.E1;

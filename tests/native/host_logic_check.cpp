@@ -102,7 +102,31 @@ static void check_saliency(int grid_h, int grid_w, int n_special, int stride, in
   }
 }
 
+// The attention tiles' LDS swizzle: distinct chunks on every 8 aligned rows (the K reads
+// of 8 lanes, one row each, at 128 bytes a cycle) and distinct (row parity, chunk) pairs
+// on every 16 (16 lanes at 256 bytes a cycle); and every aligned group of 4 rows puts a
+// 32-byte piece (an even chunk pair) on 4 disjoint chunk pairs (the transposing V reads).
+static void check_tile_swizzle() {
+  for (int r0 = 0; r0 < 64; r0 += 8) {
+    int seen = 0;
+    for (int r = r0; r < r0 + 8; ++r) seen |= 1 << rv::attn_tile_swizzle(r);
+    CHECK(seen == 0xFF, "rows %d..%d: swizzle values not distinct", r0, r0 + 7);
+  }
+  for (int r0 = 0; r0 < 64; r0 += 16) {
+    int seen = 0;
+    for (int r = r0; r < r0 + 16; ++r) seen |= 1 << (rv::attn_tile_swizzle(r) + 8 * (r & 1));
+    CHECK(seen == 0xFFFF, "rows %d..%d: (parity, swizzle) pairs not distinct", r0, r0 + 15);
+  }
+  for (int r0 = 0; r0 < 64; r0 += 4)
+    for (int c = 0; c < 8; c += 2) {
+      int seen = 0;
+      for (int r = r0; r < r0 + 4; ++r) seen |= 3 << ((c ^ rv::attn_tile_swizzle(r)) & 6);
+      CHECK(seen == 0xFF, "rows %d..%d, chunks %d,%d: pieces overlap", r0, r0 + 3, c, c + 1);
+    }
+}
+
 int main() {
+  check_tile_swizzle();
   static const int shapes[][4] = {  // n_tokens, n_fkeys, mem_len, n_heads
       {1041, 1041, 0, 16},   {1041, 1041, 1000, 16}, {1041, 1041, 5000, 16}, {1041, 1041, 9990, 16},
       {1041, 1041, 52000, 16}, {1041, 0, 11031, 16}, {1374, 1374, 26000, 16}, {16384, 16384, 3000, 2},
