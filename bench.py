@@ -706,7 +706,7 @@ def main():
     p.add_argument("--shared", action="store_true",
                    help="head-averaged selection (one top-k per layer) instead of head-specific")
     p.add_argument("--staged", action="store_true",
-                   help="stage each frame's K/V in the memory arenas (rv_mem_stage_frame, timed as its "
+                   help="stage each frame's K/V in the memory arenas (rv_mem_stage_frames, timed as its "
                         "own phase), attend over the contiguous arena (rv_attend_staged) and admit by "
                         "in-place compaction (rv_admit_staged_layers)")
     p.add_argument("--fused", action="store_true",
@@ -929,10 +929,9 @@ def main():
         if ev is not None:
             ev[0].record(stream)
         if args.staged:  # the producer's part: the frame's K/V into each arena's tail
-            for l in range(L):
-                st = lib.rv_mem_stage_frame(mems[l].handle, vp(kp[l]), vp(vpp[l]), N, s_h)
-                if st:
-                    raise rv.RVError(st, lib.rv_last_error().decode())
+            st = lib.rv_mem_stage_frames(L, mem_arr, ka, va, N, s_h)
+            if st:
+                raise rv.RVError(st, lib.rv_last_error().decode())
             if ev is not None:
                 ev[1].record(stream)
         for l in range(L):

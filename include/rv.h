@@ -296,6 +296,15 @@ rv_status rv_mem_stage(rv_mem m, int n_tokens, void **K_tail, void **V_tail,
  * memory) into the staged rows, on `stream`. */
 rv_status rv_mem_stage_frame(rv_mem m, const void *K, const void *V, int n_tokens, void *stream);
 
+/* rv_mem_stage_frame for n_layers memories (one per layer, equal head counts) and their
+ * frames K[l], V[l], with one copy launch for up to 24 layers.  Every memory gets its
+ * room before anything is enqueued: a failure (RV_ERR_INVALID for a NULL pointer or
+ * differing head counts, RV_ERR_CAPACITY / RV_ERR_OOM from the growth of layer l) copies
+ * nothing, though layers before l may have grown (dropping nothing: their length is
+ * unchanged). */
+rv_status rv_mem_stage_frames(int n_layers, const rv_mem *mems, const void *const *K, const void *const *V,
+                              int n_tokens, void *stream);
+
 /* rv_attend_frame (Sec. 3.1 Eq. 3, Sec. 3.3 LSE and saliency) for a frame staged in m:
  * the keys and values of head h are arena rows 0 .. length + n_tokens - 1 of m, i.e. the
  * memory followed by the staged frame.  Q, out: [n_tokens][n_heads][64] bf16; lse,

@@ -616,6 +616,20 @@ __global__ __launch_bounds__(256) void stage_kernel(uint16_t* dK, uint16_t* dV, 
   *reinterpret_cast<uint4*>(dV + d) = reinterpret_cast<const uint4*>(V)[c];
 }
 
+// Several layers' frames in one launch: blockIdx.y is the layer.
+__global__ __launch_bounds__(256) void stage_layers_kernel(StageArgs a) {
+  const StageLayer& L = a.layer[blockIdx.y];
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= (int64_t)a.n_tokens * a.n_heads * 8) return;
+  const int chunk = (int)(c & 7);
+  const int64_t row = c >> 3;  // token * H + head
+  const int h = (int)(row % a.n_heads);
+  const int64_t j = row / a.n_heads;
+  const int64_t d = ((int64_t)h * L.head_stride + j) * D + chunk * 8;
+  *reinterpret_cast<uint4*>(L.dK + d) = reinterpret_cast<const uint4*>(L.K)[c];
+  *reinterpret_cast<uint4*>(L.dV + d) = reinterpret_cast<const uint4*>(L.V)[c];
+}
+
 }  // namespace
 
 hipError_t launch_stage(uint16_t* dK, uint16_t* dV, int64_t head_stride, const uint16_t* K, const uint16_t* V,
@@ -623,6 +637,13 @@ hipError_t launch_stage(uint16_t* dK, uint16_t* dV, int64_t head_stride, const u
   const int64_t chunks = (int64_t)n * H * 8;
   hipLaunchKernelGGL(stage_kernel, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, dK, dV, head_stride,
                      K, V, n, H);
+  return hipGetLastError();
+}
+
+hipError_t launch_stage_layers(const StageArgs& a, hipStream_t s) {
+  const int64_t chunks = (int64_t)a.n_tokens * a.n_heads * 8;
+  hipLaunchKernelGGL(stage_layers_kernel, dim3((unsigned)((chunks + 255) / 256), (unsigned)a.n_layers), dim3(256), 0,
+                     s, a);
   return hipGetLastError();
 }
 

@@ -706,6 +706,34 @@ rv_status rv_mem_stage_frame(rv_mem m, const void* K, const void* V, int n_token
   return RV_OK;
 }
 
+rv_status rv_mem_stage_frames(int n_layers, const rv_mem* mems, const void* const* K, const void* const* V,
+                              int n_tokens, void* stream) {
+  if (n_layers < 1) return fail(RV_ERR_INVALID, "n_layers must be >= 1");
+  if (!mems || !K || !V) return fail(RV_ERR_INVALID, "mems, K and V are required");
+  for (int l = 0; l < n_layers; ++l) {
+    if (!mems[l] || !K[l] || !V[l]) return fail(RV_ERR_INVALID, "layer %d: memory, K and V are required", l);
+    if (mems[l]->n_heads != mems[0]->n_heads) return fail(RV_ERR_INVALID, "layer %d: head count differs", l);
+  }
+  // Room for every layer first, so that a failure enqueues nothing.
+  for (int l = 0; l < n_layers; ++l) {
+    rv_status st = rv_mem_stage(mems[l], n_tokens, nullptr, nullptr, nullptr, stream);
+    if (st != RV_OK) return st;
+  }
+  for (int l0 = 0; l0 < n_layers; l0 += rv::kMaxLayersPerLaunch) {
+    rv::StageArgs a{};
+    a.n_tokens = n_tokens;
+    a.n_heads = mems[0]->n_heads;
+    a.n_layers = std::min(rv::kMaxLayersPerLaunch, n_layers - l0);
+    for (int i = 0; i < a.n_layers; ++i) {
+      const rv_mem m = mems[l0 + i];
+      a.layer[i] = rv::StageLayer{m->K + m->len * rv::kHeadDim, m->V + m->len * rv::kHeadDim,
+                                  (const uint16_t*)K[l0 + i], (const uint16_t*)V[l0 + i], m->cap};
+    }
+    RV_HIP(rv::launch_stage_layers(a, (hipStream_t)stream), "stage launch");
+  }
+  return RV_OK;
+}
+
 rv_status rv_attend_staged(const void* Q, int n_tokens, rv_mem m, const rv_qsub* qs, void* out, float* lse,
                            float* saliency, void* stream) {
   if (!m) return fail(RV_ERR_INVALID, "memory is NULL");

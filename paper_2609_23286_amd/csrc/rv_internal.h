@@ -21,6 +21,8 @@ hipError_t static_scratch_address(float** ptr);
 // dK / dV + (h * head_stride + j) * 64.
 hipError_t launch_stage(uint16_t* dK, uint16_t* dV, int64_t head_stride, const uint16_t* K, const uint16_t* V,
                         int n, int H, hipStream_t s);
+// The same for a.n_layers layers' frames in one launch.
+hipError_t launch_stage_layers(const StageArgs& a, hipStream_t s);
 // Records the hardware XCC id of each of n_blocks workgroups into ids (device memory).
 hipError_t launch_xcc_probe(int* ids, int n_blocks, hipStream_t s);
 // max_lds: the device's LDS limit per workgroup (bytes), for the kernel attribute.

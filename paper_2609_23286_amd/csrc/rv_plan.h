@@ -135,6 +135,21 @@ struct AdmitArgs {
                            //   order before the selection (0: one row, the saliency itself)
 };
 
+// Frames copied to staged arena rows, one layer per grid row (rv_mem_stage_frames).
+struct StageLayer {
+  uint16_t* dK;            // row j of head h goes to dK / dV + (h * head_stride + j) * 64
+  uint16_t* dV;
+  const uint16_t* K;       // the frame: [n_tokens][n_heads][64] bf16
+  const uint16_t* V;
+  int64_t head_stride;
+};
+struct StageArgs {
+  StageLayer layer[kMaxLayersPerLaunch];
+  int n_tokens;
+  int n_heads;
+  int n_layers;
+};
+
 constexpr int kSalQStride = kHeadDim + 8;  // staged sampled-query rows: 72 elements (144 bytes)
 constexpr int kAdmitStaticLdsMargin = 4096;  // LDS left for the admission kernels' static arrays
 

@@ -71,6 +71,7 @@ def _load():
                                     vp], i32),
         "rv_mem_stage": ([vp, i32, P(vp), P(vp), P(i64), vp], i32),
         "rv_mem_stage_frame": ([vp, vp, vp, i32, vp], i32),
+        "rv_mem_stage_frames": ([i32, P(vp), P(vp), P(vp), i32, vp], i32),
         "rv_attend_staged": ([vp, i32, vp, P(rv_qsub), vp, vp, vp, vp], i32),
         "rv_admit_staged_layers": ([i32, P(vp), P(vp), i32, P(rv_qsub), i32, P(vp), i32, P(vp), P(vp), vp], i32),
         "rv_reserve_workspace": ([i32, i32, i64, i32], i32),
@@ -360,6 +361,19 @@ def admit_layers(Q, K, V, lse, qs, budget, mems, frame_id, saliency_out=None, id
         L, pack(Q, shp, 2, "Q"), pack(K, shp, 2, "K"), pack(V, shp, 2, "V"), pack(lse, (H, N), 4, "lse"),
         N, ctypes.byref(q), budget, arr(*[m.handle for m in mems]), frame_id, sal, idx, _stream(stream)))
 
+
+
+def stage_frames(mems, K, V, stream=None):
+    """rv_mem_stage_frames: stage each layer's frame (K[l], V[l]: [N, H, 64] bf16) in
+    mems[l], one copy launch for up to 24 layers."""
+    L = len(mems)
+    N = K[0].shape[0]
+    shp = (N, mems[0].n_heads, HEAD_DIM)
+    arr = ctypes.c_void_p * L
+    _check(_lib.rv_mem_stage_frames(L, arr(*[m.handle for m in mems]),
+                                    arr(*[_ptr(k, shp, 2, f"K[{i}]") for i, k in enumerate(K)]),
+                                    arr(*[_ptr(v, shp, 2, f"V[{i}]") for i, v in enumerate(V)]), N,
+                                    _stream(stream)))
 
 # ---- seeded stream generator on the GPU (benchmark inputs) -------------------------
 _synth = None

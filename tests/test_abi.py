@@ -76,6 +76,11 @@ def test_invalid_arguments_are_rejected_before_any_device_work():
     assert L.rv_mem_stage(None, 10, None, None, None, None) == rv.RV_ERR_INVALID
     assert L.rv_mem_stage_frame(None, vp(1), vp(1), 10, None) == rv.RV_ERR_INVALID
     assert L.rv_mem_stage_frame(vp(1), None, vp(1), 10, None) == rv.RV_ERR_INVALID
+    arr1 = (vp * 1)
+    assert L.rv_mem_stage_frames(0, arr1(vp(1)), arr1(vp(1)), arr1(vp(1)), 10, None) == rv.RV_ERR_INVALID
+    assert L.rv_mem_stage_frames(1, None, arr1(vp(1)), arr1(vp(1)), 10, None) == rv.RV_ERR_INVALID
+    assert L.rv_mem_stage_frames(1, arr1(None), arr1(vp(1)), arr1(vp(1)), 10, None) == rv.RV_ERR_INVALID
+    assert L.rv_mem_stage_frames(1, arr1(vp(1)), arr1(None), arr1(vp(1)), 10, None) == rv.RV_ERR_INVALID
     assert L.rv_attend_staged(vp(1), 10, None, None, vp(1), vp(1), None, None) == rv.RV_ERR_INVALID
     assert L.rv_admit_staged_layers(0, None, None, 10, None, 1, None, 0, None, None,
                                     None) == rv.RV_ERR_INVALID

@@ -578,6 +578,52 @@ def test_staged_calls_need_a_staged_frame(rv):
     mem.close()
 
 
+def test_staged_frames_in_one_launch_equal_per_layer_staging(rv):
+    """rv_mem_stage_frames (26 layers: launches of 24 and 2) stages what rv_mem_stage_frame
+    stages layer by layer, over memories with and without room for the frame: the
+    lengths stay put, the staged attention gives the same bits, and after the staged
+    admission (in-place compaction of the chosen staged rows) the arenas hold the same
+    bytes."""
+    import torch
+    L, H, N, M, budget = 26, 3, 130, 70, 4
+    qs = (10, 13, 0, 2)
+    print(f"stage_frames L={L} H={H} N={N} M={M}", flush=True)
+    runs = []
+    for batched in (False, True):
+        mems, frames = [], []
+        for l in range(L):
+            Q, K, V = frame(90 + l, N, H)
+            mem = rv.Memory(H, reserve_tokens=M + (N if l % 2 else 0), max_tokens=M + N + 8)
+            memK, memV = memory_rows(95 + l, H, M)
+            mem.write(torch.from_numpy(memK.view(np.int16)), torch.from_numpy(memV.view(np.int16)))
+            mems.append(mem)
+            frames.append((to_dev(Q), to_dev(K), to_dev(V)))
+        if batched:
+            rv.stage_frames(mems, [f[1] for f in frames], [f[2] for f in frames])
+        else:
+            for mem, f in zip(mems, frames):
+                mem.stage_frame(f[1], f[2])
+        assert all(m.len == M for m in mems)
+        outs, lses = [], []
+        for mem, f in zip(mems, frames):
+            out = torch.empty_like(f[0])
+            lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
+            rv.attend_staged(f[0], mem, out, lse)
+            outs.append(out)
+            lses.append(lse)
+        sals = [torch.empty((H, N), dtype=torch.float32, device="cuda") for _ in range(L)]
+        rv.admit_staged_layers([f[0] for f in frames], lses, qs, budget, mems, 3, sals)
+        rv.device_status()
+        runs.append(([o.cpu() for o in outs], [x.cpu() for x in lses], [m.read() for m in mems]))
+        assert all(m.len == M + budget for m in mems)
+        for m in mems:
+            m.close()
+    (oa, la, ma), (ob, lb, mb) = runs
+    for l in range(L):
+        assert (oa[l] == ob[l]).all() and (la[l] == lb[l]).all(), f"layer {l}"
+        assert all((x == y).all() for x, y in zip(ma[l], mb[l])), f"layer {l}"
+
+
 FUSED_CASES = [  # (N, H, M, qs, plan overrides): ragged blocks, empty memory, a block with no
                  # sampled query, every query sampled, units covered whole by one chunk
     (1041, 16, 0, (28, 37, 5, 2), {}),
