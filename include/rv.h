@@ -14,8 +14,9 @@
  * General conventions
  *   - Every tensor pointer named in a compute call is a DEVICE pointer on the current
  *     HIP device, owned by the caller, unless stated otherwise.
- *   - bf16 means IEEE-754 binary32 truncated to its upper 16 bits (bfloat16), stored
- *     as 2-byte little-endian words.
+ *   - bf16 means bfloat16: the upper 16 bits of an IEEE-754 binary32, stored as 2-byte
+ *     little-endian words; values the library produces in bf16 are rounded to nearest
+ *     (ties to even).
  *   - Frame tensors Q, K, V, out: [n_tokens][n_heads][head_dim] bf16, contiguous (the
  *     layout a fused QKV projection writes).  Per-head vectors (lse, saliency):
  *     [n_heads][n_tokens] fp32.  Memory: [n_heads][head_stride][head_dim] bf16, rows
