@@ -135,13 +135,14 @@ def admission_traffic(workload):
 
 def bench_args():
     """This command's benchmark arguments, without the summary options."""
+    n_args = {"--pmc-summary": 2, "--trace-summary": 2, "--mfma-summary": 4}
     out, skip = [], 0
     for a in sys.argv[1:]:
         if skip:
             skip -= 1
             continue
-        if a in ("--pmc-summary", "--trace-summary", "--mfma-summary"):
-            skip = 3 if a == "--mfma-summary" else 2
+        if a in n_args:
+            skip = n_args[a]
             continue
         out.append(a)
     return " ".join(out)

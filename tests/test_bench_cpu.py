@@ -139,3 +139,13 @@ def test_traffic_summary_scales_by_the_calibration_copy(tmp_path, monkeypatch):
         assert bench.recorded_traffic(k, "w") == pytest.approx(expect)
     assert bench.attention_traffic("w") == pytest.approx((1000 * 2 + 500 + 300 * 2 + 100) * 1024)
     assert bench.admission_traffic("w") == pytest.approx((2000 * 2 + 50 + 80 * 2 + 60) * 1024)
+
+
+def test_summary_commands_quote_the_benchmark_arguments_only(monkeypatch):
+    """Each summary option's own arguments are dropped from the quoted benchmark command."""
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--steps", "20", "--mfma-summary", "a", "b", "c", "t.json",
+                                      "--warmup", "5"])
+    assert bench.bench_args() == "--steps 20 --warmup 5"
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--trace-summary", "d", "t.json", "--staged", "--pmc-summary",
+                                      "f", "w"])
+    assert bench.bench_args() == "--staged"
