@@ -190,6 +190,11 @@ template <bool kFirst>
 __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8 (&qf)[4], int lane, int valid,
                                              SoftmaxState& sm) {
   const int l32 = lane & 31, half = lane >> 5;
+  // Wave priority 1 from the score MFMAs through the softmax, 0 for the value product: of
+  // the two waves sharing a SIMD, the one in the first part of its tile issues first, which
+  // keeps the pair out of step so that one's MFMAs run under the other's vector work
+  // (about +1 % per stream over a uniform priority).  Priority changes no result.
+  __builtin_amdgcn_s_setprio(1);
   f32x16 s0 = {}, s1 = {};
 #pragma unroll
   for (int ds = 0; ds < 4; ++ds) {
@@ -254,6 +259,7 @@ __device__ __forceinline__ void tile_compute(const uint16_t* stage, const bf16x8
     if (__any(!(rsum < kOverflowGuard))) exact();
   }
   sm.l += rsum;
+  __builtin_amdgcn_s_setprio(0);
 
   // V^T operand through transposing LDS reads.  Within each 16-lane group, lane i
   // receives element i%4 of the 8-byte chunk addressed by lane 4r + i/4 (r = 0..3), so
