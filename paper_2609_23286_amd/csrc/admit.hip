@@ -196,6 +196,11 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
         load_q(p0, qf);
         for (int qb = p0; qb < p1; qb += 32) {
           if (prefetch && qb == q_prefetch) load_k(bb + NW * kBlocksPerStep, kn);
+          // Wave priority 0 for the MFMAs, 1 from the next block's row reads through the
+          // exponentials: of the waves sharing a SIMD, those in their vector work issue
+          // first, so the MFMAs of the others run under it (about -2 % per launch against a
+          // uniform priority; priority changes no result).
+          __builtin_amdgcn_s_setprio(0);
           // Each block's accumulator starts at -8 LSE of its 16 rows (queries
           // qb + 8*(r/4) + 4*half + r%4), so the MFMAs leave 8 (z - LSE) in it and the
           // two blocks' chains are independent.
@@ -214,6 +219,7 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
           for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int ds = 0; ds < 4; ++ds) z[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ds], kf[b][ds], z[b], 0, 0, 0);
+          __builtin_amdgcn_s_setprio(1);
           if (qb + 32 < p1) load_q(qb + 32, qf);  // the next block's rows, under this block's exponentials
 #pragma unroll
           for (int b = 0; b < NB; ++b) {
@@ -229,6 +235,7 @@ __device__ __forceinline__ void sal_body(const AdmitArgs& a, unsigned char* smem
             acc[b] += e[0];
           }
         }
+        __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
           const float tot = acc[b] + __shfl_xor(acc[b], 32);
