@@ -43,7 +43,8 @@
  *     in 64-key tiles, default 2), RV_ATTN_SPLIT_SLACK (tiles by which the aligned split
  *     may exceed stream-K before stream-K is taken, default 1), RV_ATTN_FIRST_PCT (tiles
  *     of a stream-K chunk served by a workgroup dispatched first on its CU, in per cent
- *     of the others', default 140).
+ *     of the others'; by default the share that makes the later chunks end on unit
+ *     boundaries when one lies in 115-160, else 140).
  */
 #ifndef RV_H
 #define RV_H

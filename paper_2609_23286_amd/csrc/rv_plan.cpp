@@ -65,18 +65,53 @@ AttnPlan plan_attention(int n_cus, int n_queues, int n_tokens, int n_fkeys, int6
     // placement gives the same results).
     p.U = p.T;
     const int64_t work = (int64_t)max_units * p.T;
-    const int pct = std::max(100, env_int("RV_ATTN_FIRST_PCT", kFirstChunkPct));
+    const int pct_env = env_int("RV_ATTN_FIRST_PCT", 0);
+    const int pct = std::max(100, pct_env > 0 ? pct_env : kFirstChunkPct);
     // (no second workgroup per CU to favour the first over: uniform chunks)
     const int n_first = n_cus / nq < wgq ? std::max(0, n_cus / nq) : 0;
     const int n_rest = wgq - n_first;
     // (lengths are kept below 2^30 scaled positions: a chunk that long only arises with a
     // handful of workgroup slots, and more, shorter chunks are then used instead)
     const int64_t e_lo = (int64_t)e_min * kCutScale, e_hi = (int64_t)1 << 30;
-    const int64_t e1 = std::max<int64_t>(e_lo, ceil_div(work * kCutScale * 100, (int64_t)n_first * pct + (int64_t)n_rest * 100));
-    p.E1 = (int)std::min(e_hi, e1);
-    p.E = (int)std::min(e_hi, std::max<int64_t>(e_lo, ceil_div((int64_t)p.E1 * pct, 100)));
-    p.n_first = p.E == p.E1 ? 0 : n_first;
-    if (p.n_first == 0) p.E = p.E1;  // (no first workgroups to favour)
+    // Unit-aligned form: later chunks of exactly T/k tiles (k dividing n_rest) cover the
+    // queue's last n_rest/k units k to a unit, and the first chunks share the units before
+    // them equally, so that every unit boundary is a chunk boundary and no later chunk
+    // starts a second segment.  Taken (unless RV_ATTN_FIRST_PCT sets the share) when the
+    // first chunks then hold kAlignMinPct..kAlignMaxPct per cent of a later one's tiles,
+    // the share closest to kFirstChunkPct if several k qualify.
+    constexpr int kAlignMinPct = 115, kAlignMaxPct = 160;
+    bool aligned = false;
+    if (pct_env <= 0 && n_first > 0) {
+      int64_t best_e = 0, best_e1 = 0, best_dist = -1;
+      for (int k = 1; k <= n_rest; ++k) {
+        const int64_t rest_units = n_rest / k;
+        if (n_rest % k != 0 || rest_units >= max_units || ((int64_t)p.T * kCutScale) % k != 0) continue;
+        const int64_t first_work = (int64_t)(max_units - rest_units) * p.T * kCutScale;
+        if (first_work % n_first != 0) continue;
+        const int64_t e1 = (int64_t)p.T * kCutScale / k, e = first_work / n_first;
+        if (e * 100 < e1 * kAlignMinPct || e * 100 > e1 * kAlignMaxPct || e1 < e_lo || e > e_hi) continue;
+        const int64_t dist = std::abs(e * 100 - e1 * kFirstChunkPct) * 1000 / e1;  // (in 1/1000 per cent)
+        if (best_dist < 0 || dist < best_dist) {
+          best_dist = dist;
+          best_e = e;
+          best_e1 = e1;
+        }
+      }
+      if (best_dist >= 0) {
+        p.E = (int)best_e;
+        p.E1 = (int)best_e1;
+        p.n_first = n_first;
+        aligned = true;
+      }
+    }
+    if (!aligned) {
+      const int64_t e1 =
+          std::max<int64_t>(e_lo, ceil_div(work * kCutScale * 100, (int64_t)n_first * pct + (int64_t)n_rest * 100));
+      p.E1 = (int)std::min(e_hi, e1);
+      p.E = (int)std::min(e_hi, std::max<int64_t>(e_lo, ceil_div((int64_t)p.E1 * pct, 100)));
+      p.n_first = p.E == p.E1 ? 0 : n_first;
+      if (p.n_first == 0) p.E = p.E1;  // (no first workgroups to favour)
+    }
   }
   p.total_chunks = 0;
   int max_chunks = 0;

@@ -72,20 +72,43 @@ def test_chunks_partition_every_queue(shape, monkeypatch):
 
 
 def test_first_dispatched_chunks_are_longer_in_stream_k(monkeypatch):
-    """At the benchmark's long contexts the plan is stream-K, the first chunk of each CU's
-    pair holds 140 % of the other's tiles (rounded up, in 1/256 tiles), and the fractional
-    lengths give every one of the 512 workgroup slots a chunk of one of two neighbouring
-    integer lengths."""
+    """At the benchmark's long contexts the plan is stream-K in its unit-aligned form: the
+    later chunks are a quarter of a unit (T/4 tiles, so four of them end exactly on each
+    unit boundary of the queue's last 8 of 18 units) and the first chunk of each CU's pair
+    shares the first 10 units with the other 31 (125 % of a later chunk's tiles); the
+    fractional lengths give every one of the 512 workgroup slots a chunk of one of two
+    neighbouring integer lengths.  With RV_ATTN_FIRST_PCT set, the share is that per cent
+    (rounded up, in 1/256 tiles)."""
     for k in ENV_KEYS:
         monkeypatch.delenv(k, raising=False)
     p = rv.attention_plan(1041, 1041, 9990, 16, 256, 8)
     assert p.U == p.T == 174 and p.n_first == 32
-    assert p.E == -(-p.E1 * 140 // 100)
+    assert p.E1 * 4 == p.T * 256 and p.E * 32 == 10 * p.T * 256 and p.E * 100 == p.E1 * 125
     assert p.grid == 512
     units = p.unit_base[1] - p.unit_base[0]
     lengths = [b - a for a, b in (chunk_range(p, c, units) for c in range(p.n_chunks[0]))]
     assert set(lengths[:32]) <= {p.E // 256, -(-p.E // 256)}
     assert set(lengths[32:-1]) <= {p.E1 // 256, -(-p.E1 // 256)} and 1 <= lengths[-1] <= -(-p.E1 // 256)
+    monkeypatch.setenv("RV_ATTN_FIRST_PCT", "140")
+    p = rv.attention_plan(1041, 1041, 9990, 16, 256, 8)
+    assert p.n_first == 32 and p.E == -(-p.E1 * 140 // 100) and p.grid == 512
+
+
+@pytest.mark.parametrize("M", [1500, 2500, 4990, 7770, 9990])
+def test_aligned_plans_start_every_unit_at_a_chunk_boundary(M, monkeypatch):
+    """In the unit-aligned form no later chunk holds tiles of two units, and the first
+    chunks end on a unit boundary (for every queue, including those with fewer units)."""
+    for k in ENV_KEYS:
+        monkeypatch.delenv(k, raising=False)
+    p = rv.attention_plan(1041, 1041, M, 16, 256, 8)
+    assert p.U == p.T and p.n_first == 32 and (p.T * 256) % p.E1 == 0
+    assert p.n_first * p.E % (p.T * 256) == 0
+    for q in range(8):
+        units = p.unit_base[q + 1] - p.unit_base[q]
+        for c in range(p.n_first, p.n_chunks[q]):
+            a, b = chunk_range(p, c, units)
+            if b > a:
+                assert a // p.T == (b - 1) // p.T, (q, c, a, b)
 
 
 def test_plan_rejects_bad_sizes():
