@@ -438,42 +438,58 @@ __device__ void process_segment(const AttnArgs& a, int q, int c, int unit, int u
   }
 
   const float l_tot = half_sum(sm.l);
-  if (t0 == 0 && t1 == a.T) {
-    if (wave_active && qi < a.n_tokens) {
-      const float inv = 1.f / l_tot;
-      uint16_t* op = a.out + ((int64_t)qi * a.n_heads + h) * D + 4 * half;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        *reinterpret_cast<uint2*>(op + 8 * j) =
-            to_bf16x4(sm.o0[4 * j] * inv, sm.o0[4 * j + 1] * inv, sm.o0[4 * j + 2] * inv, sm.o0[4 * j + 3] * inv);
-        *reinterpret_cast<uint2*>(op + 32 + 8 * j) =
-            to_bf16x4(sm.o1[4 * j] * inv, sm.o1[4 * j + 1] * inv, sm.o1[4 * j + 2] * inv, sm.o1[4 * j + 3] * inv);
-      }
-      if (half == 0) a.lse[(int64_t)h * a.n_tokens + qi] = (sm.m + __log2f(l_tot)) * kLn2;
-    }
-    return;
-  }
-
-  // Partial result: merged by the second launch.
-  const int seg = chunk_start(a, c) >= (int64_t)ui * a.U ? 0 : 1;
-  float* ps = a.part + (int64_t)(2 * (a.chunk_base[q] + c) + seg) * kAttnSlotFloats;
+  // The output rows (normalised by the row sum, bf16) go out through LDS: each wave stages
+  // its 32 rows (row stride kOutStageRow elements, so that the 32 rows' 8-byte pieces spread
+  // over the banks), then writes whole 128-byte rows, 8 lanes a row (before: each store
+  // wrote 16 bytes into each of 32 rows; 2 % per stream).  The ring is free: the last
+  // step ended with a barrier.
+  constexpr int kOutStageRow = D + 8;
+  uint16_t* const st = lds + wave * 32 * kOutStageRow;
   if (wave_active) {
-    // normalised partial output in bf16 (the merge weights it by 2^(m - M) l), m and l in fp32
-    const int row = wave * 32 + l32;
     const float inv = 1.f / l_tot;
-    uint16_t* po = reinterpret_cast<uint16_t*>(ps) + row * D + 4 * half;
+    uint16_t* sp = st + l32 * kOutStageRow + 4 * half;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      *reinterpret_cast<uint2*>(po + 8 * j) =
+      *reinterpret_cast<uint2*>(sp + 8 * j) =
           to_bf16x4(sm.o0[4 * j] * inv, sm.o0[4 * j + 1] * inv, sm.o0[4 * j + 2] * inv, sm.o0[4 * j + 3] * inv);
-      *reinterpret_cast<uint2*>(po + 32 + 8 * j) =
+      *reinterpret_cast<uint2*>(sp + 32 + 8 * j) =
           to_bf16x4(sm.o1[4 * j] * inv, sm.o1[4 * j + 1] * inv, sm.o1[4 * j + 2] * inv, sm.o1[4 * j + 3] * inv);
     }
-    if (half == 0) {
-      ps[kSlotStatsFloat + row] = sm.m;
-      ps[kSlotStatsFloat + BQ + row] = l_tot;
+  }
+  __syncthreads();
+  const int r8 = lane >> 3, c8 = (lane & 7) * 8;
+  if (t0 == 0 && t1 == a.T) {
+    // the whole unit in this chunk: final output rows and LSE
+    if (wave_active) {
+      if (half == 0 && qi < a.n_tokens) a.lse[(int64_t)h * a.n_tokens + qi] = (sm.m + __log2f(l_tot)) * kLn2;
+#pragma unroll
+      for (int pass = 0; pass < 4; ++pass) {
+        const int r = pass * 8 + r8, qr = q0 + r;
+        if (qr < a.n_tokens)
+          *reinterpret_cast<uint4*>(a.out + ((int64_t)qr * a.n_heads + h) * D + c8) =
+              *reinterpret_cast<const uint4*>(st + r * kOutStageRow + c8);
+      }
+    }
+  } else {
+    // partial result, merged by the second launch: the normalised output rows in bf16
+    // (the merge weights them by 2^(m - M) l), then m and l in fp32
+    const int seg = chunk_start(a, c) >= (int64_t)ui * a.U ? 0 : 1;
+    float* ps = a.part + (int64_t)(2 * (a.chunk_base[q] + c) + seg) * kAttnSlotFloats;
+    if (wave_active) {
+      if (half == 0) {
+        const int row = wave * 32 + l32;
+        ps[kSlotStatsFloat + row] = sm.m;
+        ps[kSlotStatsFloat + BQ + row] = l_tot;
+      }
+      uint16_t* po = reinterpret_cast<uint16_t*>(ps) + wave * 32 * D;
+#pragma unroll
+      for (int pass = 0; pass < 4; ++pass) {
+        const int r = pass * 8 + r8;
+        *reinterpret_cast<uint4*>(po + r * D + c8) = *reinterpret_cast<const uint4*>(st + r * kOutStageRow + c8);
+      }
     }
   }
+  __syncthreads();  // (the ring is the next segment's)
 }
 
 // Requests a field from every 64-byte line of the argument block at once: the reads that
