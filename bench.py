@@ -50,6 +50,7 @@ KERNEL_SOURCES = {"attn_fwd_kernel": ("attend.hip",) + _HOST,
                   "select_kernel": ("admit.hip",) + _HOST}
 ADMISSION_KERNELS = ("sal_kernel", "select_kernel")  # one launch each per frame
 COPY_CALIBRATION_BYTES = 256 << 20   # read and written once by the calibration copy
+WARMUP_MIN_S = 0.1                   # least wall time of warm-up frames (when --warmup > 0)
 
 
 def log(*a):
@@ -148,24 +149,60 @@ def bench_args():
     return " ".join(out)
 
 
-def summarize_pmc(fetch_dir, write_dir, workload):
+def timed_start(dispatches, steps, layers):
+    """Start timestamp of the timed frames in a profiled benchmark run, from its dispatches
+    [(kernel name, start timestamp)]: the first of the last steps x layers attention
+    launches (a frame-staging launch before it in the frame counts too).  Earlier
+    dispatches are the input generation and the warm-up frames.  None (keep everything)
+    when steps or layers is not given or the run has fewer launches."""
+    if not steps or not layers:
+        return None
+    attn = sorted(t for n, t in dispatches if "attn_fwd_kernel" in n)
+    if len(attn) < steps * layers:
+        return None
+    t0 = attn[-steps * layers]
+    stage = sorted(t for n, t in dispatches if "stage_layers_kernel" in n)
+    if len(stage) >= steps:
+        t0 = min(t0, stage[-steps])
+    return t0
+
+
+def counter_rows(d):
+    """Rows of every *counter_collection.csv under d."""
+    import csv
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        rows.extend(csv.DictReader(open(f)))
+    return rows
+
+
+def timed_counter_rows(rows, steps, layers):
+    """The counter rows of the timed frames' dispatches (all rows when that is unknown)."""
+    first = {}
+    for r in rows:
+        first.setdefault(r["Dispatch_Id"], (r["Kernel_Name"], int(r["Start_Timestamp"])))
+    t0 = timed_start(list(first.values()), steps, layers)
+    return rows if t0 is None else [r for r in rows if int(r["Start_Timestamp"]) >= t0]
+
+
+def summarize_pmc(fetch_dir, write_dir, workload, steps=None, layers=None):
     """Reduce two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; counter CSVs) of this
-    benchmark started with --copy-calibration into per-launch HBM traffic.  The
+    benchmark started with --copy-calibration into per-launch HBM traffic of the timed
+    frames' dispatches (timed_start; all dispatches when steps or layers is None).  The
     calibration copy reads and writes COPY_CALIBRATION_BYTES once; the counters'
     readings for it give the factors that turn KiB per dispatch into bytes."""
-    import csv
 
-    def per_kernel(d, counter):
+    def per_kernel(rows, counter):
         out = {}
-        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
-            for r in csv.DictReader(open(f)):
-                if r["Counter_Name"] != counter:
-                    continue
-                name = r["Kernel_Name"]
-                out.setdefault(name, []).append(float(r["Counter_Value"]))
+        for r in rows:
+            if r["Counter_Name"] == counter:
+                out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
         return out
 
-    fetch, write = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+    f_rows, w_rows = counter_rows(fetch_dir), counter_rows(write_dir)
+    fetch_all, write_all = per_kernel(f_rows, "FETCH_SIZE"), per_kernel(w_rows, "WRITE_SIZE")
+    fetch = per_kernel(timed_counter_rows(f_rows, steps, layers), "FETCH_SIZE")
+    write = per_kernel(timed_counter_rows(w_rows, steps, layers), "WRITE_SIZE")
 
     def find(d, key):
         hits = [v for k, v in d.items() if key in k]
@@ -174,8 +211,8 @@ def summarize_pmc(fetch_dir, write_dir, workload):
         return hits[0]
 
     copy_key = "neg_kernel"
-    cf = max(find(fetch, copy_key))
-    cw = max(find(write, copy_key))
+    cf = max(find(fetch_all, copy_key))
+    cw = max(find(write_all, copy_key))
     f_scale = COPY_CALIBRATION_BYTES / (cf * 1024.0)
     w_scale = COPY_CALIBRATION_BYTES / (cw * 1024.0)
     for kernel in KERNEL_SOURCES:
@@ -197,7 +234,8 @@ def summarize_pmc(fetch_dir, write_dir, workload):
             f"python /root/repo/bench.py {bench_args()} --pmc-summary <out>/fetch <out>/write",
             "```",
             "",
-            f"- dispatches: {len(fv)} (FETCH_SIZE pass), {len(wv)} (WRITE_SIZE pass)",
+            f"- dispatches: {len(fv)} (FETCH_SIZE pass), {len(wv)} (WRITE_SIZE pass)"
+            + (", those of the timed frames" if steps and layers else ""),
             f"- fetch_kib_per_dispatch_mean: {f_kib:.1f}",
             f"- write_kib_per_dispatch_mean: {w_kib:.1f}",
             f"- copy_fetch_kib: {cf:.1f} (for {COPY_CALIBRATION_BYTES} bytes read)",
@@ -233,23 +271,22 @@ def mfma_path(workload):
 
 def summarize_mfma(dir_a, dir_b, dir_c, bench_json, workload):
     """Reduce three rocprofv3 --pmc runs of this benchmark (the counters of MFMA_PASSES) into
-    per-dispatch matrix-core, vector-ALU and wave-state activity of each kernel, and tie the
-    attention kernel's to the benchmark line of the same command (bench_json)."""
-    import csv
+    per-dispatch matrix-core, vector-ALU and wave-state activity of each kernel over the
+    timed frames' dispatches, and tie the attention kernel's to the benchmark line of the
+    same command (bench_json)."""
+    bench = json.loads(open(bench_json).read().strip().splitlines()[-1])
 
     def per_kernel(d):
         out = {}
-        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
-            for r in csv.DictReader(open(f)):
-                name = r["Kernel_Name"].replace("rv::(anonymous namespace)::", "").split("(")[0]
-                out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
-                if r["Counter_Name"] == "GRBM_GUI_ACTIVE":
-                    out[name].setdefault("duration_ns", []).append(
-                        float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+        for r in timed_counter_rows(counter_rows(d), bench["steps"], bench["config"].get("layers")):
+            name = r["Kernel_Name"].replace("rv::(anonymous namespace)::", "").split("(")[0]
+            out.setdefault(name, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            if r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+                out[name].setdefault("duration_ns", []).append(
+                    float(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
         return out
 
     a, b, w = per_kernel(dir_a), per_kernel(dir_b), per_kernel(dir_c)
-    bench = json.loads(open(bench_json).read().strip().splitlines()[-1])
     mean = lambda v: sum(v) / len(v)
     lines = [f"# Matrix-core and vector-ALU activity per dispatch, {workload}", "",
              "Three counter passes over the benchmark command (one run each, the program after `--`):", "",
@@ -331,21 +368,32 @@ def summarize_mfma(dir_a, dir_b, dir_c, bench_json, workload):
 
 def summarize_trace(trace_dir, bench_json, workload):
     """Write profiles/kernel_trace__<workload>.md from a rocprofv3 --kernel-trace --stats
-    run of this benchmark (its *_kernel_stats.csv) and the JSON line that run printed."""
+    run of this benchmark (its *_kernel_trace.csv, the timed frames' dispatches: see
+    timed_start) and the JSON line that run printed."""
     import csv
-    stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
-    if not stats:
-        raise SystemExit(f"no kernel_stats.csv under {trace_dir}")
-    rows = list(csv.DictReader(open(stats[0])))
+    traces = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if not traces:
+        raise SystemExit(f"no kernel_trace.csv under {trace_dir}")
     bench = json.loads(open(bench_json).read().strip().splitlines()[-1])
 
     def short(name):
         name = name.replace("rv::(anonymous namespace)::", "").replace("(anonymous namespace)::", "")
         return name.split("(")[0]
 
-    avg = {short(r["Name"]): float(r["AverageNs"]) / 1e3 for r in rows}
-    total = {short(r["Name"]): float(r["TotalDurationNs"]) / 1e3 for r in rows}
-    calls = {short(r["Name"]): int(r["Calls"]) for r in rows}
+    disp = [(r["Kernel_Name"], int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+            for r in csv.DictReader(open(traces[0]))]
+    t0 = timed_start([(n, t) for n, t, _ in disp], bench["steps"], bench["config"].get("layers"))
+    durs = {}
+    for n, t, e in disp:
+        if t0 is None or t >= t0:
+            durs.setdefault(short(n), []).append(e - t)
+    grand = sum(sum(v) for v in durs.values()) or 1
+    rows = sorted(({"Name": k, "Calls": len(v), "TotalDurationNs": sum(v), "AverageNs": sum(v) / len(v),
+                    "Percentage": 100.0 * sum(v) / grand, "MinNs": min(v), "MaxNs": max(v)}
+                   for k, v in durs.items()), key=lambda r: -r["TotalDurationNs"])
+    avg = {r["Name"]: r["AverageNs"] / 1e3 for r in rows}
+    total = {r["Name"]: r["TotalDurationNs"] / 1e3 for r in rows}
+    calls = {r["Name"]: r["Calls"] for r in rows}
     # One attention step = attn_fwd_kernel, plus attn_merge_kernel for a split plan.
     attn_step = ((total.get("attn_fwd_kernel", 0.0) + total.get("attn_merge_kernel", 0.0))
                  / max(calls.get("attn_fwd_kernel", 1), 1))
@@ -355,12 +403,13 @@ def summarize_trace(trace_dir, bench_json, workload):
              "rocprofv3 --kernel-trace --stats --output-format csv -d <out>/trace -o bench -- \\",
              f"    python /root/repo/bench.py {bench_args()} --no-cpu-baseline > <out>/trace.json",
              f"python /root/repo/bench.py {bench_args()} --trace-summary <out>/trace <out>/trace.json", "```", "",
-             "Kernel statistics (durations in ns; counts include the warm-up frames; the input",
-             "generator kernels run before the timed region):", "",
+             "Kernel statistics of the timed frames' dispatches (durations in ns, from the trace:",
+             "everything from the first of the timed frames' attention launches on; the input",
+             "generation and the warm-up frames before it are left out):", "",
              "| Kernel | Calls | Total ns | Average ns | % | Min ns | Max ns |", "|---|---|---|---|---|---|---|"]
     for r in rows:
-        lines.append(f"| `{short(r['Name'])}` | {r['Calls']} | {int(float(r['TotalDurationNs']))} | "
-                     f"{float(r['AverageNs']):.0f} | {float(r['Percentage']):.2f} | {r['MinNs']} | {r['MaxNs']} |")
+        lines.append(f"| `{r['Name']}` | {r['Calls']} | {int(r['TotalDurationNs'])} | "
+                     f"{r['AverageNs']:.0f} | {r['Percentage']:.2f} | {r['MinNs']} | {r['MaxNs']} |")
     adm = sum(avg.get(k, 0.0) for k in ADMISSION_KERNELS)
     lines += ["", "The same run's benchmark line (HIP events on the compute stream):", "",
               f"- frames/s: {bench['value']:.1f}",
@@ -787,7 +836,7 @@ def main():
         summarize_trace(*args.trace_summary, wkey or cfg.name)
         return
     if args.pmc_summary:
-        summarize_pmc(*args.pmc_summary, wkey or cfg.name)
+        summarize_pmc(*args.pmc_summary, wkey or cfg.name, steps=K_steps, layers=cfg.n_layers)
         return
     if args.mfma_summary:
         summarize_mfma(*args.mfma_summary, wkey or cfg.name)
@@ -818,14 +867,12 @@ def main():
     # Frames: the whole stream in order from its initial memory, or a stratified sample
     # of it taken longest memory first, each layer's memory cut back (rv_mem_truncate,
     # host-side only) to the length the frame has in the stream, so the timed frames run
-    # back to back.
+    # back to back.  The W warm-up frames repeat the first timed frame (below).
     if full:
         timed = list(range(n_stream))
-        warm = list(range(min(W, n_stream)))
     else:
         timed = sorted(stratified(n_stream, K_steps), reverse=True)
-        warm = sorted(stratified(n_stream, W), reverse=True) if W > 0 else []
-    frame_ids = sorted(set(timed) | set(warm))
+    frame_ids = sorted(set(timed))
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -973,17 +1020,27 @@ def main():
             raise rv.RVError(st, lib.rv_last_error().decode())
 
     # ---- warm-up, then the timed frames --------------------------------------------
+    # Warm-up: runs of the first timed frame on the memories it starts from, each
+    # followed by cutting every memory back to that start (host-side), so that the timed
+    # frames follow warm-up work on the same data: W of them, and (W > 0) as many more as
+    # fill WARMUP_MIN_S of wall time.  The device reaches its sustained speed only after
+    # some tens of milliseconds under load: after 5 warm-up frames (≈ 6 ms) a 20-frame
+    # sample ran 3 % slower than the same frames inside the whole stream, after 50 or
+    # more as fast.  (Warming up on other frames and then refilling the memories, as
+    # before, also left the device idle just before timing.)
     initial = (lambda l: mem_len(l, 0)) if full else (lambda l: rows_max[l])
     fill_memories(initial)
-    for t in warm:
-        run_frame(t)
-    torch.cuda.synchronize()
-    # the stream starts again from its initial memory (a stratified run's warm-up frames
-    # cut the memories back, and cutting back is the only length change between frames)
-    fill_memories(initial)
-
+    start_len = [m.len for m in mems]
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in timed]
     end_event = torch.cuda.Event(enable_timing=True)
+    warm_runs, t_warm = 0, time.perf_counter()
+    while warm_runs < W or (W > 0 and time.perf_counter() - t_warm < WARMUP_MIN_S):
+        run_frame(timed[0])
+        for l, m in enumerate(mems):
+            m.truncate(start_len[l])
+        warm_runs += 1
+        if warm_runs % 10 == 0:  # (so that the wall clock follows the device)
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i, t in enumerate(timed):
@@ -1041,7 +1098,7 @@ def main():
         "unit": "frames/s",
         "n_gpus": 1,
         "steps": n_timed,
-        "warmup": W,
+        "warmup": W, "warmup_frames_run": warm_runs,
         "ms_per_step": elapsed / n_timed * 1e3,
         "higher_is_better": True,
         "scaling": "weak",

@@ -149,3 +149,24 @@ def test_summary_commands_quote_the_benchmark_arguments_only(monkeypatch):
     monkeypatch.setattr(sys, "argv", ["bench.py", "--trace-summary", "d", "t.json", "--staged", "--pmc-summary",
                                       "f", "w"])
     assert bench.bench_args() == "--staged"
+
+
+def test_profile_summaries_keep_the_timed_frames_dispatches():
+    """Generator and warm-up dispatches precede the timed frames: the window starts at the
+    first of the last steps x layers attention launches (or the frame-staging launch
+    before it), and without steps and layers nothing is left out."""
+    d = [("gen_qkv_kernel", 1), ("attn_fwd_kernel", 10), ("attn_merge_kernel", 11), ("attn_fwd_kernel", 12),
+         ("sal_kernel", 13), ("select_kernel", 14),                                  # warm-up frame
+         ("attn_fwd_kernel", 20), ("attn_fwd_kernel", 22), ("attn_merge_kernel", 23), ("sal_kernel", 24),
+         ("select_kernel", 25), ("attn_fwd_kernel", 30), ("attn_fwd_kernel", 32), ("sal_kernel", 34),
+         ("select_kernel", 35)]                                                      # two timed frames
+    assert bench.timed_start(d, 2, 2) == 20
+    assert bench.timed_start(d, None, 2) is None and bench.timed_start(d, 9, 2) is None
+    staged = [("stage_layers_kernel", 5)] + d[:6] + [("stage_layers_kernel", 19)] + d[6:11] + \
+             [("stage_layers_kernel", 29)] + d[11:]
+    assert bench.timed_start(staged, 2, 2) == 19
+    rows = [{"Dispatch_Id": str(i), "Kernel_Name": n, "Start_Timestamp": str(t), "Counter_Name": c}
+            for i, (n, t) in enumerate(d) for c in ("FETCH_SIZE", "WRITE_SIZE")]
+    kept = bench.timed_counter_rows(rows, 2, 2)
+    assert len(kept) == 2 * 9 and min(int(r["Start_Timestamp"]) for r in kept) == 20
+    assert bench.timed_counter_rows(rows, None, None) == rows
