@@ -92,20 +92,21 @@ def test_attend_and_saliency_match_oracle(rv, N, H, M, sigma):
 
 
 PLANS = [  # (workgroups per CU, minimum chunk, split: -1 auto, 0 stream-K, k > 0 k-way,
-           #  per cent of a later stream-K chunk's tiles given to a first-dispatched one)
+           #  per cent of a later stream-K chunk's tiles given to a first-dispatched one;
+           #  "" the default: the unit-aligned share where one exists, as at 1041 x 16, M = 3000)
     ("1", "1", "0", "140"), ("2", "2", "0", "140"), ("4", "1", "0", "140"), ("1", "100000", "0", "140"),
     ("2", "2", "-1", "140"), ("1", "1", "1", "140"), ("2", "1", "7", "140"), ("2", "1", "64", "140"),
     ("4", "3", "-1", "140"), ("2", "1", "0", "100"), ("2", "1", "0", "101"), ("2", "2", "0", "400"),
-    ("4", "1", "0", "250"),
+    ("4", "1", "0", "250"), ("2", "2", "0", ""), ("2", "2", "-1", ""),
 ]
 
 
 @pytest.mark.parametrize("wg_per_cu,min_chunk,split,first_pct", PLANS)
 def test_work_plans_agree_with_oracle(rv, wg_per_cu, min_chunk, split, first_pct, monkeypatch):
     """Work plans (stream-K chunks of one key tile, of a few, whole units, with the
-    first-dispatched chunks as long as the others or longer; aligned k-way splits with
-    k = 1, several, more pieces than tiles) change only the rounding order of the
-    partial merges."""
+    first-dispatched chunks as long as the others or longer, or the unit-aligned form;
+    aligned k-way splits with k = 1, several, more pieces than tiles) change only the
+    rounding order of the partial merges."""
     monkeypatch.setenv("RV_ATTN_WG_PER_CU", wg_per_cu)
     monkeypatch.setenv("RV_ATTN_MIN_CHUNK", min_chunk)
     monkeypatch.setenv("RV_ATTN_SPLIT", split)
